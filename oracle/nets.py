@@ -1,0 +1,179 @@
+"""Network definitions for the oracle (test infrastructure only).
+
+Five synthetic workloads, written independently of the product library's own
+definitions.  A network is a list of operations in forward order; tensor 0 is
+the input batch and tensor i+1 is the output of operation i.
+
+Each operation carries the planner layer it belongs to.  Following the layer
+decomposition of Sec. III-A, one layer is one weighted operation (conv or FC)
+together with the parameter-less operations that follow it (ReLU, pooling,
+flatten, residual add, global average pooling); BatchNorm's scale and shift
+belong to the convolution they normalise, and branches at the same depth form
+one layer, so a residual block's 1x1 projection joins the layer of the block's
+first convolution.
+
+Parameter-server order: layers in order, and within a layer the operations in
+forward order, each contributing conv/FC weight then bias, or BN gamma then
+beta.  Conv weights are KRSC, FC weights [out][in] over the NHWC-flattened
+input.
+"""
+from __future__ import annotations
+
+
+def _op(kind, inp, layer, **kw):
+    d = {"op": kind, "in": inp, "layer": layer}
+    d.update(kw)
+    return d
+
+
+class _Builder:
+    def __init__(self):
+        self.ops = []
+        self.layer = 0
+
+    def new_layer(self):
+        self.layer += 1
+
+    def add(self, kind, inp, **kw):
+        self.ops.append(_op(kind, inp, self.layer, **kw))
+        return len(self.ops)  # tensor id of the output
+
+    def conv(self, inp, k, r, stride=1, pad=0, bias=True):
+        return self.add("conv", inp, k=k, r=r, s=r, stride=stride, pad=pad, bias=bias)
+
+    def fc(self, inp, out, bias=True):
+        return self.add("fc", inp, out=out, bias=bias)
+
+
+def tiny():
+    """Tiny CNN: conv3x3(3->8)+ReLU+maxpool2, conv3x3(8->16)+ReLU+maxpool2, FC(1024->64)+ReLU, FC(64->10)."""
+    b = _Builder()
+    t = 0
+    for k in (8, 16):
+        b.new_layer()
+        t = b.conv(t, k, 3, pad=1)
+        t = b.add("relu", t)
+        t = b.add("maxpool", t, r=2, s=2, stride=2, pad=0)
+    b.new_layer()
+    t = b.fc(t, 64)
+    t = b.add("relu", t)
+    b.new_layer()
+    b.fc(t, 10)
+    return {"name": "tiny", "ops": b.ops, "hwc": (32, 32, 3), "classes": 10}
+
+
+def alexnet():
+    """AlexNet-style 8-layer CNN (no LRN, no dropout; paddings 2, 2, 1, 1, 1)."""
+    b = _Builder()
+    t = 0
+    spec = [(64, 11, 4, 2, True), (192, 5, 1, 2, True), (384, 3, 1, 1, False),
+            (256, 3, 1, 1, False), (256, 3, 1, 1, True)]
+    for k, r, st, pad, pool in spec:
+        b.new_layer()
+        t = b.conv(t, k, r, stride=st, pad=pad)
+        t = b.add("relu", t)
+        if pool:
+            t = b.add("maxpool", t, r=3, s=3, stride=2, pad=0)
+    for out, relu in ((4096, True), (4096, True), (1000, False)):
+        b.new_layer()
+        t = b.fc(t, out)
+        if relu:
+            t = b.add("relu", t)
+    return {"name": "alexnet", "ops": b.ops, "hwc": (224, 224, 3), "classes": 1000}
+
+
+def vgg16():
+    """VGG-16: 13 conv3x3 pad 1 with ReLU, five 2x2 max-pools, FC 25088->4096->4096->1000."""
+    b = _Builder()
+    t = 0
+    cfg = [64, 64, "M", 128, 128, "M", 256, 256, 256, "M", 512, 512, 512, "M", 512, 512, 512, "M"]
+    for v in cfg:
+        if v == "M":
+            t = b.add("maxpool", t, r=2, s=2, stride=2, pad=0)
+        else:
+            b.new_layer()
+            t = b.conv(t, v, 3, pad=1)
+            t = b.add("relu", t)
+    for out, relu in ((4096, True), (4096, True), (1000, False)):
+        b.new_layer()
+        t = b.fc(t, out)
+        if relu:
+            t = b.add("relu", t)
+    return {"name": "vgg16", "ops": b.ops, "hwc": (224, 224, 3), "classes": 1000}
+
+
+def resnet18_small():
+    """ResNet-18 for 32x32 inputs: 3x3 stem, 4 stages of 2 basic blocks, global avg-pool, FC 512->10."""
+    b = _Builder()
+    b.new_layer()
+    t = b.conv(0, 64, 3, pad=1, bias=False)
+    t = b.add("bn", t)
+    t = b.add("relu", t)
+    cin = 64
+    for cout, first_stride in ((64, 1), (128, 2), (256, 2), (512, 2)):
+        for blk in range(2):
+            st = first_stride if blk == 0 else 1
+            x = t
+            b.new_layer()
+            u = b.conv(x, cout, 3, stride=st, pad=1, bias=False)
+            u = b.add("bn", u)
+            u = b.add("relu", u)
+            short = x
+            if st != 1 or cin != cout:
+                short = b.conv(x, cout, 1, stride=st, pad=0, bias=False)
+                short = b.add("bn", short)
+            b.new_layer()
+            u = b.conv(u, cout, 3, pad=1, bias=False)
+            u = b.add("bn", u)
+            u = b.add("add", u, other=short)
+            t = b.add("relu", u)
+            cin = cout
+    t = b.add("gap", t)
+    b.new_layer()
+    b.fc(t, 10)
+    return {"name": "resnet18", "ops": b.ops, "hwc": (32, 32, 3), "classes": 10}
+
+
+def resnet50():
+    """ResNet-50 (stride on the 3x3 conv of a bottleneck, projection in each stage's first block)."""
+    b = _Builder()
+    b.new_layer()
+    t = b.conv(0, 64, 7, stride=2, pad=3, bias=False)
+    t = b.add("bn", t)
+    t = b.add("relu", t)
+    t = b.add("maxpool", t, r=3, s=3, stride=2, pad=1)
+    cin = 64
+    for width, blocks, first_stride in ((64, 3, 1), (128, 4, 2), (256, 6, 2), (512, 3, 2)):
+        cout = 4 * width
+        for blk in range(blocks):
+            st = first_stride if blk == 0 else 1
+            x = t
+            b.new_layer()
+            u = b.conv(x, width, 1, bias=False)
+            u = b.add("bn", u)
+            u = b.add("relu", u)
+            short = x
+            if blk == 0:
+                short = b.conv(x, cout, 1, stride=st, pad=0, bias=False)
+                short = b.add("bn", short)
+            b.new_layer()
+            u = b.conv(u, width, 3, stride=st, pad=1, bias=False)
+            u = b.add("bn", u)
+            u = b.add("relu", u)
+            b.new_layer()
+            u = b.conv(u, cout, 1, bias=False)
+            u = b.add("bn", u)
+            u = b.add("add", u, other=short)
+            t = b.add("relu", u)
+            cin = cout
+    t = b.add("gap", t)
+    b.new_layer()
+    b.fc(t, 1000)
+    return {"name": "resnet50", "ops": b.ops, "hwc": (224, 224, 3), "classes": 1000}
+
+
+NETS = {"tiny": tiny, "alexnet": alexnet, "resnet18": resnet18_small, "vgg16": vgg16, "resnet50": resnet50}
+
+
+def get(name):
+    return NETS[name]()

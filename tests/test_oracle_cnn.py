@@ -1,0 +1,260 @@
+"""Pins for the oracle CNN iteration.
+
+* Forward operators against torch's CPU float64 library routines (conv2d with
+  stride and padding, max_pool2d with padding, batch_norm in training mode,
+  adaptive average pooling) - special cases that reduce to a library routine.
+* Backward operators against torch autograd in float64 on the same inputs.
+* Whole-network gradients against central finite differences in float64, on
+  the tiny workload and on a small residual network that has every operator
+  (BN, stride-2 conv, 1x1 projection, residual add, padded 3x3/2 max-pool,
+  global average pooling).
+* Closed forms: with the last FC zeroed the loss is exactly ln(classes) and
+  the last bias gradient is (1/classes - onehot) averaged over the batch; the
+  server update is w - 0.01 g.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle import cnn, nets
+
+
+def _nchw(a):
+    return torch.from_numpy(np.ascontiguousarray(a.transpose(0, 3, 1, 2)))
+
+
+def _nhwc(t):
+    return t.detach().numpy().transpose(0, 2, 3, 1)
+
+
+@pytest.mark.parametrize("shape", [
+    # N, H, W, C, K, R, stride, pad
+    (2, 9, 7, 3, 5, 3, 1, 1),
+    (2, 11, 11, 4, 6, 3, 2, 1),
+    (1, 23, 23, 3, 4, 11, 4, 2),
+    (3, 8, 8, 6, 7, 1, 2, 0),
+    (2, 14, 14, 3, 8, 7, 2, 3),
+    (2, 6, 6, 5, 3, 5, 1, 2),
+])
+def test_conv_against_torch(shape):
+    N, H, W, C, K, R, st, pad = shape
+    x = synth.random_tensor(1, (N, H, W, C)).astype(np.float64)
+    w = synth.random_tensor(2, (K, R, R, C)).astype(np.float64)
+    b = synth.random_tensor(3, (K,)).astype(np.float64)
+    y = cnn.conv2d_forward(x, w, b, st, pad)
+    xt = _nchw(x).requires_grad_(True)
+    wt = torch.from_numpy(np.ascontiguousarray(w.transpose(0, 3, 1, 2))).requires_grad_(True)
+    yt = torch.nn.functional.conv2d(xt, wt, torch.from_numpy(b), stride=st, padding=pad)
+    np.testing.assert_allclose(y, _nhwc(yt), rtol=1e-12, atol=1e-12)
+    dy = synth.random_tensor(4, y.shape).astype(np.float64)
+    yt.backward(_nchw(dy))
+    dx = cnn.conv2d_backward_data(dy, w, (H, W), st, pad)
+    dw = cnn.conv2d_backward_filter(x, dy, (R, R), st, pad)
+    np.testing.assert_allclose(dx, _nhwc(xt.grad), rtol=1e-11, atol=1e-11)
+    np.testing.assert_allclose(dw, wt.grad.numpy().transpose(0, 2, 3, 1), rtol=1e-11, atol=1e-11)
+
+
+@pytest.mark.parametrize("cfg", [(2, 2, 0, 8), (3, 2, 0, 13), (3, 2, 1, 12), (3, 2, 0, 55)])
+def test_maxpool_against_torch(cfg):
+    r, st, pad, H = cfg
+    x = synth.random_tensor(5, (2, H, H, 3)).astype(np.float64)
+    y, arg = cnn.maxpool_forward(x, r, r, st, pad)
+    xt = _nchw(x).requires_grad_(True)
+    yt = torch.nn.functional.max_pool2d(xt, r, st, pad)
+    np.testing.assert_array_equal(y, _nhwc(yt))
+    dy = synth.random_tensor(6, y.shape).astype(np.float64)
+    yt.backward(_nchw(dy))
+    dx = cnn.maxpool_backward(dy, arg, x.shape, r, r, st, pad)
+    np.testing.assert_allclose(dx, _nhwc(xt.grad), rtol=1e-13, atol=1e-13)
+
+
+def test_maxpool_ties_pick_first():
+    x = np.zeros((1, 4, 4, 1))
+    x[0, 1, 1, 0] = 0.0
+    y, arg = cnn.maxpool_forward(x, 2, 2, 2, 0)
+    assert (arg == 0).all()
+    # values that only differ below float32 resolution count as a tie
+    x = np.zeros((1, 2, 2, 1))
+    x[0, 0, 1, 0] = 1e-60
+    y, arg = cnn.maxpool_forward(x, 2, 2, 2, 0)
+    assert arg[0, 0, 0, 0] == 0
+
+
+def test_batchnorm_against_torch():
+    x = (synth.random_tensor(7, (3, 5, 4, 6)) * 3 + 1).astype(np.float64)
+    gamma = synth.random_tensor(8, (6,)).astype(np.float64)
+    beta = synth.random_tensor(9, (6,)).astype(np.float64)
+    y, xhat, invstd = cnn.batchnorm_forward(x, gamma, beta)
+    xt = _nchw(x).requires_grad_(True)
+    gt = torch.from_numpy(gamma).requires_grad_(True)
+    bt = torch.from_numpy(beta).requires_grad_(True)
+    yt = torch.nn.functional.batch_norm(xt, None, None, gt, bt, training=True, eps=cnn.BN_EPS)
+    np.testing.assert_allclose(y, _nhwc(yt), rtol=1e-12, atol=1e-12)
+    dy = synth.random_tensor(10, y.shape).astype(np.float64)
+    yt.backward(_nchw(dy))
+    dx, dg, db = cnn.batchnorm_backward(dy, xhat, invstd, gamma)
+    np.testing.assert_allclose(dx, _nhwc(xt.grad), rtol=1e-10, atol=1e-12)
+    np.testing.assert_allclose(dg, gt.grad.numpy(), rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(db, bt.grad.numpy(), rtol=1e-12, atol=1e-12)
+
+
+def test_softmax_xent_against_torch():
+    z = synth.random_tensor(11, (5, 7)).astype(np.float64) * 4
+    y = np.array([0, 6, 3, 3, 1])
+    loss, dz = cnn.softmax_xent(z, y)
+    zt = torch.from_numpy(z).requires_grad_(True)
+    lt = torch.nn.functional.cross_entropy(zt, torch.from_numpy(y))
+    lt.backward()
+    assert abs(loss - lt.item()) < 1e-13
+    np.testing.assert_allclose(dz, zt.grad.numpy(), rtol=1e-12, atol=1e-14)
+
+
+def _mini_resnet():
+    """Small network with every operator kind, for finite differences."""
+    ops = []
+
+    def add(kind, inp, layer, **kw):
+        d = {"op": kind, "in": inp, "layer": layer}
+        d.update(kw)
+        ops.append(d)
+        return len(ops)
+
+    t = add("conv", 0, 1, k=4, r=3, s=3, stride=1, pad=1, bias=False)
+    t = add("bn", t, 1)
+    t = add("relu", t, 1)
+    t = add("maxpool", t, 1, r=3, s=3, stride=2, pad=1)
+    x = t
+    u = add("conv", x, 2, k=6, r=3, s=3, stride=2, pad=1, bias=False)
+    u = add("bn", u, 2)
+    u = add("relu", u, 2)
+    sc = add("conv", x, 2, k=6, r=1, s=1, stride=2, pad=0, bias=False)
+    sc = add("bn", sc, 2)
+    u = add("conv", u, 3, k=6, r=3, s=3, stride=1, pad=1, bias=True)
+    u = add("bn", u, 3)
+    u = add("add", u, 3, other=sc)
+    u = add("relu", u, 3)
+    u = add("gap", u, 3)
+    add("fc", u, 4, out=5, bias=True)
+    return {"name": "mini", "ops": ops, "hwc": (10, 10, 3), "classes": 5}
+
+
+def _fd_check(spec, batch, seed, n_probe, rel):
+    net = cnn.Net(spec, batch)
+    x, y, p = synth.cnn_inputs(seed, batch, spec["hwc"], spec["classes"], net.param_specs)
+    p = p.astype(np.float64)
+    loss, g = net.loss_and_grads(x, y, p)
+    rng = np.random.default_rng(seed + 100)
+    idx = set(rng.choice(net.n_params, size=n_probe, replace=False).tolist())
+    for l in range(1, net.L + 1):   # probe every layer's first and last parameter too
+        lo, cnt = net.layer_ranges[l]
+        idx.update((lo, lo + cnt - 1))
+    gmax = np.abs(g).max()
+    for i in sorted(idx):
+        h = 1e-6 * max(1.0, abs(p[i]))
+        pp, pm = p.copy(), p.copy()
+        pp[i] += h
+        pm[i] -= h
+        fd = (net.loss(x, y, pp) - net.loss(x, y, pm)) / (2 * h)
+        assert abs(fd - g[i]) <= rel * gmax + 1e-7 * abs(g[i]), (i, fd, g[i])
+    return loss
+
+
+def test_finite_differences_tiny():
+    _fd_check(nets.tiny(), 2, 0, 60, 1e-6)
+
+
+def test_finite_differences_all_operators():
+    _fd_check(_mini_resnet(), 3, 1, 120, 1e-6)
+
+
+def test_zero_last_fc_gives_ln_classes():
+    spec = nets.tiny()
+    net = cnn.Net(spec, 4)
+    x, y, p = synth.cnn_inputs(0, 4, spec["hwc"], spec["classes"], net.param_specs)
+    lo, cnt = net.layer_ranges[net.L]
+    p = p.astype(np.float64)
+    p[lo:lo + cnt] = 0.0
+    loss, g = net.loss_and_grads(x, y, p)
+    assert loss == pytest.approx(math.log(10), abs=1e-15)
+    onehot = np.zeros((4, 10))
+    onehot[np.arange(4), y] = 1
+    db = (1.0 / 10 - onehot).mean(axis=0)
+    np.testing.assert_allclose(g[lo + cnt - 10:lo + cnt], db, rtol=0, atol=1e-15)
+
+
+def test_sgd_closed_form():
+    w = synth.random_tensor(12, (100,))
+    g = synth.random_tensor(13, (100,))
+    np.testing.assert_array_equal(cnn.sgd(w, g), w.astype(np.float64) - 0.01 * g.astype(np.float64))
+
+
+@pytest.mark.parametrize("name,count", [("tiny", 67642), ("alexnet", 61100840), ("resnet18", 11173962),
+                                        ("vgg16", 138357544), ("resnet50", 25557032)])
+def test_parameter_counts(name, count):
+    net = cnn.Net(nets.get(name), 1)
+    assert net.n_params == count
+    assert sum(c for _, c in net.layer_ranges.values()) == count
+    assert {"tiny": 4, "alexnet": 8, "resnet18": 18, "vgg16": 16, "resnet50": 50}[name] == net.L
+
+
+def _torch_loss(spec, net, x, y, p):
+    """The same network evaluated with torch float64 library routines (NCHW inside)."""
+    pt = torch.from_numpy(np.asarray(p, dtype=np.float64)).requires_grad_(True)
+
+    def prm(i, name):
+        off, shape = net.pslots[i][name]
+        return pt[off:off + int(np.prod(shape))].reshape(shape)
+
+    F = torch.nn.functional
+    t = [_nchw(np.asarray(x, dtype=np.float64))]
+    for i, op in enumerate(spec["ops"]):
+        a = t[op["in"]]
+        k = op["op"]
+        if k == "conv":
+            w = prm(i, "w").permute(0, 3, 1, 2)
+            b = prm(i, "b") if op["bias"] else None
+            o = F.conv2d(a, w, b, stride=op["stride"], padding=op["pad"])
+        elif k == "fc":
+            flat = a.permute(0, 2, 3, 1).reshape(a.shape[0], -1)   # NHWC flatten
+            o = F.linear(flat, prm(i, "w"), prm(i, "b") if op["bias"] else None)
+            o = o.reshape(a.shape[0], -1, 1, 1)
+        elif k == "bn":
+            o = F.batch_norm(a, None, None, prm(i, "gamma"), prm(i, "beta"), training=True, eps=cnn.BN_EPS)
+        elif k == "relu":
+            o = F.relu(a)
+        elif k == "maxpool":
+            o = F.max_pool2d(a, op["r"], op["stride"], op["pad"])
+        elif k == "gap":
+            o = F.adaptive_avg_pool2d(a, 1)
+        elif k == "add":
+            o = a + t[op["other"]]
+        t.append(o)
+    loss = F.cross_entropy(t[-1].reshape(net.batch, -1), torch.from_numpy(np.asarray(y, dtype=np.int64)))
+    loss.backward()
+    return loss.item(), pt.grad.numpy()
+
+
+@pytest.mark.parametrize("which", ["tiny", "mini"])
+def test_network_against_torch(which):
+    spec = nets.tiny() if which == "tiny" else _mini_resnet()
+    batch = 3
+    net = cnn.Net(spec, batch)
+    x, y, p = synth.cnn_inputs(3, batch, spec["hwc"], spec["classes"], net.param_specs)
+    loss, g = net.loss_and_grads(x, y, p)
+    lt, gt = _torch_loss(spec, net, x, y, p)
+    assert abs(loss - lt) <= 1e-12 * max(1.0, abs(lt))
+    np.testing.assert_allclose(g, gt, rtol=1e-9, atol=1e-12 * np.abs(gt).max())
+
+
+@pytest.mark.slow
+def test_resnet18_against_torch():
+    spec = nets.resnet18_small()
+    net = cnn.Net(spec, 2)
+    x, y, p = synth.cnn_inputs(2, 2, spec["hwc"], spec["classes"], net.param_specs)
+    loss, g = net.loss_and_grads(x, y, p)
+    lt, gt = _torch_loss(spec, net, x, y, p)
+    assert abs(loss - lt) <= 1e-11 * max(1.0, abs(lt))
+    np.testing.assert_allclose(g, gt, rtol=1e-8, atol=1e-11 * np.abs(gt).max())
