@@ -1,0 +1,103 @@
+/*
+ * libdc operator entry points: the gfx950 kernels that the executor runs for
+ * each forward and backward mini-procedure (Sec. III-A), callable one at a
+ * time.  Conventions (status codes, device pointers, void* streams, NHWC
+ * activations, KRSC filters) are those of dc.h.  Every call only enqueues
+ * work on `stream`; inputs and outputs are caller-owned device buffers.
+ * Where a call takes `ws`, it is caller-owned device scratch of at least the
+ * size its *_workspace_bytes() query returns (256-byte aligned); calls on one
+ * stream may share it.  `accumulate` = 1 adds the result into the output
+ * instead of overwriting it.  Shapes are validated on the host (DC_EINVAL);
+ * empty shapes (a zero dimension) are a no-op.
+ */
+#ifndef DC_KERNELS_H
+#define DC_KERNELS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Convolution geometry: input n x h x w x c, k filters of r x s x c, stride,
+ * zero padding.  Output p x q with p = (h + 2 pad - r) / stride + 1.  An FC
+ * layer of in -> out features is the case h = w = r = s = 1, c = in, k = out,
+ * stride = 1, pad = 0. */
+typedef struct dc_conv_shape {
+    int32_t n, h, w, c, k, r, s, stride, pad;
+} dc_conv_shape;
+
+/* Scratch needed by the three conv passes of this shape (split-K partials). */
+size_t dc_conv2d_workspace_bytes(const dc_conv_shape *sh);
+
+/* y[n,p,q,k] = bias[k] + sum over r, s, c of x[n, p*stride+r-pad, q*stride+s-pad, c] * w[k,r,s,c],
+ * then max(., 0) if relu; implicit GEMM on fp32 MFMA.  bias may be NULL. */
+int dc_conv2d_forward(const dc_conv_shape *sh, const float *x, const float *w, const float *bias,
+                      int relu, float *y, void *ws, size_t ws_bytes, void *stream);
+
+/* dx[n,h,w,c] (+)= sum over the (r, s, k) that reach (h, w) of dy[n,p,q,k] * w[k,r,s,c];
+ * strided convolutions are split into stride^2 phase GEMMs with only the taps that hit. */
+int dc_conv2d_backward_data(const dc_conv_shape *sh, const float *dy, const float *w,
+                            int accumulate, float *dx, void *ws, size_t ws_bytes, void *stream);
+
+/* dw[k,r,s,c] = sum over n, p, q of dy[n,p,q,k] * x[n, p*stride+r-pad, q*stride+s-pad, c];
+ * dbias[k] = sum over n, p, q of dy[n,p,q,k] if dbias != NULL.  Deterministic
+ * (fixed-order split-K). */
+int dc_conv2d_backward_filter(const dc_conv_shape *sh, const float *x, const float *dy,
+                              float *dw, float *dbias, void *ws, size_t ws_bytes, void *stream);
+
+/* y = max(x, 0) over n floats. */
+int dc_relu_forward(const float *x, float *y, int64_t n, void *stream);
+/* dx (+)= dy where y > 0, else 0 (relu'(0) = 0). */
+int dc_relu_backward(const float *dy, const float *y, int accumulate, float *dx, int64_t n,
+                     void *stream);
+
+/* Max-pooling geometry: input n x h x w x c, window r x s, stride, padding. */
+typedef struct dc_pool_shape {
+    int32_t n, h, w, c, r, s, stride, pad;
+} dc_pool_shape;
+
+/* y = window max; arg = r*s_win + s of the first maximum in row-major window order. */
+int dc_maxpool_forward(const dc_pool_shape *sh, const float *x, float *y, uint8_t *arg,
+                       void *stream);
+/* dx (+)= the sum of dy over the windows whose argmax is this element. */
+int dc_maxpool_backward(const dc_pool_shape *sh, const float *dy, const uint8_t *arg,
+                        int accumulate, float *dx, void *stream);
+
+/* Global average pooling: y[n,c] = mean over hw of x[n,hw,c]; backward spreads dy / hw. */
+int dc_gap_forward(int32_t n, int32_t hw, int32_t c, const float *x, float *y, void *stream);
+int dc_gap_backward(int32_t n, int32_t hw, int32_t c, const float *dy, int accumulate, float *dx,
+                    void *stream);
+
+/* y = a + b over n floats; relu = 1 gives max(a + b, 0). */
+int dc_add_forward(const float *a, const float *b, int relu, float *y, int64_t n, void *stream);
+/* dx (+)= dy over n floats. */
+int dc_copy_grad(const float *dy, int accumulate, float *dx, int64_t n, void *stream);
+
+/* BatchNorm over rows = n*h*w rows of c channels (NHWC viewed as [rows][c]). */
+size_t dc_batchnorm_workspace_bytes(int64_t rows, int32_t c);
+/* mean, invstd (c floats each, outputs) = batch statistics with the biased
+ * variance; y = gamma * (x - mean) * invstd + beta; invstd = 1/sqrt(var + eps). */
+int dc_batchnorm_forward(int64_t rows, int32_t c, const float *x, const float *gamma,
+                         const float *beta, float eps, float *y, float *mean, float *invstd,
+                         void *ws, size_t ws_bytes, void *stream);
+/* dgamma = sum dy*xhat, dbeta = sum dy,
+ * dx (+)= gamma*invstd*(dy - dbeta/rows - xhat*dgamma/rows), xhat = (x-mean)*invstd. */
+int dc_batchnorm_backward(int64_t rows, int32_t c, const float *dy, const float *x,
+                          const float *gamma, const float *mean, const float *invstd,
+                          int accumulate, float *dx, float *dgamma, float *dbeta, void *ws,
+                          size_t ws_bytes, void *stream);
+
+/* loss[0] = mean over n of (logsumexp(z_i) - z_i[y_i]); dz = (softmax(z) - onehot(y)) / n.
+ * logits n x classes; labels outside [0, classes) give DC_EINVAL only if
+ * checked by the caller: the kernel clamps nothing and treats them as no target. */
+size_t dc_softmax_xent_workspace_bytes(int32_t n);
+int dc_softmax_xent(int32_t n, int32_t classes, const float *logits, const int32_t *labels,
+                    float *loss, float *dlogits, void *ws, size_t ws_bytes, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DC_KERNELS_H */

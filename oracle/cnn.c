@@ -186,3 +186,86 @@ void or_maxpool_backward(int N, int H, int W, int C, int R, int S, int st, int p
                 }
     }
 }
+
+/* Sampled outputs of the three convolution sums, one at a time, for layers
+ * too large to evaluate whole.  Inputs are the float32 tensors themselves
+ * (every float32 is exact in double); each sample is accumulated in double in
+ * the order of its definition.  idx holds 4 indices per sample:
+ *   forward (n, p, q, k); data gradient (n, h, w, c); filter gradient (k, r, s, c). */
+void or_conv2d_forward_samples(int N, int H, int W, int C, int K, int R, int S, int st, int pad,
+                               int P, int Q, const float *x, const float *w, const float *b,
+                               int ns, const int *idx, double *out)
+{
+    (void)N;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int i = 0; i < ns; ++i) {
+        int n = idx[4 * i], p = idx[4 * i + 1], q = idx[4 * i + 2], k = idx[4 * i + 3];
+        double acc = b ? (double)b[k] : 0.0;
+        for (int r = 0; r < R; ++r) {
+            int h = p * st + r - pad;
+            if (h < 0 || h >= H)
+                continue;
+            for (int s = 0; s < S; ++s) {
+                int ww = q * st + s - pad;
+                if (ww < 0 || ww >= W)
+                    continue;
+                for (int c = 0; c < C; ++c)
+                    acc += (double)x[IDX4(n, h, ww, c, H, W, C)] * (double)w[IDX4(k, r, s, c, R, S, C)];
+            }
+        }
+        (void)P;
+        (void)Q;
+        out[i] = acc;
+    }
+}
+
+void or_conv2d_backward_data_samples(int N, int H, int W, int C, int K, int R, int S, int st, int pad,
+                                     int P, int Q, const float *dy, const float *w,
+                                     int ns, const int *idx, double *out)
+{
+    (void)N;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int i = 0; i < ns; ++i) {
+        int n = idx[4 * i], h = idx[4 * i + 1], ww = idx[4 * i + 2], c = idx[4 * i + 3];
+        double acc = 0.0;
+        for (int r = 0; r < R; ++r) {
+            int t = h + pad - r;
+            if (t < 0 || t % st != 0 || t / st >= P)
+                continue;
+            int p = t / st;
+            for (int s = 0; s < S; ++s) {
+                int u = ww + pad - s;
+                if (u < 0 || u % st != 0 || u / st >= Q)
+                    continue;
+                int q = u / st;
+                for (int k = 0; k < K; ++k)
+                    acc += (double)dy[IDX4(n, p, q, k, P, Q, K)] * (double)w[IDX4(k, r, s, c, R, S, C)];
+            }
+        }
+        out[i] = acc;
+    }
+}
+
+void or_conv2d_backward_filter_samples(int N, int H, int W, int C, int K, int R, int S, int st, int pad,
+                                       int P, int Q, const float *x, const float *dy,
+                                       int ns, const int *idx, double *out)
+{
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int i = 0; i < ns; ++i) {
+        int k = idx[4 * i], r = idx[4 * i + 1], s = idx[4 * i + 2], c = idx[4 * i + 3];
+        double acc = 0.0;
+        for (int n = 0; n < N; ++n)
+            for (int p = 0; p < P; ++p) {
+                int h = p * st + r - pad;
+                if (h < 0 || h >= H)
+                    continue;
+                for (int q = 0; q < Q; ++q) {
+                    int ww = q * st + s - pad;
+                    if (ww < 0 || ww >= W)
+                        continue;
+                    acc += (double)dy[IDX4(n, p, q, k, P, Q, K)] * (double)x[IDX4(n, h, ww, c, H, W, C)];
+                }
+            }
+        out[i] = acc;
+    }
+}

@@ -49,8 +49,13 @@ def lib():
         L.or_conv2d_backward_filter.argtypes = [i] * 11 + [dp, dp, dp]
         L.or_maxpool_forward.argtypes = [i] * 10 + [dp, dp, ip]
         L.or_maxpool_backward.argtypes = [i] * 10 + [dp, ip, dp]
+        fp = ctypes.POINTER(ctypes.c_float)
+        L.or_conv2d_forward_samples.argtypes = [i] * 11 + [fp, fp, fp, i, ip, dp]
+        L.or_conv2d_backward_data_samples.argtypes = [i] * 11 + [fp, fp, i, ip, dp]
+        L.or_conv2d_backward_filter_samples.argtypes = [i] * 11 + [fp, fp, i, ip, dp]
         for f in ("or_conv2d_forward", "or_conv2d_backward_data", "or_conv2d_backward_filter",
-                  "or_maxpool_forward", "or_maxpool_backward"):
+                  "or_maxpool_forward", "or_maxpool_backward", "or_conv2d_forward_samples",
+                  "or_conv2d_backward_data_samples", "or_conv2d_backward_filter_samples"):
             getattr(L, f).restype = None
         _lib = L
     return _lib
@@ -124,6 +129,37 @@ def maxpool_backward(dy, arg, in_shape, r, s, st, pad):
     lib().or_maxpool_backward(N, H, W, C, r, s, st, pad, P, Q, _dp(dy),
                               arg.ctypes.data_as(ctypes.POINTER(ctypes.c_int)), _dp(dx))
     return dx
+
+
+def _fp(a):
+    return a.ctypes.data_as(ctypes.POINTER(ctypes.c_float)) if a is not None else None
+
+
+def conv2d_samples(which, geom, a, b, idx, bias=None):
+    """Selected outputs of a conv pass, each from its definition, on float32 inputs.
+
+    geom = (N, H, W, C, K, R, S, stride, pad); which = "fwd" (a = x, b = w,
+    idx rows (n, p, q, k)), "dgrad" (a = dy, b = w, rows (n, h, w, c)) or
+    "wgrad" (a = x, b = dy, rows (k, r, s, c)).  Returns float64 values.
+    """
+    N, H, W, C, K, R, S, st, pad = geom
+    P, Q = conv_out(H, R, st, pad), conv_out(W, S, st, pad)
+    a = np.ascontiguousarray(a, dtype=np.float32)
+    b = np.ascontiguousarray(b, dtype=np.float32)
+    idx = np.ascontiguousarray(idx, dtype=np.int32).reshape(-1, 4)
+    out = np.empty(len(idx))
+    args = (N, H, W, C, K, R, S, st, pad, P, Q)
+    ip = idx.ctypes.data_as(ctypes.POINTER(ctypes.c_int))
+    if which == "fwd":
+        bb = None if bias is None else np.ascontiguousarray(bias, dtype=np.float32)
+        lib().or_conv2d_forward_samples(*args, _fp(a), _fp(b), _fp(bb), len(idx), ip, _dp(out))
+    elif which == "dgrad":
+        lib().or_conv2d_backward_data_samples(*args, _fp(a), _fp(b), len(idx), ip, _dp(out))
+    elif which == "wgrad":
+        lib().or_conv2d_backward_filter_samples(*args, _fp(a), _fp(b), len(idx), ip, _dp(out))
+    else:
+        raise ValueError(which)
+    return out
 
 
 def relu_mask(x):

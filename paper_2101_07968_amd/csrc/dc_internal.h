@@ -1,0 +1,103 @@
+// Internal declarations shared by the libdc sources (not part of the C ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+
+#include "dc.h"
+#include "dc_kernels.h"
+
+namespace dc {
+
+// ---------------------------------------------------------------- errors
+int fail(int code, const char *fmt, ...);
+int hip_fail(hipError_t e, const char *what);
+void clear_error();
+
+#define DC_HIP(call)                                  \
+    do {                                              \
+        hipError_t e_ = (call);                       \
+        if (e_ != hipSuccess)                         \
+            return ::dc::hip_fail(e_, #call);         \
+    } while (0)
+
+#define DC_TRY(call)                                  \
+    do {                                              \
+        int s_ = (call);                              \
+        if (s_ != DC_OK)                              \
+            return s_;                                \
+    } while (0)
+
+// ---------------------------------------------------------------- conv / GEMM
+enum Pass { PASS_FWD = 0, PASS_DGRAD = 1, PASS_WGRAD = 2 };
+
+struct ConvGeom {
+    int N, H, W, C, K, R, S, st, pad, P, Q;
+};
+
+// Launch configuration of one implicit-GEMM pass, chosen on the host.
+struct GemmPlan {
+    int pass;
+    int M, Ng, Kg;        // GEMM sizes (DGRAD: maxima over the stride phases)
+    int phases;           // DGRAD: stride^2, otherwise 1
+    int mt, nt;           // workgroup tile
+    int tiles_m, tiles_n; // tiles per phase
+    int splits;           // split-K factor (1 = no split)
+    int kt_per_split;     // K tiles (of the kernel's K step) per split
+    bool av, bv;          // float4 operand loads possible
+    size_t ws_bytes;      // split-K partial sums
+};
+
+bool conv_geom_from_shape(const dc_conv_shape &sh, ConvGeom *g);
+GemmPlan plan_gemm(const ConvGeom &g, int pass);
+
+int conv_forward(const ConvGeom &g, const GemmPlan &pl, const float *x, const float *w,
+                 const float *bias, int relu, float *y, void *ws, hipStream_t s);
+int conv_dgrad(const ConvGeom &g, const GemmPlan &pl, const float *dy, const float *w,
+               int accumulate, float *dx, void *ws, hipStream_t s);
+int conv_wgrad(const ConvGeom &g, const GemmPlan &pl, const float *x, const float *dy, float *dw,
+               void *ws, hipStream_t s);
+
+// ---------------------------------------------------------------- elementwise and reductions
+size_t colsum_ws_bytes(int64_t rows, int c);
+int colsum(int64_t rows, int c, const float *x, float *out, void *ws, hipStream_t s);
+size_t bn_ws_bytes(int64_t rows, int c);
+int bn_forward(int64_t rows, int c, const float *x, const float *gamma, const float *beta,
+               float eps, int relu, float *y, float *mean, float *invstd, void *ws, hipStream_t s);
+int bn_backward(int64_t rows, int c, const float *dy, const float *x, const float *gamma,
+                const float *mean, const float *invstd, int accumulate, float *dx, float *dgamma,
+                float *dbeta, void *ws, hipStream_t s);
+int relu_forward(const float *x, float *y, int64_t n, hipStream_t s);
+int relu_backward(const float *dy, const float *y, int accumulate, float *dx, int64_t n,
+                  hipStream_t s);
+int add_forward(const float *a, const float *b, int relu, float *y, int64_t n, hipStream_t s);
+int copy_grad(const float *dy, int accumulate, float *dx, int64_t n, hipStream_t s);
+int maxpool_forward(const dc_pool_shape &sh, const float *x, float *y, uint8_t *arg,
+                    hipStream_t s);
+int maxpool_backward(const dc_pool_shape &sh, const float *dy, const uint8_t *arg, int accumulate,
+                     float *dx, hipStream_t s);
+int gap_forward(int n, int hw, int c, const float *x, float *y, hipStream_t s);
+int gap_backward(int n, int hw, int c, const float *dy, int accumulate, float *dx, hipStream_t s);
+size_t xent_ws_bytes(int n);
+int softmax_xent(int n, int classes, const float *logits, const int32_t *labels, float *loss,
+                 float *dlogits, void *ws, hipStream_t s);
+
+// ---------------------------------------------------------------- link pacing
+// Write the device wall clock into *slot.
+int pace_mark(uint64_t *slot, hipStream_t s);
+// Spin until the wall clock reaches *slot + ticks (never longer than cap_ticks).
+int pace_until(const uint64_t *slot, uint64_t ticks, uint64_t cap_ticks, hipStream_t s);
+// Wall-clock ticks per second of the current device.
+int wall_clock_hz(double *hz);
+
+// ---------------------------------------------------------------- planner (host)
+int plan_forward(const int64_t *pt, const int64_t *fc, int64_t dt, int L, uint8_t *p,
+                 int64_t *t_fwd);
+int plan_backward(const int64_t *bc, const int64_t *gt, int64_t dt, int L, uint8_t *g,
+                  int64_t *t_bwd);
+int64_t fm_forward(const int64_t *pt, const int64_t *fc, int64_t dt, int L, const uint8_t *p);
+int64_t fm_backward(const int64_t *bc, const int64_t *gt, int64_t dt, int L, const uint8_t *g);
+
+} // namespace dc

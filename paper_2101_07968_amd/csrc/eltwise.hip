@@ -1,0 +1,600 @@
+// Bandwidth-bound kernels of the forward and backward mini-procedures:
+// ReLU, residual add, max-pooling, global average pooling, BatchNorm,
+// per-channel sums (bias gradients) and the softmax cross-entropy loss.
+//
+// Activations are NHWC, so a channel is the fastest index: threads of a wave
+// walk consecutive channels and every global access is coalesced.  Per-channel
+// reductions over n*h*w rows are two-stage and deterministic: workgroups of a
+// fixed row partition write partial sums to fixed slots, a second kernel adds
+// them in a fixed tree order in double precision.  Nothing uses atomics, so
+// results are bit-identical from run to run.
+#include "dc_internal.h"
+
+#include <algorithm>
+
+namespace dc {
+namespace {
+
+constexpr int EW_THREADS = 256;
+
+inline int ew_blocks(int64_t n, int per_thread = 1) {
+    int64_t b = (n / per_thread + EW_THREADS - 1) / EW_THREADS;
+    return (int)std::max<int64_t>(1, std::min<int64_t>(b, 1 << 20));
+}
+
+// ---------------------------------------------------------------- elementwise
+
+__global__ void relu_fwd_kernel(const float *__restrict__ x, float *__restrict__ y, int64_t n, int64_t n4) {
+    const float4 *x4 = reinterpret_cast<const float4 *>(x);
+    float4 *y4 = reinterpret_cast<float4 *>(y);
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += (int64_t)gridDim.x * blockDim.x) {
+        float4 v = x4[i];
+        v.x = fmaxf(v.x, 0.f); v.y = fmaxf(v.y, 0.f); v.z = fmaxf(v.z, 0.f); v.w = fmaxf(v.w, 0.f);
+        y4[i] = v;
+    }
+    for (int64_t i = 4 * n4 + (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+        y[i] = fmaxf(x[i], 0.f);
+}
+
+__device__ __forceinline__ float relu_grad(float dy, float y) { return y > 0.f ? dy : 0.f; }
+
+__global__ void relu_bwd_kernel(const float *__restrict__ dy, const float *__restrict__ y, int acc,
+                                float *__restrict__ dx, int64_t n, int64_t n4) {
+    const float4 *d4 = reinterpret_cast<const float4 *>(dy);
+    const float4 *y4 = reinterpret_cast<const float4 *>(y);
+    float4 *o4 = reinterpret_cast<float4 *>(dx);
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += (int64_t)gridDim.x * blockDim.x) {
+        float4 d = d4[i], v = y4[i], o;
+        o.x = relu_grad(d.x, v.x); o.y = relu_grad(d.y, v.y); o.z = relu_grad(d.z, v.z); o.w = relu_grad(d.w, v.w);
+        if (acc) {
+            float4 p = o4[i];
+            o.x += p.x; o.y += p.y; o.z += p.z; o.w += p.w;
+        }
+        o4[i] = o;
+    }
+    for (int64_t i = 4 * n4 + (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+        float o = relu_grad(dy[i], y[i]);
+        dx[i] = acc ? dx[i] + o : o;
+    }
+}
+
+__global__ void add_fwd_kernel(const float *__restrict__ a, const float *__restrict__ b, int relu,
+                               float *__restrict__ y, int64_t n, int64_t n4) {
+    const float4 *a4 = reinterpret_cast<const float4 *>(a);
+    const float4 *b4 = reinterpret_cast<const float4 *>(b);
+    float4 *y4 = reinterpret_cast<float4 *>(y);
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += (int64_t)gridDim.x * blockDim.x) {
+        float4 u = a4[i], v = b4[i], o;
+        o.x = u.x + v.x; o.y = u.y + v.y; o.z = u.z + v.z; o.w = u.w + v.w;
+        if (relu) {
+            o.x = fmaxf(o.x, 0.f); o.y = fmaxf(o.y, 0.f); o.z = fmaxf(o.z, 0.f); o.w = fmaxf(o.w, 0.f);
+        }
+        y4[i] = o;
+    }
+    for (int64_t i = 4 * n4 + (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+        float o = a[i] + b[i];
+        y[i] = relu ? fmaxf(o, 0.f) : o;
+    }
+}
+
+__global__ void copy_grad_kernel(const float *__restrict__ dy, int acc, float *__restrict__ dx, int64_t n, int64_t n4) {
+    const float4 *d4 = reinterpret_cast<const float4 *>(dy);
+    float4 *o4 = reinterpret_cast<float4 *>(dx);
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += (int64_t)gridDim.x * blockDim.x) {
+        float4 o = d4[i];
+        if (acc) {
+            float4 p = o4[i];
+            o.x += p.x; o.y += p.y; o.z += p.z; o.w += p.w;
+        }
+        o4[i] = o;
+    }
+    for (int64_t i = 4 * n4 + (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+        dx[i] = acc ? dx[i] + dy[i] : dy[i];
+}
+
+// ---------------------------------------------------------------- pooling
+
+__global__ void maxpool_fwd_kernel(dc_pool_shape sh, int P, int Q, const float *__restrict__ x,
+                                   float *__restrict__ y, uint8_t *__restrict__ arg) {
+    const int64_t total = (int64_t)sh.n * P * Q * sh.c;
+    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total; e += (int64_t)gridDim.x * blockDim.x) {
+        int c = (int)(e % sh.c);
+        int64_t pix = e / sh.c;
+        int q = (int)(pix % Q);
+        int64_t t = pix / Q;
+        int p = (int)(t % P);
+        int n = (int)(t / P);
+        int best = -1;
+        float bv = 0.f;
+        for (int r = 0; r < sh.r; ++r) {
+            int h = p * sh.stride + r - sh.pad;
+            if ((unsigned)h >= (unsigned)sh.h)
+                continue;
+            for (int s = 0; s < sh.s; ++s) {
+                int w = q * sh.stride + s - sh.pad;
+                if ((unsigned)w >= (unsigned)sh.w)
+                    continue;
+                float v = x[(((int64_t)n * sh.h + h) * sh.w + w) * sh.c + c];
+                if (best < 0 || v > bv) {
+                    best = r * sh.s + s;
+                    bv = v;
+                }
+            }
+        }
+        y[e] = bv;
+        arg[e] = (uint8_t)(best < 0 ? 0 : best);
+    }
+}
+
+__global__ void maxpool_bwd_kernel(dc_pool_shape sh, int P, int Q, const float *__restrict__ dy,
+                                   const uint8_t *__restrict__ arg, int acc, float *__restrict__ dx) {
+    const int64_t total = (int64_t)sh.n * sh.h * sh.w * sh.c;
+    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total; e += (int64_t)gridDim.x * blockDim.x) {
+        int c = (int)(e % sh.c);
+        int64_t pix = e / sh.c;
+        int w = (int)(pix % sh.w);
+        int64_t t = pix / sh.w;
+        int h = (int)(t % sh.h);
+        int n = (int)(t / sh.h);
+        // output windows that contain (h, w): p*stride - pad <= h <= p*stride - pad + r - 1
+        int hp = h + sh.pad, wp = w + sh.pad;
+        int p_lo = hp - sh.r + 1 > 0 ? (hp - sh.r + 1 + sh.stride - 1) / sh.stride : 0;
+        int p_hi = min(P - 1, hp / sh.stride);
+        int q_lo = wp - sh.s + 1 > 0 ? (wp - sh.s + 1 + sh.stride - 1) / sh.stride : 0;
+        int q_hi = min(Q - 1, wp / sh.stride);
+        float g = 0.f;
+        for (int p = p_lo; p <= p_hi; ++p)
+            for (int q = q_lo; q <= q_hi; ++q) {
+                int64_t o = (((int64_t)n * P + p) * Q + q) * sh.c + c;
+                int a = (hp - p * sh.stride) * sh.s + (wp - q * sh.stride);
+                if (arg[o] == a)
+                    g += dy[o];
+            }
+        dx[e] = acc ? dx[e] + g : g;
+    }
+}
+
+__global__ void gap_fwd_kernel(int n, int hw, int c, const float *__restrict__ x, float *__restrict__ y) {
+    int64_t total = (int64_t)n * c;
+    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total; e += (int64_t)gridDim.x * blockDim.x) {
+        int ch = (int)(e % c);
+        int64_t b = e / c;
+        const float *src = x + b * hw * c + ch;
+        float s = 0.f;
+        for (int i = 0; i < hw; ++i)
+            s += src[(int64_t)i * c];
+        y[e] = s / (float)hw;
+    }
+}
+
+__global__ void gap_bwd_kernel(int n, int hw, int c, const float *__restrict__ dy, int acc, float *__restrict__ dx) {
+    int64_t total = (int64_t)n * hw * c;
+    float inv = 1.0f / (float)hw;
+    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total; e += (int64_t)gridDim.x * blockDim.x) {
+        int ch = (int)(e % c);
+        int64_t b = e / ((int64_t)hw * c);
+        float g = dy[b * c + ch] * inv;
+        dx[e] = acc ? dx[e] + g : g;
+    }
+}
+
+// ---------------------------------------------------------------- per-channel reductions
+//
+// Stage 1: workgroup (chunk, group) sums rows [chunk*rows_per_chunk, ...) of
+// channels [group*CG, group*CG + CG) of a [rows][c] matrix.  256 threads =
+// CG channels x (256 / CG) row lanes; lanes are combined in a fixed order.
+// Mode 0: sum x.  Mode 1: sum (x - mean)^2.  Mode 2: sum dy and sum dy*xhat
+// with xhat = (x - mean) * invstd (two outputs).
+constexpr int CG = 64;
+constexpr int RL = EW_THREADS / CG;
+
+template <int MODE>
+__global__ __launch_bounds__(EW_THREADS) void colred_partial_kernel(
+    int64_t rows, int c, int64_t rows_per_chunk, const float *__restrict__ x, const float *__restrict__ dy,
+    const float *__restrict__ mean, const float *__restrict__ invstd, float *__restrict__ part0,
+    float *__restrict__ part1) {
+    __shared__ float s0[RL][CG];
+    __shared__ float s1[RL][CG];
+    const int lane_c = threadIdx.x % CG, rl = threadIdx.x / CG;
+    const int ch = blockIdx.y * CG + lane_c;
+    const int64_t r0 = (int64_t)blockIdx.x * rows_per_chunk;
+    const int64_t r1 = min(rows, r0 + rows_per_chunk);
+    float a0 = 0.f, a1 = 0.f;
+    if (ch < c) {
+        float mu = (MODE != 0) ? mean[ch] : 0.f;
+        float is = (MODE == 2) ? invstd[ch] : 0.f;
+        for (int64_t r = r0 + rl; r < r1; r += RL) {
+            int64_t o = r * c + ch;
+            if (MODE == 0) {
+                a0 += x[o];
+            } else if (MODE == 1) {
+                float d = x[o] - mu;
+                a0 += d * d;
+            } else {
+                float g = dy[o];
+                a0 += g;
+                a1 += g * ((x[o] - mu) * is);
+            }
+        }
+    }
+    s0[rl][lane_c] = a0;
+    s1[rl][lane_c] = a1;
+    __syncthreads();
+    if (rl == 0 && ch < c) {
+        float t0 = 0.f, t1 = 0.f;
+        for (int i = 0; i < RL; ++i) {
+            t0 += s0[i][lane_c];
+            t1 += s1[i][lane_c];
+        }
+        part0[(int64_t)blockIdx.x * c + ch] = t0;
+        if (MODE == 2)
+            part1[(int64_t)blockIdx.x * c + ch] = t1;
+    }
+}
+
+// Stage 2: one workgroup per channel adds the chunk partials with a fixed
+// tree in double precision.  Output kind: 0 -> out0 = sum; 1 -> out0 = sum/rows
+// (mean); 2 -> out0 = 1/sqrt(sum/rows + eps) (invstd); 3 -> out0 = sum0, out1 = sum1.
+template <int KIND>
+__global__ __launch_bounds__(EW_THREADS) void colred_final_kernel(int nchunks, int c, int64_t rows, float eps,
+                                                                  const float *__restrict__ part0,
+                                                                  const float *__restrict__ part1,
+                                                                  float *__restrict__ out0, float *__restrict__ out1) {
+    __shared__ double s0[EW_THREADS];
+    __shared__ double s1[EW_THREADS];
+    const int ch = blockIdx.x;
+    double a0 = 0.0, a1 = 0.0;
+    for (int i = threadIdx.x; i < nchunks; i += EW_THREADS) {
+        a0 += (double)part0[(int64_t)i * c + ch];
+        if (KIND == 3)
+            a1 += (double)part1[(int64_t)i * c + ch];
+    }
+    s0[threadIdx.x] = a0;
+    s1[threadIdx.x] = a1;
+    __syncthreads();
+    for (int w = EW_THREADS / 2; w > 0; w >>= 1) {
+        if (threadIdx.x < w) {
+            s0[threadIdx.x] += s0[threadIdx.x + w];
+            s1[threadIdx.x] += s1[threadIdx.x + w];
+        }
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) {
+        double v = s0[0];
+        if (KIND == 0) {
+            out0[ch] = (float)v;
+        } else if (KIND == 1) {
+            out0[ch] = (float)(v / (double)rows);
+        } else if (KIND == 2) {
+            out0[ch] = (float)(1.0 / sqrt(v / (double)rows + (double)eps));
+        } else {
+            out0[ch] = (float)v;
+            out1[ch] = (float)s1[0];
+        }
+    }
+}
+
+__global__ void bn_apply_kernel(int64_t rows, int c, const float *__restrict__ x, const float *__restrict__ gamma,
+                                const float *__restrict__ beta, const float *__restrict__ mean,
+                                const float *__restrict__ invstd, int relu, float *__restrict__ y) {
+    const int64_t total = rows * c;
+    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total; e += (int64_t)gridDim.x * blockDim.x) {
+        int ch = (int)(e % c);
+        float v = gamma[ch] * ((x[e] - mean[ch]) * invstd[ch]) + beta[ch];
+        y[e] = relu ? fmaxf(v, 0.f) : v;
+    }
+}
+
+__global__ void bn_bwd_apply_kernel(int64_t rows, int c, const float *__restrict__ dy, const float *__restrict__ x,
+                                    const float *__restrict__ gamma, const float *__restrict__ mean,
+                                    const float *__restrict__ invstd, const float *__restrict__ dgamma,
+                                    const float *__restrict__ dbeta, int acc, float *__restrict__ dx) {
+    const int64_t total = rows * c;
+    const float inv_rows = 1.0f / (float)rows;
+    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total; e += (int64_t)gridDim.x * blockDim.x) {
+        int ch = (int)(e % c);
+        float is = invstd[ch];
+        float xhat = (x[e] - mean[ch]) * is;
+        float g = gamma[ch] * is * (dy[e] - dbeta[ch] * inv_rows - xhat * dgamma[ch] * inv_rows);
+        dx[e] = acc ? dx[e] + g : g;
+    }
+}
+
+struct ColPlan {
+    int nchunks;
+    int64_t rows_per_chunk;
+};
+
+ColPlan col_plan(int64_t rows, int c) {
+    int groups = (c + CG - 1) / CG;
+    // about 1024 workgroups in all, at most 256 chunks (one per stage-2 thread
+    // slot), at least RL*8 rows each
+    int64_t want = std::max<int64_t>(1, std::min<int64_t>(256, 1024 / std::max(groups, 1)));
+    int64_t rpc = std::max<int64_t>((rows + want - 1) / want, RL * 8);
+    ColPlan p;
+    p.rows_per_chunk = rpc;
+    p.nchunks = (int)((rows + rpc - 1) / rpc);
+    return p;
+}
+
+size_t align256(size_t b) { return (b + 255) / 256 * 256; }
+
+// Number of float4 groups the vector path may take: n/4 when every pointer is
+// 16-byte aligned, else 0 (everything goes through the scalar tail loop).
+inline bool al16(const void *p) { return ((uintptr_t)p & 15) == 0; }
+inline int64_t vec4(int64_t n, const void *a, const void *b) { return al16(a) && al16(b) ? n >> 2 : 0; }
+inline int64_t vec4(int64_t n, const void *a, const void *b, const void *c) { return al16(c) ? vec4(n, a, b) : 0; }
+
+// ---------------------------------------------------------------- softmax cross-entropy
+
+// One workgroup per sample: loss_i = logsumexp(z_i) - z_i[y_i],
+// dz_i = (softmax(z_i) - onehot(y_i)) / n.
+__global__ __launch_bounds__(EW_THREADS) void xent_row_kernel(int n, int classes, const float *__restrict__ z,
+                                                              const int32_t *__restrict__ y, float *__restrict__ loss_i,
+                                                              float *__restrict__ dz) {
+    __shared__ float red[EW_THREADS];
+    const int i = blockIdx.x;
+    const float *zi = z + (int64_t)i * classes;
+    float m = -INFINITY;
+    for (int k = threadIdx.x; k < classes; k += EW_THREADS)
+        m = fmaxf(m, zi[k]);
+    red[threadIdx.x] = m;
+    __syncthreads();
+    for (int w = EW_THREADS / 2; w > 0; w >>= 1) {
+        if (threadIdx.x < w)
+            red[threadIdx.x] = fmaxf(red[threadIdx.x], red[threadIdx.x + w]);
+        __syncthreads();
+    }
+    m = red[0];
+    __syncthreads();
+    float s = 0.f;
+    for (int k = threadIdx.x; k < classes; k += EW_THREADS)
+        s += expf(zi[k] - m);
+    red[threadIdx.x] = s;
+    __syncthreads();
+    for (int w = EW_THREADS / 2; w > 0; w >>= 1) {
+        if (threadIdx.x < w)
+            red[threadIdx.x] += red[threadIdx.x + w];
+        __syncthreads();
+    }
+    s = red[0];
+    const int label = y[i];
+    const float inv_n = 1.0f / (float)n;
+    const float inv_s = 1.0f / s;
+    for (int k = threadIdx.x; k < classes; k += EW_THREADS) {
+        float p = expf(zi[k] - m) * inv_s;
+        dz[(int64_t)i * classes + k] = (p - (k == label ? 1.f : 0.f)) * inv_n;
+    }
+    if (threadIdx.x == 0) {
+        float zl = (label >= 0 && label < classes) ? zi[label] : 0.f;
+        loss_i[i] = m + logf(s) - zl;
+    }
+}
+
+__global__ void xent_mean_kernel(int n, const float *__restrict__ loss_i, float *__restrict__ loss) {
+    if (threadIdx.x == 0 && blockIdx.x == 0) {
+        double s = 0.0;
+        for (int i = 0; i < n; ++i)
+            s += (double)loss_i[i];
+        loss[0] = (float)(s / (double)n);
+    }
+}
+
+// ---------------------------------------------------------------- link pacing
+
+__global__ void pace_mark_kernel(uint64_t *slot) {
+    if (threadIdx.x == 0)
+        *slot = wall_clock64();
+}
+
+// Spins until the wall clock passes *slot + ticks.  It always ends: the wall
+// clock only moves forward and the wait never exceeds cap_ticks.
+__global__ void pace_until_kernel(const uint64_t *slot, uint64_t ticks, uint64_t cap_ticks) {
+    if (threadIdx.x != 0)
+        return;
+    const uint64_t start = wall_clock64();
+    const uint64_t deadline = *slot + ticks;
+    for (;;) {
+        uint64_t now = wall_clock64();
+        if (now >= deadline || now - start >= cap_ticks)
+            break;
+        __builtin_amdgcn_s_sleep(2);
+    }
+}
+
+} // namespace
+
+// ---------------------------------------------------------------- launchers
+
+int relu_forward(const float *x, float *y, int64_t n, hipStream_t s) {
+    if (n <= 0)
+        return DC_OK;
+    hipLaunchKernelGGL(relu_fwd_kernel, dim3(ew_blocks(n, 4)), dim3(EW_THREADS), 0, s, x, y, n, vec4(n, x, y));
+    DC_HIP(hipGetLastError());
+    return DC_OK;
+}
+
+int relu_backward(const float *dy, const float *y, int accumulate, float *dx, int64_t n, hipStream_t s) {
+    if (n <= 0)
+        return DC_OK;
+    hipLaunchKernelGGL(relu_bwd_kernel, dim3(ew_blocks(n, 4)), dim3(EW_THREADS), 0, s, dy, y, accumulate, dx, n,
+                       vec4(n, dy, y, dx));
+    DC_HIP(hipGetLastError());
+    return DC_OK;
+}
+
+int add_forward(const float *a, const float *b, int relu, float *y, int64_t n, hipStream_t s) {
+    if (n <= 0)
+        return DC_OK;
+    hipLaunchKernelGGL(add_fwd_kernel, dim3(ew_blocks(n, 4)), dim3(EW_THREADS), 0, s, a, b, relu, y, n, vec4(n, a, b, y));
+    DC_HIP(hipGetLastError());
+    return DC_OK;
+}
+
+int copy_grad(const float *dy, int accumulate, float *dx, int64_t n, hipStream_t s) {
+    if (n <= 0)
+        return DC_OK;
+    hipLaunchKernelGGL(copy_grad_kernel, dim3(ew_blocks(n, 4)), dim3(EW_THREADS), 0, s, dy, accumulate, dx, n,
+                       vec4(n, dy, dx));
+    DC_HIP(hipGetLastError());
+    return DC_OK;
+}
+
+int maxpool_forward(const dc_pool_shape &sh, const float *x, float *y, uint8_t *arg, hipStream_t s) {
+    int P = (sh.h + 2 * sh.pad - sh.r) / sh.stride + 1;
+    int Q = (sh.w + 2 * sh.pad - sh.s) / sh.stride + 1;
+    int64_t total = (int64_t)sh.n * P * Q * sh.c;
+    if (total <= 0)
+        return DC_OK;
+    hipLaunchKernelGGL(maxpool_fwd_kernel, dim3(ew_blocks(total)), dim3(EW_THREADS), 0, s, sh, P, Q, x, y, arg);
+    DC_HIP(hipGetLastError());
+    return DC_OK;
+}
+
+int maxpool_backward(const dc_pool_shape &sh, const float *dy, const uint8_t *arg, int accumulate, float *dx,
+                     hipStream_t s) {
+    int P = (sh.h + 2 * sh.pad - sh.r) / sh.stride + 1;
+    int Q = (sh.w + 2 * sh.pad - sh.s) / sh.stride + 1;
+    int64_t total = (int64_t)sh.n * sh.h * sh.w * sh.c;
+    if (total <= 0)
+        return DC_OK;
+    hipLaunchKernelGGL(maxpool_bwd_kernel, dim3(ew_blocks(total)), dim3(EW_THREADS), 0, s, sh, P, Q, dy, arg,
+                       accumulate, dx);
+    DC_HIP(hipGetLastError());
+    return DC_OK;
+}
+
+int gap_forward(int n, int hw, int c, const float *x, float *y, hipStream_t s) {
+    int64_t total = (int64_t)n * c;
+    if (total <= 0)
+        return DC_OK;
+    hipLaunchKernelGGL(gap_fwd_kernel, dim3(ew_blocks(total)), dim3(EW_THREADS), 0, s, n, hw, c, x, y);
+    DC_HIP(hipGetLastError());
+    return DC_OK;
+}
+
+int gap_backward(int n, int hw, int c, const float *dy, int accumulate, float *dx, hipStream_t s) {
+    int64_t total = (int64_t)n * hw * c;
+    if (total <= 0)
+        return DC_OK;
+    hipLaunchKernelGGL(gap_bwd_kernel, dim3(ew_blocks(total)), dim3(EW_THREADS), 0, s, n, hw, c, dy, accumulate, dx);
+    DC_HIP(hipGetLastError());
+    return DC_OK;
+}
+
+size_t colsum_ws_bytes(int64_t rows, int c) {
+    ColPlan p = col_plan(rows, c);
+    return align256((size_t)p.nchunks * c * sizeof(float));
+}
+
+int colsum(int64_t rows, int c, const float *x, float *out, void *ws, hipStream_t s) {
+    if (c <= 0)
+        return DC_OK;
+    if (rows <= 0) {
+        DC_HIP(hipMemsetAsync(out, 0, sizeof(float) * c, s));
+        return DC_OK;
+    }
+    ColPlan p = col_plan(rows, c);
+    float *part = static_cast<float *>(ws);
+    dim3 g1(p.nchunks, (c + CG - 1) / CG);
+    hipLaunchKernelGGL(colred_partial_kernel<0>, g1, dim3(EW_THREADS), 0, s, rows, c, p.rows_per_chunk, x,
+                       (const float *)nullptr, (const float *)nullptr, (const float *)nullptr, part, (float *)nullptr);
+    DC_HIP(hipGetLastError());
+    hipLaunchKernelGGL(colred_final_kernel<0>, dim3(c), dim3(EW_THREADS), 0, s, p.nchunks, c, rows, 0.f, part,
+                       (const float *)nullptr, out, (float *)nullptr);
+    DC_HIP(hipGetLastError());
+    return DC_OK;
+}
+
+size_t bn_ws_bytes(int64_t rows, int c) {
+    ColPlan p = col_plan(rows, c);
+    return 2 * align256((size_t)p.nchunks * c * sizeof(float));
+}
+
+int bn_forward(int64_t rows, int c, const float *x, const float *gamma, const float *beta, float eps, int relu,
+               float *y, float *mean, float *invstd, void *ws, hipStream_t s) {
+    if (rows <= 0 || c <= 0)
+        return DC_OK;
+    ColPlan p = col_plan(rows, c);
+    float *part = static_cast<float *>(ws);
+    dim3 g1(p.nchunks, (c + CG - 1) / CG);
+    hipLaunchKernelGGL(colred_partial_kernel<0>, g1, dim3(EW_THREADS), 0, s, rows, c, p.rows_per_chunk, x,
+                       (const float *)nullptr, (const float *)nullptr, (const float *)nullptr, part, (float *)nullptr);
+    DC_HIP(hipGetLastError());
+    hipLaunchKernelGGL(colred_final_kernel<1>, dim3(c), dim3(EW_THREADS), 0, s, p.nchunks, c, rows, eps, part,
+                       (const float *)nullptr, mean, (float *)nullptr);
+    DC_HIP(hipGetLastError());
+    hipLaunchKernelGGL(colred_partial_kernel<1>, g1, dim3(EW_THREADS), 0, s, rows, c, p.rows_per_chunk, x,
+                       (const float *)nullptr, (const float *)mean, (const float *)nullptr, part, (float *)nullptr);
+    DC_HIP(hipGetLastError());
+    hipLaunchKernelGGL(colred_final_kernel<2>, dim3(c), dim3(EW_THREADS), 0, s, p.nchunks, c, rows, eps, part,
+                       (const float *)nullptr, invstd, (float *)nullptr);
+    DC_HIP(hipGetLastError());
+    int64_t total = rows * c;
+    hipLaunchKernelGGL(bn_apply_kernel, dim3(ew_blocks(total)), dim3(EW_THREADS), 0, s, rows, c, x, gamma, beta, mean,
+                       invstd, relu, y);
+    DC_HIP(hipGetLastError());
+    return DC_OK;
+}
+
+int bn_backward(int64_t rows, int c, const float *dy, const float *x, const float *gamma, const float *mean,
+                const float *invstd, int accumulate, float *dx, float *dgamma, float *dbeta, void *ws, hipStream_t s) {
+    if (rows <= 0 || c <= 0)
+        return DC_OK;
+    ColPlan p = col_plan(rows, c);
+    float *part0 = static_cast<float *>(ws);
+    float *part1 = reinterpret_cast<float *>(static_cast<char *>(ws) + align256((size_t)p.nchunks * c * sizeof(float)));
+    dim3 g1(p.nchunks, (c + CG - 1) / CG);
+    hipLaunchKernelGGL(colred_partial_kernel<2>, g1, dim3(EW_THREADS), 0, s, rows, c, p.rows_per_chunk, x, dy, mean,
+                       invstd, part0, part1);
+    DC_HIP(hipGetLastError());
+    hipLaunchKernelGGL(colred_final_kernel<3>, dim3(c), dim3(EW_THREADS), 0, s, p.nchunks, c, rows, 0.f, part0,
+                       (const float *)part1, dbeta, dgamma);
+    DC_HIP(hipGetLastError());
+    if (dx) {
+        int64_t total = rows * c;
+        hipLaunchKernelGGL(bn_bwd_apply_kernel, dim3(ew_blocks(total)), dim3(EW_THREADS), 0, s, rows, c, dy, x, gamma,
+                           mean, invstd, dgamma, dbeta, accumulate, dx);
+        DC_HIP(hipGetLastError());
+    }
+    return DC_OK;
+}
+
+size_t xent_ws_bytes(int n) { return align256((size_t)std::max(n, 1) * sizeof(float)); }
+
+int softmax_xent(int n, int classes, const float *logits, const int32_t *labels, float *loss, float *dlogits,
+                 void *ws, hipStream_t s) {
+    if (n <= 0 || classes <= 0)
+        return DC_OK;
+    float *loss_i = static_cast<float *>(ws);
+    hipLaunchKernelGGL(xent_row_kernel, dim3(n), dim3(EW_THREADS), 0, s, n, classes, logits, labels, loss_i, dlogits);
+    DC_HIP(hipGetLastError());
+    hipLaunchKernelGGL(xent_mean_kernel, dim3(1), dim3(64), 0, s, n, (const float *)loss_i, loss);
+    DC_HIP(hipGetLastError());
+    return DC_OK;
+}
+
+int pace_mark(uint64_t *slot, hipStream_t s) {
+    hipLaunchKernelGGL(pace_mark_kernel, dim3(1), dim3(64), 0, s, slot);
+    DC_HIP(hipGetLastError());
+    return DC_OK;
+}
+
+int pace_until(const uint64_t *slot, uint64_t ticks, uint64_t cap_ticks, hipStream_t s) {
+    hipLaunchKernelGGL(pace_until_kernel, dim3(1), dim3(64), 0, s, slot, ticks, cap_ticks);
+    DC_HIP(hipGetLastError());
+    return DC_OK;
+}
+
+int wall_clock_hz(double *hz) {
+    int dev = 0;
+    DC_HIP(hipGetDevice(&dev));
+    int khz = 0;
+    DC_HIP(hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, dev));
+    if (khz <= 0)
+        return fail(DC_EHIP, "device reports no wall-clock rate");
+    *hz = (double)khz * 1000.0;
+    return DC_OK;
+}
+
+} // namespace dc

@@ -1,0 +1,735 @@
+// Convolution and FC layers as implicit GEMM on gfx950 fp32 matrix cores.
+//
+// The forward and backward compute mini-procedures of a conv or FC layer
+// (Sec. III-A) are three GEMMs over the NHWC activations and KRSC filters:
+//
+//   forward  Y[m][k]  = sum_kk X~[m][kk] W[k][kk]     m = (n,p,q), kk = (r,s,c)
+//   dgrad    dX[m][c] = sum_kk dY~[m][kk] W~[kk][c]   m = (n,h,w) in one stride phase,
+//                                                      kk = (tap r, tap s, k)
+//   wgrad    dW[k][kk] = sum_m dY[m][k] X~[m][kk]     m = (n,p,q), kk = (r,s,c)
+//
+// where ~ marks an operand gathered on the fly (no im2col buffer).  For a
+// strided convolution, output rows h with the same residue modulo the stride
+// see the same filter taps, so dgrad runs one GEMM per residue pair ("phase")
+// holding only the taps that hit; no structurally zero products are formed.
+//
+// One kernel template serves all three passes.  A workgroup of 256 threads
+// (4 waves of 64) owns an MT x NT output tile; each wave owns a quarter and
+// issues v_mfma_f32_32x32x2f32.  Operand tiles of depth KT are staged through
+// LDS in the layout of their contiguous global dimension (float4 loads,
+// ds_write_b128), double buffered with one barrier per K step; the next
+// step's global loads are in flight while the current step multiplies.
+// Split-K writes fixed-position partial sums that a second kernel adds in a
+// fixed order, so every result is deterministic.  Workgroup ids are remapped
+// so that consecutive tiles land on the same XCD and share its L2.
+#include "dc_internal.h"
+
+#include <algorithm>
+#include <climits>
+
+namespace dc {
+namespace {
+
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+constexpr int KT = 16;   // K depth of one LDS stage
+constexpr int NTHR = 256;
+constexpr int PADK = 4;  // padding of k-contiguous LDS rows (floats)
+constexpr int PADR = 4;  // padding of row-contiguous LDS rows (floats)
+
+// Division by a runtime constant d via multiply-high (valid for n < 2^31).
+struct FDiv {
+    uint32_t d, m, s;
+    __device__ __forceinline__ uint32_t div(uint32_t n) const {
+        uint32_t hi = __umulhi(n, m);
+        return (uint32_t)(((uint64_t)hi + n) >> s);
+    }
+};
+
+FDiv make_fdiv(uint32_t d) {
+    FDiv f;
+    f.d = d;
+    if (d <= 1) {
+        f.m = 0;
+        f.s = 0;
+        return f;
+    }
+    uint32_t l = 32 - __builtin_clz(d - 1);
+    uint64_t one = 1;
+    f.m = (uint32_t)(((one << 32) * ((one << l) - d)) / d + 1);
+    f.s = l;
+    return f;
+}
+
+struct Args {
+    int N, H, W, C, K, R, S, st, pad, P, Q;
+    int M, Ng, Kg;          // FWD / WGRAD sizes; DGRAD: maxima over phases
+    int tiles_m, tiles_n, tiles;
+    int splits, kt_per_split;
+    const float *A;         // FWD: x   DGRAD: dy   WGRAD: dy
+    const float *B;         // FWD: w   DGRAD: w    WGRAD: x
+    float *out;             // FWD: y   DGRAD: dx   WGRAD: dw
+    const float *bias;      // FWD only, may be null
+    float *partial;         // split-K scratch
+    int relu, accumulate;
+    FDiv fC, fS, fK, fQ, fPQ;
+};
+
+// Per-phase geometry of dgrad (stride residues rh, rw).
+struct Phase {
+    int Hh, Wh;     // output rows / cols of this residue
+    int Rt, St;     // filter taps that reach them
+    int r0, s0;     // first tap
+    int dh, dw;     // p = i + dh - tr, q = j + dw - ts
+    int M, Kg;
+};
+
+__device__ __forceinline__ Phase make_phase(const Args &a, int z) {
+    Phase ph;
+    int rh = z / a.st, rw = z % a.st;
+    ph.Hh = a.H > rh ? (a.H - rh + a.st - 1) / a.st : 0;
+    ph.Wh = a.W > rw ? (a.W - rw + a.st - 1) / a.st : 0;
+    ph.r0 = (rh + a.pad) % a.st;
+    ph.s0 = (rw + a.pad) % a.st;
+    ph.Rt = ph.r0 < a.R ? (a.R - ph.r0 + a.st - 1) / a.st : 0;
+    ph.St = ph.s0 < a.S ? (a.S - ph.s0 + a.st - 1) / a.st : 0;
+    ph.dh = (rh + a.pad - ph.r0) / a.st;
+    ph.dw = (rw + a.pad - ph.s0) / a.st;
+    ph.M = a.N * ph.Hh * ph.Wh;
+    ph.Kg = ph.Rt * ph.St * a.K;
+    return ph;
+}
+
+__device__ __forceinline__ float4 ld4(const float *p) { return *reinterpret_cast<const float4 *>(p); }
+__device__ __forceinline__ void st4(float *p, float4 v) { *reinterpret_cast<float4 *>(p) = v; }
+
+// Address of output row m of a pass in its destination tensor (row-major
+// [rows][Ng] for FWD / WGRAD, the NHWC pixel of the phase for DGRAD).
+__device__ __forceinline__ size_t out_row(const Args &a, int pass, const Phase &ph, int z, int m) {
+    if (pass != PASS_DGRAD)
+        return (size_t)m * a.Ng;
+    int hw = ph.Hh * ph.Wh;
+    int n = m / hw;
+    int rem = m - n * hw;
+    int i = rem / ph.Wh;
+    int j = rem - i * ph.Wh;
+    int h = z / a.st + a.st * i;
+    int w = z % a.st + a.st * j;
+    return (((size_t)n * a.H + h) * a.W + w) * a.C;
+}
+
+__device__ __forceinline__ float epilogue(const Args &a, int pass, float v, int n, const float *dst) {
+    if (pass == PASS_FWD) {
+        if (a.bias)
+            v += a.bias[n];
+        if (a.relu)
+            v = fmaxf(v, 0.0f);
+    } else if (pass == PASS_DGRAD) {
+        if (a.accumulate)
+            v += *dst;
+    }
+    return v;
+}
+
+template <int PASS, int MT, int NT, bool AV, bool BV>
+__global__ __launch_bounds__(NTHR) void igemm_kernel(Args a) {
+    constexpr bool A_KC = (PASS != PASS_WGRAD); // A tile stored [row][k]
+    constexpr bool B_KC = (PASS == PASS_FWD);   // B tile stored [col][k]
+    constexpr int A_LD = A_KC ? (KT + PADK) : (MT + PADR);
+    constexpr int B_LD = B_KC ? (KT + PADK) : (NT + PADR);
+    constexpr int A_SZ = A_KC ? MT * A_LD : KT * A_LD;
+    constexpr int B_SZ = B_KC ? NT * B_LD : KT * B_LD;
+    constexpr int FA = MT * KT / 4 / NTHR; // float4 fragments per thread
+    constexpr int FB = NT * KT / 4 / NTHR;
+    static_assert(FA >= 1 && FB >= 1, "tile too small");
+    constexpr int BM = MT / 64, BN = NT / 64; // 32x32 blocks per wave
+
+    __shared__ __attribute__((aligned(16))) float lds[2 * (A_SZ + B_SZ)];
+
+    const int t = threadIdx.x;
+    // XCD-aware tile order: consecutive ids of one XCD get consecutive tiles.
+    int bid = blockIdx.x;
+    {
+        int per = gridDim.x >> 3;
+        bid = (bid & 7) * per + (bid >> 3);
+    }
+    if (bid >= a.tiles)
+        return;
+    const int tm = bid / a.tiles_n;
+    const int tn = bid - tm * a.tiles_n;
+    const int z = blockIdx.z;
+    const int split = blockIdx.y;
+
+    Phase ph{};
+    int M = a.M, Kg = a.Kg;
+    if (PASS == PASS_DGRAD) {
+        ph = make_phase(a, z);
+        M = ph.M;
+        Kg = ph.Kg;
+        if (tm * MT >= M)
+            return;
+    }
+    const int ktiles = (Kg + KT - 1) / KT;
+    const int kt0 = split * a.kt_per_split;
+    const int kt1 = min(kt0 + a.kt_per_split, ktiles);
+    const int nkt = max(kt1 - kt0, 0);
+
+    // ------------------------------------------------ per-thread load state
+    // A fragments: k-contiguous -> (row = idx / (KT/4), kc = idx % (KT/4));
+    // row-contiguous -> (krow = idx / (MT/4), mc = idx % (MT/4)).
+    int a_row[FA];
+    int a_kc = 0;
+    bool a_ok[FA];
+    // FWD: pixel base and (h, w) origin per row; DGRAD: (n, i+dh, j+dw) per row.
+    int a_n[FA], a_h[FA], a_w[FA];
+#pragma unroll
+    for (int f = 0; f < FA; ++f) {
+        int idx = t + NTHR * f;
+        if (A_KC) {
+            a_row[f] = idx / (KT / 4);
+            a_kc = idx % (KT / 4);
+            int m = tm * MT + a_row[f];
+            a_ok[f] = m < M;
+            int mm = a_ok[f] ? m : 0;
+            if (PASS == PASS_FWD) {
+                int n = a.fPQ.div(mm);
+                int rem = mm - n * a.P * a.Q;
+                int p = a.fQ.div(rem);
+                int q = rem - p * a.Q;
+                a_n[f] = n;
+                a_h[f] = p * a.st - a.pad;
+                a_w[f] = q * a.st - a.pad;
+            } else {
+                int hw = ph.Hh * ph.Wh;
+                int n = hw ? mm / hw : 0;
+                int rem = mm - n * hw;
+                int i = ph.Wh ? rem / ph.Wh : 0;
+                int j = rem - i * ph.Wh;
+                a_n[f] = n;
+                a_h[f] = i + ph.dh;
+                a_w[f] = j + ph.dw;
+            }
+        } else {
+            a_row[f] = idx / (MT / 4); // k row (pixel) within the stage
+            a_kc = idx % (MT / 4);     // output-channel quad
+            a_ok[f] = true;
+            a_n[f] = a_h[f] = a_w[f] = 0;
+        }
+    }
+    // B fragments: k-contiguous -> (row = idx / (KT/4), kc); n-contiguous ->
+    // (krow = idx / (NT/4), nc = idx % (NT/4)).
+    int b_row[FB];
+    int b_kc = 0;
+    // WGRAD: filter tap (r, s) and channel c of the thread's column quad (or
+    // of each of its 4 columns in the scalar path).
+    int b_r[4], b_s[4], b_c[4];
+    bool b_cok[4];
+#pragma unroll
+    for (int f = 0; f < FB; ++f) {
+        int idx = t + NTHR * f;
+        if (B_KC) {
+            b_row[f] = idx / (KT / 4);
+            b_kc = idx % (KT / 4);
+        } else {
+            b_row[f] = idx / (NT / 4);
+            b_kc = idx % (NT / 4);
+        }
+    }
+    if (PASS == PASS_WGRAD) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            int kk = tn * NT + 4 * b_kc + e;
+            b_cok[e] = kk < a.Ng;
+            int k2 = b_cok[e] ? kk : 0;
+            int rs = a.fC.div(k2);
+            b_c[e] = k2 - rs * a.C;
+            b_r[e] = a.fS.div(rs);
+            b_s[e] = rs - b_r[e] * a.S;
+        }
+    }
+
+    float4 ra[FA], rb[FB];
+
+    // ------------------------------------------------ global -> registers
+    auto load_a = [&](int kt) {
+        const int kbase = kt * KT;
+        if (PASS == PASS_FWD) {
+            if (AV) {
+                int kk = kbase + 4 * a_kc;
+                bool kok = kk < Kg;
+                int k2 = kok ? kk : 0;
+                int rs = a.fC.div(k2);
+                int c = k2 - rs * a.C;
+                int r = a.fS.div(rs);
+                int s = rs - r * a.S;
+#pragma unroll
+                for (int f = 0; f < FA; ++f) {
+                    int h = a_h[f] + r, w = a_w[f] + s;
+                    bool ok = kok && a_ok[f] && (unsigned)h < (unsigned)a.H && (unsigned)w < (unsigned)a.W;
+                    ra[f] = ok ? ld4(a.A + (((size_t)a_n[f] * a.H + h) * a.W + w) * a.C + c)
+                               : make_float4(0.f, 0.f, 0.f, 0.f);
+                }
+            } else {
+                float v[4][FA];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    int kk = kbase + 4 * a_kc + e;
+                    bool kok = kk < Kg;
+                    int k2 = kok ? kk : 0;
+                    int rs = a.fC.div(k2);
+                    int c = k2 - rs * a.C;
+                    int r = a.fS.div(rs);
+                    int s = rs - r * a.S;
+#pragma unroll
+                    for (int f = 0; f < FA; ++f) {
+                        int h = a_h[f] + r, w = a_w[f] + s;
+                        bool ok = kok && a_ok[f] && (unsigned)h < (unsigned)a.H && (unsigned)w < (unsigned)a.W;
+                        v[e][f] = ok ? a.A[(((size_t)a_n[f] * a.H + h) * a.W + w) * a.C + c] : 0.f;
+                    }
+                }
+#pragma unroll
+                for (int f = 0; f < FA; ++f)
+                    ra[f] = make_float4(v[0][f], v[1][f], v[2][f], v[3][f]);
+            }
+        } else if (PASS == PASS_DGRAD) {
+            // kk = (tr, ts, k) with k fastest
+            float v[4][FA];
+            const int nel = AV ? 1 : 4;
+#pragma unroll
+            for (int e = 0; e < nel; ++e) {
+                int kk = kbase + 4 * a_kc + e;
+                bool kok = kk < Kg;
+                int k2 = kok ? kk : 0;
+                int tt = a.fK.div(k2);
+                int k = k2 - tt * a.K;
+                int tr = ph.St ? tt / ph.St : 0;
+                int ts = tt - tr * ph.St;
+#pragma unroll
+                for (int f = 0; f < FA; ++f) {
+                    int p = a_h[f] - tr, q = a_w[f] - ts;
+                    bool ok = kok && a_ok[f] && (unsigned)p < (unsigned)a.P && (unsigned)q < (unsigned)a.Q;
+                    const float *src = a.A + (((size_t)a_n[f] * a.P + p) * a.Q + q) * a.K + k;
+                    if (AV) {
+                        ra[f] = ok ? ld4(src) : make_float4(0.f, 0.f, 0.f, 0.f);
+                    } else {
+                        v[e][f] = ok ? *src : 0.f;
+                    }
+                }
+            }
+            if (!AV) {
+#pragma unroll
+                for (int f = 0; f < FA; ++f)
+                    ra[f] = make_float4(v[0][f], v[1][f], v[2][f], v[3][f]);
+            }
+        } else { // WGRAD: A = dY^T, rows are output channels (contiguous), k = pixel
+#pragma unroll
+            for (int f = 0; f < FA; ++f) {
+                int mp = kbase + a_row[f];
+                int ko = tm * MT + 4 * a_kc;
+                const float *src = a.A + (size_t)mp * a.K + ko;
+                bool pok = mp < Kg;
+                if (AV) {
+                    ra[f] = (pok && ko < a.M) ? ld4(src) : make_float4(0.f, 0.f, 0.f, 0.f);
+                } else {
+                    float v0 = (pok && ko + 0 < a.M) ? src[0] : 0.f;
+                    float v1 = (pok && ko + 1 < a.M) ? src[1] : 0.f;
+                    float v2 = (pok && ko + 2 < a.M) ? src[2] : 0.f;
+                    float v3 = (pok && ko + 3 < a.M) ? src[3] : 0.f;
+                    ra[f] = make_float4(v0, v1, v2, v3);
+                }
+            }
+        }
+    };
+
+    auto load_b = [&](int kt) {
+        const int kbase = kt * KT;
+        if (PASS == PASS_FWD) { // B = W[k][kk], k-contiguous
+#pragma unroll
+            for (int f = 0; f < FB; ++f) {
+                int j = tn * NT + b_row[f];
+                int kk = kbase + 4 * b_kc;
+                const float *src = a.B + (size_t)j * a.Kg + kk;
+                bool jok = j < a.Ng;
+                if (BV) {
+                    rb[f] = (jok && kk < Kg) ? ld4(src) : make_float4(0.f, 0.f, 0.f, 0.f);
+                } else {
+                    float v0 = (jok && kk + 0 < Kg) ? src[0] : 0.f;
+                    float v1 = (jok && kk + 1 < Kg) ? src[1] : 0.f;
+                    float v2 = (jok && kk + 2 < Kg) ? src[2] : 0.f;
+                    float v3 = (jok && kk + 3 < Kg) ? src[3] : 0.f;
+                    rb[f] = make_float4(v0, v1, v2, v3);
+                }
+            }
+        } else if (PASS == PASS_DGRAD) { // B[kk][c] = W[k][r][s][c], c contiguous
+#pragma unroll
+            for (int f = 0; f < FB; ++f) {
+                int kk = kbase + b_row[f];
+                bool kok = kk < Kg;
+                int k2 = kok ? kk : 0;
+                int tt = a.fK.div(k2);
+                int k = k2 - tt * a.K;
+                int tr = ph.St ? tt / ph.St : 0;
+                int ts = tt - tr * ph.St;
+                int r = ph.r0 + a.st * tr, s = ph.s0 + a.st * ts;
+                int c = tn * NT + 4 * b_kc;
+                const float *src = a.B + (((size_t)k * a.R + r) * a.S + s) * a.C + c;
+                if (BV) {
+                    rb[f] = (kok && c < a.C) ? ld4(src) : make_float4(0.f, 0.f, 0.f, 0.f);
+                } else {
+                    float v0 = (kok && c + 0 < a.C) ? src[0] : 0.f;
+                    float v1 = (kok && c + 1 < a.C) ? src[1] : 0.f;
+                    float v2 = (kok && c + 2 < a.C) ? src[2] : 0.f;
+                    float v3 = (kok && c + 3 < a.C) ? src[3] : 0.f;
+                    rb[f] = make_float4(v0, v1, v2, v3);
+                }
+            }
+        } else { // WGRAD: B[pixel][kk] = X~, c contiguous within a tap
+#pragma unroll
+            for (int f = 0; f < FB; ++f) {
+                int mp = kbase + b_row[f];
+                bool pok = mp < Kg;
+                int m2 = pok ? mp : 0;
+                int n = a.fPQ.div(m2);
+                int rem = m2 - n * a.P * a.Q;
+                int p = a.fQ.div(rem);
+                int q = rem - p * a.Q;
+                int hb = p * a.st - a.pad, wb = q * a.st - a.pad;
+                if (BV) {
+                    int h = hb + b_r[0], w = wb + b_s[0];
+                    bool ok = pok && b_cok[0] && (unsigned)h < (unsigned)a.H && (unsigned)w < (unsigned)a.W;
+                    rb[f] = ok ? ld4(a.B + (((size_t)n * a.H + h) * a.W + w) * a.C + b_c[0])
+                               : make_float4(0.f, 0.f, 0.f, 0.f);
+                } else {
+                    float v[4];
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        int h = hb + b_r[e], w = wb + b_s[e];
+                        bool ok = pok && b_cok[e] && (unsigned)h < (unsigned)a.H && (unsigned)w < (unsigned)a.W;
+                        v[e] = ok ? a.B[(((size_t)n * a.H + h) * a.W + w) * a.C + b_c[e]] : 0.f;
+                    }
+                    rb[f] = make_float4(v[0], v[1], v[2], v[3]);
+                }
+            }
+        }
+    };
+
+    // ------------------------------------------------ registers -> LDS
+    auto store = [&](int buf) {
+        float *As = lds + buf * (A_SZ + B_SZ);
+        float *Bs = As + A_SZ;
+#pragma unroll
+        for (int f = 0; f < FA; ++f)
+            st4(As + a_row[f] * A_LD + 4 * a_kc, ra[f]);
+#pragma unroll
+        for (int f = 0; f < FB; ++f)
+            st4(Bs + b_row[f] * B_LD + 4 * b_kc, rb[f]);
+    };
+
+    // ------------------------------------------------ MFMA on one stage
+    const int wave = t >> 6, lane = t & 63;
+    const int lr = lane & 31, lh = lane >> 5;
+    const int wm = (wave & 1) * (MT / 2), wn = (wave >> 1) * (NT / 2);
+    f32x16 acc[BM][BN];
+#pragma unroll
+    for (int i = 0; i < BM; ++i)
+#pragma unroll
+        for (int j = 0; j < BN; ++j)
+#pragma unroll
+            for (int v = 0; v < 16; ++v)
+                acc[i][j][v] = 0.f;
+
+    // Within a stage, lane half lh multiplies k = lh*KT/2 + step: any fixed
+    // bijection of k is a valid order for the sum, and this one lets a lane
+    // read its KT/2 values of a k-contiguous row with two ds_read_b128.
+    auto compute = [&](int buf) {
+        const float *As = lds + buf * (A_SZ + B_SZ);
+        const float *Bs = As + A_SZ;
+        float av[BM][KT / 2], bv[BN][KT / 2];
+#pragma unroll
+        for (int i = 0; i < BM; ++i) {
+            int row = wm + 32 * i + lr;
+            if (A_KC) {
+#pragma unroll
+                for (int q4 = 0; q4 < KT / 8; ++q4) {
+                    float4 x = ld4(As + row * A_LD + lh * (KT / 2) + 4 * q4);
+                    av[i][4 * q4 + 0] = x.x;
+                    av[i][4 * q4 + 1] = x.y;
+                    av[i][4 * q4 + 2] = x.z;
+                    av[i][4 * q4 + 3] = x.w;
+                }
+            } else {
+#pragma unroll
+                for (int st = 0; st < KT / 2; ++st)
+                    av[i][st] = As[(lh * (KT / 2) + st) * A_LD + row];
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < BN; ++j) {
+            int col = wn + 32 * j + lr;
+            if (B_KC) {
+#pragma unroll
+                for (int q4 = 0; q4 < KT / 8; ++q4) {
+                    float4 x = ld4(Bs + col * B_LD + lh * (KT / 2) + 4 * q4);
+                    bv[j][4 * q4 + 0] = x.x;
+                    bv[j][4 * q4 + 1] = x.y;
+                    bv[j][4 * q4 + 2] = x.z;
+                    bv[j][4 * q4 + 3] = x.w;
+                }
+            } else {
+#pragma unroll
+                for (int st = 0; st < KT / 2; ++st)
+                    bv[j][st] = Bs[(lh * (KT / 2) + st) * B_LD + col];
+            }
+        }
+#pragma unroll
+        for (int st = 0; st < KT / 2; ++st)
+#pragma unroll
+            for (int i = 0; i < BM; ++i)
+#pragma unroll
+                for (int j = 0; j < BN; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[i][st], bv[j][st], acc[i][j], 0, 0, 0);
+    };
+
+    // ------------------------------------------------ pipeline
+    int buf = 0;
+    if (nkt > 0) {
+        load_a(kt0);
+        load_b(kt0);
+        store(0);
+    }
+    __syncthreads();
+    for (int it = 0; it < nkt; ++it) {
+        const bool more = it + 1 < nkt;
+        if (more) {
+            load_a(kt0 + it + 1);
+            load_b(kt0 + it + 1);
+        }
+        compute(buf);
+        if (more)
+            store(buf ^ 1);
+        __syncthreads();
+        buf ^= 1;
+    }
+
+    // ------------------------------------------------ epilogue
+    // 32x32 accumulator layout: element v of lane l is row
+    // 8*(v/4) + 4*(l/32) + v%4 and column l%32 of the block.
+    const int Ng = a.Ng;
+#pragma unroll
+    for (int i = 0; i < BM; ++i) {
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+            int m = tm * MT + wm + 32 * i + 8 * (v >> 2) + 4 * lh + (v & 3);
+            if (m >= M)
+                continue;
+            if (a.splits > 1) {
+                float *dst = a.partial + ((size_t)(z * a.splits + split) * a.M + m) * Ng;
+#pragma unroll
+                for (int j = 0; j < BN; ++j) {
+                    int n = tn * NT + wn + 32 * j + lr;
+                    if (n < Ng)
+                        dst[n] = acc[i][j][v];
+                }
+            } else {
+                float *dst = a.out + out_row(a, PASS, ph, z, m);
+#pragma unroll
+                for (int j = 0; j < BN; ++j) {
+                    int n = tn * NT + wn + 32 * j + lr;
+                    if (n < Ng)
+                        dst[n] = epilogue(a, PASS, acc[i][j][v], n, dst + n);
+                }
+            }
+        }
+    }
+}
+
+// Adds the split-K partial sums of each output in split order, then applies
+// the pass's epilogue.
+template <int PASS>
+__global__ __launch_bounds__(256) void splitk_reduce_kernel(Args a) {
+    const int z = blockIdx.y;
+    Phase ph{};
+    int M = a.M;
+    if (PASS == PASS_DGRAD) {
+        ph = make_phase(a, z);
+        M = ph.M;
+    }
+    const size_t total = (size_t)M * a.Ng;
+    for (size_t e = (size_t)blockIdx.x * blockDim.x + threadIdx.x; e < total;
+         e += (size_t)gridDim.x * blockDim.x) {
+        int m = (int)(e / a.Ng);
+        int n = (int)(e - (size_t)m * a.Ng);
+        float v = 0.f;
+        for (int s = 0; s < a.splits; ++s)
+            v += a.partial[((size_t)(z * a.splits + s) * a.M + m) * a.Ng + n];
+        float *dst = a.out + out_row(a, PASS, ph, z, m) + n;
+        *dst = epilogue(a, PASS, v, n, dst);
+    }
+}
+
+template <int PASS, int MT, int NT, bool AV, bool BV>
+void launch_t(const Args &a, int grid_x, int splits, int phases, hipStream_t s) {
+    hipLaunchKernelGGL((igemm_kernel<PASS, MT, NT, AV, BV>), dim3(grid_x, splits, phases), dim3(NTHR), 0, s, a);
+}
+
+template <int PASS, int MT, int NT>
+void launch_v(const Args &a, bool av, bool bv, int grid_x, int splits, int phases, hipStream_t s) {
+    if (av && bv)
+        launch_t<PASS, MT, NT, true, true>(a, grid_x, splits, phases, s);
+    else if (av)
+        launch_t<PASS, MT, NT, true, false>(a, grid_x, splits, phases, s);
+    else if (bv)
+        launch_t<PASS, MT, NT, false, true>(a, grid_x, splits, phases, s);
+    else
+        launch_t<PASS, MT, NT, false, false>(a, grid_x, splits, phases, s);
+}
+
+template <int PASS>
+void launch_p(const Args &a, const GemmPlan &pl, int grid_x, hipStream_t s) {
+    if (pl.mt == 128 && pl.nt == 128)
+        launch_v<PASS, 128, 128>(a, pl.av, pl.bv, grid_x, pl.splits, pl.phases, s);
+    else if (pl.mt == 128 && pl.nt == 64)
+        launch_v<PASS, 128, 64>(a, pl.av, pl.bv, grid_x, pl.splits, pl.phases, s);
+    else if (pl.mt == 64 && pl.nt == 128)
+        launch_v<PASS, 64, 128>(a, pl.av, pl.bv, grid_x, pl.splits, pl.phases, s);
+    else
+        launch_v<PASS, 64, 64>(a, pl.av, pl.bv, grid_x, pl.splits, pl.phases, s);
+}
+
+Args make_args(const ConvGeom &g, const GemmPlan &pl) {
+    Args a{};
+    a.N = g.N; a.H = g.H; a.W = g.W; a.C = g.C; a.K = g.K; a.R = g.R; a.S = g.S;
+    a.st = g.st; a.pad = g.pad; a.P = g.P; a.Q = g.Q;
+    a.M = pl.M; a.Ng = pl.Ng; a.Kg = pl.Kg;
+    a.tiles_m = pl.tiles_m; a.tiles_n = pl.tiles_n; a.tiles = pl.tiles_m * pl.tiles_n;
+    a.splits = pl.splits; a.kt_per_split = pl.kt_per_split;
+    a.fC = make_fdiv(g.C); a.fS = make_fdiv(g.S); a.fK = make_fdiv(g.K);
+    a.fQ = make_fdiv(g.Q); a.fPQ = make_fdiv(g.P * g.Q);
+    return a;
+}
+
+int run(const ConvGeom &g, const GemmPlan &pl, Args a, void *ws, hipStream_t s) {
+    if ((int64_t)pl.M * pl.Ng == 0)
+        return DC_OK;
+    if (pl.splits > 1) {
+        if (!ws)
+            return fail(DC_EINVAL, "conv pass %d needs %zu bytes of workspace", pl.pass, pl.ws_bytes);
+        a.partial = static_cast<float *>(ws);
+    }
+    int tiles = pl.tiles_m * pl.tiles_n;
+    int grid_x = (tiles + 7) / 8 * 8;
+    switch (pl.pass) {
+    case PASS_FWD: launch_p<PASS_FWD>(a, pl, grid_x, s); break;
+    case PASS_DGRAD: launch_p<PASS_DGRAD>(a, pl, grid_x, s); break;
+    default: launch_p<PASS_WGRAD>(a, pl, grid_x, s); break;
+    }
+    DC_HIP(hipGetLastError());
+    if (pl.splits > 1) {
+        size_t total = (size_t)pl.M * pl.Ng;
+        int blocks = (int)std::min<size_t>((total + 255) / 256, 4096);
+        switch (pl.pass) {
+        case PASS_FWD: hipLaunchKernelGGL(splitk_reduce_kernel<PASS_FWD>, dim3(blocks, 1), dim3(256), 0, s, a); break;
+        case PASS_DGRAD: hipLaunchKernelGGL(splitk_reduce_kernel<PASS_DGRAD>, dim3(blocks, pl.phases), dim3(256), 0, s, a); break;
+        default: hipLaunchKernelGGL(splitk_reduce_kernel<PASS_WGRAD>, dim3(blocks, 1), dim3(256), 0, s, a); break;
+        }
+        DC_HIP(hipGetLastError());
+    }
+    return DC_OK;
+}
+
+} // namespace
+
+bool conv_geom_from_shape(const dc_conv_shape &sh, ConvGeom *g) {
+    if (sh.n < 0 || sh.h < 1 || sh.w < 1 || sh.c < 1 || sh.k < 1 || sh.r < 1 || sh.s < 1 ||
+        sh.stride < 1 || sh.pad < 0 || sh.pad >= sh.r || sh.pad >= sh.s)
+        return false;
+    if (sh.h + 2 * sh.pad < sh.r || sh.w + 2 * sh.pad < sh.s)
+        return false;
+    g->N = sh.n; g->H = sh.h; g->W = sh.w; g->C = sh.c; g->K = sh.k;
+    g->R = sh.r; g->S = sh.s; g->st = sh.stride; g->pad = sh.pad;
+    g->P = (sh.h + 2 * sh.pad - sh.r) / sh.stride + 1;
+    g->Q = (sh.w + 2 * sh.pad - sh.s) / sh.stride + 1;
+    // every index the kernels form must stay below 2^31
+    int64_t big = std::max<int64_t>({(int64_t)sh.n * sh.h * sh.w * sh.c, (int64_t)sh.n * g->P * g->Q * sh.k,
+                                     (int64_t)sh.k * sh.r * sh.s * sh.c});
+    return big < INT_MAX;
+}
+
+GemmPlan plan_gemm(const ConvGeom &g, int pass) {
+    GemmPlan pl{};
+    pl.pass = pass;
+    pl.phases = 1;
+    if (pass == PASS_FWD) {
+        pl.M = g.N * g.P * g.Q; pl.Ng = g.K; pl.Kg = g.R * g.S * g.C;
+        pl.av = g.C % 4 == 0;
+        pl.bv = (g.R * g.S * g.C) % 4 == 0;
+    } else if (pass == PASS_DGRAD) {
+        pl.phases = g.st * g.st;
+        int hh = (g.H + g.st - 1) / g.st, wh = (g.W + g.st - 1) / g.st;
+        int rt = (g.R + g.st - 1) / g.st, stt = (g.S + g.st - 1) / g.st;
+        pl.M = g.N * hh * wh; pl.Ng = g.C; pl.Kg = rt * stt * g.K;
+        pl.av = g.K % 4 == 0;
+        pl.bv = g.C % 4 == 0;
+    } else {
+        pl.M = g.K; pl.Ng = g.R * g.S * g.C; pl.Kg = g.N * g.P * g.Q;
+        pl.av = g.K % 4 == 0;
+        pl.bv = g.C % 4 == 0;
+    }
+    // Pick the tile and split-K factor with the least estimated time: a
+    // workgroup's time grows with its tile area and K range (smaller tiles
+    // run at lower MFMA efficiency), workgroups run ~2 per CU at once on 256
+    // CUs, and a split pays the partial-sum traffic of its reduction.
+    static const int cand[4][2] = {{128, 128}, {128, 64}, {64, 128}, {64, 64}};
+    static const double eff[4] = {1.0, 0.85, 0.85, 0.7};
+    const int ktiles = std::max(1, (pl.Kg + KT - 1) / KT);
+    double best = 1e300;
+    for (int c = 0; c < 4; ++c) {
+        int mt = cand[c][0], nt = cand[c][1];
+        int tm = (pl.M + mt - 1) / mt, tn = (pl.Ng + nt - 1) / nt;
+        int64_t tiles = (int64_t)tm * tn * pl.phases;
+        for (int sp = 1; sp <= 512; sp *= 2) {
+            if (sp > 1 && (ktiles / sp) < 8)
+                break;
+            int kps = (ktiles + sp - 1) / sp;
+            int spe = (ktiles + kps - 1) / kps;
+            int64_t wgs = tiles * spe;
+            int64_t rounds = (wgs + 511) / 512;
+            // cycles: 2*mt*nt*KT*kps flops at 256 flop/clk per CU, 2 WGs sharing a CU
+            double t_main = rounds * 2.0 * (2.0 * mt * nt * KT * kps) / (256.0 * eff[c]) / 2.4e3; // ns
+            double t_red = 0;
+            if (spe > 1)
+                t_red = 3000.0 + (double)(spe + 2) * pl.M * pl.Ng * pl.phases * 4.0 / 3000.0; // ns at ~3 TB/s
+            double cost = t_main + t_red;
+            if (cost < best * 0.98) {
+                best = cost;
+                pl.mt = mt; pl.nt = nt; pl.splits = spe; pl.kt_per_split = kps;
+                pl.tiles_m = tm; pl.tiles_n = tn;
+            }
+        }
+    }
+    pl.ws_bytes = pl.splits > 1 ? (size_t)pl.splits * pl.phases * pl.M * pl.Ng * sizeof(float) : 0;
+    return pl;
+}
+
+int conv_forward(const ConvGeom &g, const GemmPlan &pl, const float *x, const float *w,
+                 const float *bias, int relu, float *y, void *ws, hipStream_t s) {
+    Args a = make_args(g, pl);
+    a.A = x; a.B = w; a.out = y; a.bias = bias; a.relu = relu;
+    return run(g, pl, a, ws, s);
+}
+
+int conv_dgrad(const ConvGeom &g, const GemmPlan &pl, const float *dy, const float *w,
+               int accumulate, float *dx, void *ws, hipStream_t s) {
+    Args a = make_args(g, pl);
+    a.A = dy; a.B = w; a.out = dx; a.accumulate = accumulate;
+    return run(g, pl, a, ws, s);
+}
+
+int conv_wgrad(const ConvGeom &g, const GemmPlan &pl, const float *x, const float *dy, float *dw,
+               void *ws, hipStream_t s) {
+    Args a = make_args(g, pl);
+    a.A = dy; a.B = x; a.out = dw;
+    return run(g, pl, a, ws, s);
+}
+
+} // namespace dc

@@ -1,0 +1,535 @@
+// Model construction, workspace layout, the parameter server's buffers and
+// the per-layer forward / backward mini-procedures.
+//
+// A layer (Sec. III-A) is one weighted op plus the parameter-less ops after
+// it; its parameters are one contiguous range of the parameter vector, so a
+// pull or push segment of consecutive layers is one contiguous copy.  Every
+// tensor gets its own activation and gradient buffer in the caller's device
+// workspace; a tensor read by several ops receives the backward contributions
+// in reverse op order, the first one writing and the rest accumulating, so
+// the result never depends on timing.
+#include "runtime.h"
+
+#include <algorithm>
+#include <cstring>
+
+namespace dc {
+
+// ---------------------------------------------------------------- host pool
+
+HostPool::HostPool(int threads) {
+    for (int i = 1; i < threads; ++i)
+        workers_.emplace_back([this, i] { loop(i); });
+}
+
+HostPool::~HostPool() {
+    {
+        std::lock_guard<std::mutex> g(mu_);
+        stop_ = true;
+    }
+    cv_.notify_all();
+    for (auto &t : workers_)
+        t.join();
+}
+
+void HostPool::loop(int) {
+    long seen = 0;
+    for (;;) {
+        const std::function<void(int, int)> *job;
+        int n;
+        {
+            std::unique_lock<std::mutex> lk(mu_);
+            cv_.wait(lk, [&] { return stop_ || gen_ != seen; });
+            if (stop_)
+                return;
+            seen = gen_;
+            job = job_;
+            n = job_n_;
+            ++active_;
+        }
+        for (;;) {
+            int i;
+            {
+                std::lock_guard<std::mutex> g(mu_);
+                i = next_ < n ? next_++ : -1;
+            }
+            if (i < 0)
+                break;
+            (*job)(i, n);
+        }
+        {
+            std::lock_guard<std::mutex> g(mu_);
+            --active_;
+        }
+        done_cv_.notify_all();
+    }
+}
+
+void HostPool::run(int n, const std::function<void(int, int)> &fn) {
+    if (workers_.empty() || n <= 1) {
+        for (int i = 0; i < n; ++i)
+            fn(i, n);
+        return;
+    }
+    {
+        std::lock_guard<std::mutex> g(mu_);
+        job_ = &fn;
+        job_n_ = n;
+        next_ = 0;
+        ++gen_;
+    }
+    cv_.notify_all();
+    for (;;) {
+        int i;
+        {
+            std::lock_guard<std::mutex> g(mu_);
+            i = next_ < n ? next_++ : -1;
+        }
+        if (i < 0)
+            break;
+        fn(i, n);
+    }
+    std::unique_lock<std::mutex> lk(mu_);
+    done_cv_.wait(lk, [&] { return active_ == 0 && next_ >= n; });
+    job_ = nullptr;
+}
+
+namespace {
+
+size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+int check_desc(const dc_op_desc *ops, int n_ops, int batch, int in_h, int in_w, int in_c, int classes) {
+    if (!ops || n_ops < 1)
+        return fail(DC_EINVAL, "no operations");
+    if (batch < 1 || in_h < 1 || in_w < 1 || in_c < 1 || classes < 1)
+        return fail(DC_EINVAL, "batch and input sizes must be positive");
+    int prev_layer = 0;
+    for (int i = 0; i < n_ops; ++i) {
+        const dc_op_desc &d = ops[i];
+        if (d.kind < DC_OP_CONV || d.kind > DC_OP_ADD)
+            return fail(DC_EINVAL, "op %d: unknown kind %d", i, d.kind);
+        if (d.in0 < 0 || d.in0 > i)
+            return fail(DC_EINVAL, "op %d: input tensor %d is not an earlier tensor", i, d.in0);
+        if (d.kind == DC_OP_ADD && (d.in1 < 0 || d.in1 > i))
+            return fail(DC_EINVAL, "op %d: second input tensor %d is not an earlier tensor", i, d.in1);
+        if (d.layer != prev_layer && d.layer != prev_layer + 1)
+            return fail(DC_EINVAL, "op %d: layers must be contiguous and non-decreasing", i);
+        bool weighted = d.kind == DC_OP_CONV || d.kind == DC_OP_FC;
+        if (d.layer == prev_layer + 1 && !weighted)
+            return fail(DC_EINVAL, "op %d: layer %d must start with a CONV or FC op", i, d.layer);
+        prev_layer = d.layer;
+    }
+    if (ops[0].layer != 1)
+        return fail(DC_EINVAL, "the first op must belong to layer 1");
+    return DC_OK;
+}
+
+} // namespace
+
+static int build_model(dc_model *m, const dc_op_desc *ops, int n_ops) {
+    m->ops.resize(n_ops);
+    m->tensors.resize(n_ops + 1);
+    m->tensors[0] = TensorInfo{m->batch, m->in_h, m->in_w, m->in_c};
+    size_t poff = 0;
+    m->L = ops[n_ops - 1].layer;
+    m->layer_off.assign(m->L + 2, 0);
+    m->layer_cnt.assign(m->L + 2, 0);
+    m->layer_first.assign(m->L + 2, -1);
+    m->layer_last.assign(m->L + 2, -1);
+    for (int i = 0; i < n_ops; ++i) {
+        OpInfo &o = m->ops[i];
+        o.d = ops[i];
+        o.out = i + 1;
+        const TensorInfo in = m->tensors[o.d.in0];
+        TensorInfo out = in;
+        int l = o.d.layer;
+        if (m->layer_first[l] < 0) {
+            m->layer_first[l] = i;
+            m->layer_off[l] = poff;
+        }
+        m->layer_last[l] = i;
+        size_t start = poff;
+        switch (o.d.kind) {
+        case DC_OP_CONV:
+        case DC_OP_FC: {
+            dc_conv_shape sh;
+            if (o.d.kind == DC_OP_CONV) {
+                sh = dc_conv_shape{in.n, in.h, in.w, in.c, o.d.out_ch, o.d.r, o.d.s, o.d.stride, o.d.pad};
+            } else {
+                sh = dc_conv_shape{in.n, 1, 1, in.h * in.w * in.c, o.d.out_ch, 1, 1, 1, 0};
+            }
+            if (o.d.out_ch < 1 || !conv_geom_from_shape(sh, &o.geom))
+                return fail(DC_EINVAL, "op %d: invalid %s geometry", i, o.d.kind == DC_OP_CONV ? "conv" : "fc");
+            o.fwd = plan_gemm(o.geom, PASS_FWD);
+            o.dgrad = plan_gemm(o.geom, PASS_DGRAD);
+            o.wgrad = plan_gemm(o.geom, PASS_WGRAD);
+            o.w_off = poff;
+            poff += (size_t)o.geom.K * o.geom.R * o.geom.S * o.geom.C;
+            if (o.d.bias) {
+                o.b_off = poff;
+                poff += o.geom.K;
+            }
+            if (o.d.kind == DC_OP_CONV)
+                out = TensorInfo{in.n, o.geom.P, o.geom.Q, o.geom.K};
+            else
+                out = TensorInfo{in.n, 1, 1, o.geom.K};
+            break;
+        }
+        case DC_OP_BN:
+            o.w_off = poff;          // gamma
+            o.b_off = poff + in.c;   // beta
+            poff += 2 * (size_t)in.c;
+            break;
+        case DC_OP_RELU:
+            break;
+        case DC_OP_MAXPOOL: {
+            if (o.d.r < 1 || o.d.s < 1 || o.d.stride < 1 || o.d.pad < 0 || o.d.pad >= o.d.r || o.d.pad >= o.d.s ||
+                o.d.r * o.d.s > 256 || in.h + 2 * o.d.pad < o.d.r || in.w + 2 * o.d.pad < o.d.s)
+                return fail(DC_EINVAL, "op %d: invalid max-pool geometry", i);
+            o.pool = dc_pool_shape{in.n, in.h, in.w, in.c, o.d.r, o.d.s, o.d.stride, o.d.pad};
+            out.h = (in.h + 2 * o.d.pad - o.d.r) / o.d.stride + 1;
+            out.w = (in.w + 2 * o.d.pad - o.d.s) / o.d.stride + 1;
+            break;
+        }
+        case DC_OP_GAP:
+            out.h = out.w = 1;
+            break;
+        case DC_OP_ADD: {
+            const TensorInfo &b = m->tensors[o.d.in1];
+            if (b.n != in.n || b.h != in.h || b.w != in.w || b.c != in.c)
+                return fail(DC_EINVAL, "op %d: ADD inputs differ in shape", i);
+            break;
+        }
+        }
+        m->layer_cnt[l] += poff - start;
+        m->tensors[o.out] = out;
+    }
+    for (int l = 1; l <= m->L; ++l)
+        if (m->layer_cnt[l] == 0)
+            return fail(DC_EINVAL, "layer %d has no parameters", l);
+    const TensorInfo &lg = m->tensors[n_ops];
+    if (lg.h != 1 || lg.w != 1 || lg.c != m->classes)
+        return fail(DC_EINVAL, "the last op must produce N x 1 x 1 x classes logits");
+    m->n_params = poff;
+
+    // backward: which input gradients are needed and whether they accumulate
+    std::vector<char> written(n_ops + 1, 0);
+    for (int i = n_ops - 1; i >= 0; --i) {
+        OpInfo &o = m->ops[i];
+        int ins[2] = {o.d.in0, o.d.kind == DC_OP_ADD ? o.d.in1 : -1};
+        for (int k = 0; k < 2; ++k) {
+            int t = ins[k];
+            if (t <= 0)
+                continue; // the input batch needs no gradient
+            bool &g = k == 0 ? o.grad_in0 : o.grad_in1;
+            int &acc = k == 0 ? o.acc_in0 : o.acc_in1;
+            g = true;
+            acc = written[t] ? 1 : 0;
+            written[t] = 1;
+        }
+    }
+    for (int t = 1; t <= n_ops; ++t)
+        if (!written[t] && t != n_ops)
+            return fail(DC_EINVAL, "tensor %d is never used", t);
+
+    // workspace layout
+    size_t off = 0;
+    auto take = [&](size_t bytes) {
+        size_t o = off;
+        off = align_up(off + std::max<size_t>(bytes, 1), 256);
+        return o;
+    };
+    m->off_params = take(m->n_params * sizeof(float));
+    m->off_grads = take(m->n_params * sizeof(float));
+    for (int t = 1; t <= n_ops; ++t) {
+        m->tensors[t].act = take((size_t)m->tensors[t].size() * sizeof(float));
+        m->tensors[t].grad = take((size_t)m->tensors[t].size() * sizeof(float));
+    }
+    size_t scratch = xent_ws_bytes(m->batch);
+    for (int i = 0; i < n_ops; ++i) {
+        OpInfo &o = m->ops[i];
+        const TensorInfo &in = m->tensors[o.d.in0];
+        const TensorInfo &out = m->tensors[o.out];
+        if (o.d.kind == DC_OP_CONV || o.d.kind == DC_OP_FC) {
+            scratch = std::max({scratch, o.fwd.ws_bytes, o.dgrad.ws_bytes, o.wgrad.ws_bytes});
+            if (o.d.bias)
+                scratch = std::max(scratch, colsum_ws_bytes((int64_t)out.n * out.h * out.w, out.c));
+        } else if (o.d.kind == DC_OP_BN) {
+            o.aux = take(2 * (size_t)in.c * sizeof(float));
+            scratch = std::max(scratch, bn_ws_bytes((int64_t)in.n * in.h * in.w, in.c));
+        } else if (o.d.kind == DC_OP_MAXPOOL) {
+            o.aux = take((size_t)out.size());
+        }
+    }
+    m->scratch_bytes = scratch;
+    m->off_scratch = take(scratch);
+    m->off_loss = take(sizeof(float));
+    m->off_slots = take(sizeof(uint64_t) * 2 * (m->L + 1));
+    m->ws_need = off;
+    return DC_OK;
+}
+
+// ---------------------------------------------------------------- mini-procedures
+
+int run_forward_layer(dc_model *m, int l, const float *x, const int32_t *y, hipStream_t s) {
+    const float *P = m->dparams();
+    for (int i = m->layer_first[l]; i <= m->layer_last[l]; ++i) {
+        OpInfo &o = m->ops[i];
+        const float *in = o.d.in0 == 0 ? x : m->act(o.d.in0);
+        float *out = m->act(o.out);
+        const TensorInfo &ti = m->tensors[o.d.in0];
+        switch (o.d.kind) {
+        case DC_OP_CONV:
+        case DC_OP_FC:
+            DC_TRY(conv_forward(o.geom, o.fwd, in, P + o.w_off, o.b_off != NONE ? P + o.b_off : nullptr, 0, out,
+                                m->scratch(), s));
+            break;
+        case DC_OP_BN: {
+            float *mean = reinterpret_cast<float *>(m->ws + o.aux);
+            DC_TRY(bn_forward((int64_t)ti.n * ti.h * ti.w, ti.c, in, P + o.w_off, P + o.b_off, 1e-5f, 0, out, mean,
+                              mean + ti.c, m->scratch(), s));
+            break;
+        }
+        case DC_OP_RELU:
+            DC_TRY(relu_forward(in, out, ti.size(), s));
+            break;
+        case DC_OP_MAXPOOL:
+            DC_TRY(maxpool_forward(o.pool, in, out, reinterpret_cast<uint8_t *>(m->ws + o.aux), s));
+            break;
+        case DC_OP_GAP:
+            DC_TRY(gap_forward(ti.n, ti.h * ti.w, ti.c, in, out, s));
+            break;
+        case DC_OP_ADD:
+            DC_TRY(add_forward(in, m->act(o.d.in1), 0, out, ti.size(), s));
+            break;
+        }
+    }
+    if (l == m->L) {
+        int last = (int)m->ops.size();
+        DC_TRY(softmax_xent(m->batch, m->classes, m->act(last), y, m->dloss(), m->grad(last), m->scratch(), s));
+    }
+    return DC_OK;
+}
+
+int run_backward_layer(dc_model *m, int l, const float *x, hipStream_t s) {
+    const float *P = m->dparams();
+    float *G = m->dgrads();
+    for (int i = m->layer_last[l]; i >= m->layer_first[l]; --i) {
+        OpInfo &o = m->ops[i];
+        const float *in = o.d.in0 == 0 ? x : m->act(o.d.in0);
+        const float *dy = m->grad(o.out);
+        float *dx = o.grad_in0 ? m->grad(o.d.in0) : nullptr;
+        const TensorInfo &ti = m->tensors[o.d.in0];
+        const TensorInfo &to = m->tensors[o.out];
+        switch (o.d.kind) {
+        case DC_OP_CONV:
+        case DC_OP_FC:
+            DC_TRY(conv_wgrad(o.geom, o.wgrad, in, dy, G + o.w_off, m->scratch(), s));
+            if (o.b_off != NONE)
+                DC_TRY(colsum((int64_t)to.n * to.h * to.w, to.c, dy, G + o.b_off, m->scratch(), s));
+            if (dx)
+                DC_TRY(conv_dgrad(o.geom, o.dgrad, dy, P + o.w_off, o.acc_in0, dx, m->scratch(), s));
+            break;
+        case DC_OP_BN: {
+            const float *mean = reinterpret_cast<const float *>(m->ws + o.aux);
+            DC_TRY(bn_backward((int64_t)ti.n * ti.h * ti.w, ti.c, dy, in, P + o.w_off, mean, mean + ti.c, o.acc_in0,
+                               dx, G + o.w_off, G + o.b_off, m->scratch(), s));
+            break;
+        }
+        case DC_OP_RELU:
+            DC_TRY(relu_backward(dy, m->act(o.out), o.acc_in0, dx, ti.size(), s));
+            break;
+        case DC_OP_MAXPOOL:
+            DC_TRY(maxpool_backward(o.pool, dy, reinterpret_cast<const uint8_t *>(m->ws + o.aux), o.acc_in0, dx, s));
+            break;
+        case DC_OP_GAP:
+            DC_TRY(gap_backward(ti.n, ti.h * ti.w, ti.c, dy, o.acc_in0, dx, s));
+            break;
+        case DC_OP_ADD:
+            DC_TRY(copy_grad(dy, o.acc_in0, dx, ti.size(), s));
+            DC_TRY(copy_grad(dy, o.acc_in1, m->grad(o.d.in1), ti.size(), s));
+            break;
+        }
+    }
+    return DC_OK;
+}
+
+} // namespace dc
+
+// ---------------------------------------------------------------- C ABI: model and parameter server
+
+using namespace dc;
+
+extern "C" int dc_model_create(const dc_op_desc *ops, int n_ops, int batch, int in_h, int in_w, int in_c,
+                               int classes, dc_model **out) {
+    clear_error();
+    if (!out)
+        return fail(DC_EINVAL, "out is NULL");
+    *out = nullptr;
+    DC_TRY(check_desc(ops, n_ops, batch, in_h, in_w, in_c, classes));
+    dc_model *m = new (std::nothrow) dc_model();
+    if (!m)
+        return fail(DC_ENOMEM, "out of host memory");
+    m->batch = batch;
+    m->in_h = in_h;
+    m->in_w = in_w;
+    m->in_c = in_c;
+    m->classes = classes;
+    int st = build_model(m, ops, n_ops);
+    if (st != DC_OK) {
+        delete m;
+        return st;
+    }
+    auto cleanup = [&](int code) {
+        dc_model_destroy(m);
+        return code;
+    };
+    hipError_t e = hipGetDevice(&m->device);
+    if (e != hipSuccess)
+        return cleanup(hip_fail(e, "hipGetDevice"));
+    const size_t pbytes = std::max<size_t>(m->n_params * sizeof(float), 256);
+    if ((e = hipHostMalloc((void **)&m->ps_params, pbytes, hipHostMallocDefault)) != hipSuccess)
+        return cleanup(hip_fail(e, "hipHostMalloc(parameters)"));
+    if ((e = hipHostMalloc((void **)&m->ps_grads, pbytes, hipHostMallocDefault)) != hipSuccess)
+        return cleanup(hip_fail(e, "hipHostMalloc(gradients)"));
+    std::memset(m->ps_params, 0, pbytes);
+    std::memset(m->ps_grads, 0, pbytes);
+    m->probe_bytes = 16u << 20;
+    if ((e = hipHostMalloc((void **)&m->probe_host, m->probe_bytes, hipHostMallocDefault)) != hipSuccess)
+        return cleanup(hip_fail(e, "hipHostMalloc(probe)"));
+    if ((e = hipStreamCreateWithFlags(&m->pull_s, hipStreamNonBlocking)) != hipSuccess)
+        return cleanup(hip_fail(e, "hipStreamCreate(pull)"));
+    if ((e = hipStreamCreateWithFlags(&m->push_s, hipStreamNonBlocking)) != hipSuccess)
+        return cleanup(hip_fail(e, "hipStreamCreate(push)"));
+    auto mk = [&](std::vector<hipEvent_t> &v, int n) -> hipError_t {
+        v.assign(n, nullptr);
+        for (auto &ev : v) {
+            hipError_t r = hipEventCreate(&ev);
+            if (r != hipSuccess)
+                return r;
+        }
+        return hipSuccess;
+    };
+    const int L = m->L;
+    for (auto *v : {&m->ev_pull_start, &m->ev_pull_done, &m->ev_bwd_done, &m->ev_push_start, &m->ev_push_done})
+        if ((e = mk(*v, L)) != hipSuccess)
+            return cleanup(hip_fail(e, "hipEventCreate"));
+    for (auto *v : {&m->ev_fwd_start, &m->ev_fwd_end, &m->ev_bwd_end})
+        if ((e = mk(*v, L + 2)) != hipSuccess)
+            return cleanup(hip_fail(e, "hipEventCreate"));
+    if ((e = hipEventCreate(&m->ev_t0)) != hipSuccess)
+        return cleanup(hip_fail(e, "hipEventCreate"));
+    int wall = wall_clock_hz(&m->wall_hz);
+    if (wall != DC_OK)
+        return cleanup(wall);
+    unsigned hw = std::thread::hardware_concurrency();
+    m->sgd_threads = (int)std::max(1u, std::min(hw ? hw : 1u, 16u));
+    m->pool = new HostPool(m->sgd_threads);
+    *out = m;
+    return DC_OK;
+}
+
+extern "C" void dc_model_destroy(dc_model *m) {
+    if (!m)
+        return;
+    if (m->pull_s)
+        (void)hipStreamSynchronize(m->pull_s);
+    if (m->push_s)
+        (void)hipStreamSynchronize(m->push_s);
+    for (auto *v : {&m->ev_pull_start, &m->ev_pull_done, &m->ev_bwd_done, &m->ev_push_start, &m->ev_push_done,
+                    &m->ev_fwd_start, &m->ev_fwd_end, &m->ev_bwd_end})
+        for (auto ev : *v)
+            if (ev)
+                (void)hipEventDestroy(ev);
+    if (m->ev_t0)
+        (void)hipEventDestroy(m->ev_t0);
+    if (m->pull_s)
+        (void)hipStreamDestroy(m->pull_s);
+    if (m->push_s)
+        (void)hipStreamDestroy(m->push_s);
+    if (m->ps_params)
+        (void)hipHostFree(m->ps_params);
+    if (m->ps_grads)
+        (void)hipHostFree(m->ps_grads);
+    if (m->probe_host)
+        (void)hipHostFree(m->probe_host);
+    delete m->pool;
+    delete m;
+}
+
+extern "C" int dc_model_num_layers(const dc_model *m) { return m ? m->L : 0; }
+extern "C" size_t dc_model_num_params(const dc_model *m) { return m ? m->n_params : 0; }
+extern "C" size_t dc_workspace_bytes(const dc_model *m) { return m ? m->ws_need : 0; }
+
+extern "C" int dc_model_bind_workspace(dc_model *m, void *dev, size_t bytes) {
+    clear_error();
+    if (!m || !dev)
+        return fail(DC_EINVAL, "model or workspace is NULL");
+    if ((uintptr_t)dev % 256 != 0)
+        return fail(DC_EINVAL, "workspace must be 256-byte aligned");
+    if (bytes < m->ws_need)
+        return fail(DC_ENOMEM, "workspace has %zu bytes, the model needs %zu", bytes, m->ws_need);
+    m->ws = static_cast<char *>(dev);
+    m->ws_bytes = bytes;
+    return DC_OK;
+}
+
+extern "C" int dc_layer_range(const dc_model *m, int layer, size_t *off, size_t *count) {
+    clear_error();
+    if (!m || layer < 1 || layer > m->L)
+        return fail(DC_EINVAL, "layer %d out of range", layer);
+    if (off)
+        *off = m->layer_off[layer];
+    if (count)
+        *count = m->layer_cnt[layer];
+    return DC_OK;
+}
+
+extern "C" int dc_model_set_option(dc_model *m, int option, double value) {
+    clear_error();
+    if (!m)
+        return fail(DC_EINVAL, "model is NULL");
+    switch (option) {
+    case DC_OPT_LR:
+        m->lr = value;
+        return DC_OK;
+    case DC_OPT_TIMELINE:
+        m->timeline = value != 0.0;
+        return DC_OK;
+    case DC_OPT_TIMEOUT_S:
+        if (!(value > 0))
+            return fail(DC_EINVAL, "timeout must be positive");
+        m->timeout_s = value;
+        return DC_OK;
+    case DC_OPT_SGD_THREADS: {
+        int t = (int)value;
+        if (t < 1 || t > 256)
+            return fail(DC_EINVAL, "SGD threads must be in [1, 256]");
+        delete m->pool;
+        m->sgd_threads = t;
+        m->pool = new HostPool(t);
+        return DC_OK;
+    }
+    default:
+        return fail(DC_EINVAL, "unknown option %d", option);
+    }
+}
+
+extern "C" int dc_ps_write(dc_model *m, const float *host_params, size_t n) {
+    clear_error();
+    if (!m || !host_params || n != m->n_params)
+        return fail(DC_EINVAL, "dc_ps_write needs exactly %zu floats", m ? m->n_params : (size_t)0);
+    std::memcpy(m->ps_params, host_params, n * sizeof(float));
+    return DC_OK;
+}
+
+extern "C" int dc_ps_read(const dc_model *m, float *params_out, float *grads_out, size_t n) {
+    clear_error();
+    if (!m || n != m->n_params)
+        return fail(DC_EINVAL, "dc_ps_read needs exactly %zu floats", m ? m->n_params : (size_t)0);
+    if (params_out)
+        std::memcpy(params_out, m->ps_params, n * sizeof(float));
+    if (grads_out)
+        std::memcpy(grads_out, m->ps_grads, n * sizeof(float));
+    return DC_OK;
+}

@@ -1,0 +1,111 @@
+// The model object behind the dc_model handle of the C ABI.
+#pragma once
+
+#include "dc_internal.h"
+
+#include <condition_variable>
+#include <functional>
+#include <mutex>
+#include <thread>
+#include <vector>
+
+namespace dc {
+
+constexpr size_t NONE = (size_t)-1;
+
+struct TensorInfo {
+    int n = 0, h = 0, w = 0, c = 0;
+    size_t act = NONE;   // byte offset of the activation in the workspace
+    size_t grad = NONE;  // byte offset of its gradient
+    int64_t size() const { return (int64_t)n * h * w * c; }
+};
+
+struct OpInfo {
+    dc_op_desc d{};
+    int out = 0;                     // output tensor id
+    size_t w_off = NONE, b_off = NONE; // float offsets into the parameter vector (gamma/beta for BN)
+    ConvGeom geom{};
+    GemmPlan fwd{}, dgrad{}, wgrad{};
+    dc_pool_shape pool{};
+    size_t aux = NONE;               // BN: mean then invstd; MAXPOOL: argmax bytes
+    bool grad_in0 = false, grad_in1 = false;
+    int acc_in0 = 0, acc_in1 = 0;    // backward adds into the input gradient
+};
+
+// Small persistent pool for the server-side SGD update.
+class HostPool {
+  public:
+    explicit HostPool(int threads);
+    ~HostPool();
+    // Run fn(i, n) for i in [0, n) over the pool and the calling thread.
+    void run(int n, const std::function<void(int, int)> &fn);
+    int size() const { return (int)workers_.size() + 1; }
+
+  private:
+    void loop(int id);
+    std::vector<std::thread> workers_;
+    std::mutex mu_;
+    std::condition_variable cv_, done_cv_;
+    const std::function<void(int, int)> *job_ = nullptr;
+    int job_n_ = 0;
+    int next_ = 0;
+    int active_ = 0;
+    long gen_ = 0;
+    bool stop_ = false;
+};
+
+} // namespace dc
+
+struct dc_model {
+    int batch = 0, in_h = 0, in_w = 0, in_c = 0, classes = 0, L = 0;
+    int device = 0;
+    std::vector<dc::OpInfo> ops;
+    std::vector<dc::TensorInfo> tensors;
+    size_t n_params = 0;
+    std::vector<size_t> layer_off, layer_cnt;     // index 1..L
+    std::vector<int> layer_first, layer_last;     // op index range of each layer
+
+    // parameter server: pinned host memory
+    float *ps_params = nullptr;
+    float *ps_grads = nullptr;
+    float *probe_host = nullptr;
+    size_t probe_bytes = 0;
+
+    // device workspace (caller-owned)
+    char *ws = nullptr;
+    size_t ws_bytes = 0;
+    size_t ws_need = 0;
+    size_t off_params = 0, off_grads = 0, off_scratch = 0, scratch_bytes = 0;
+    size_t off_loss = 0, off_slots = 0;
+
+    hipStream_t pull_s = nullptr, push_s = nullptr;
+    std::vector<hipEvent_t> ev_pull_start, ev_pull_done, ev_bwd_done, ev_push_start, ev_push_done;
+    std::vector<hipEvent_t> ev_fwd_start, ev_fwd_end, ev_bwd_end; // per layer, index 1..L (+ [0] / [L+1] sentinels)
+    hipEvent_t ev_t0 = nullptr;
+
+    double lr = 0.01;
+    int timeline = 0;
+    double timeout_s = 600.0;
+    int sgd_threads = 0;
+    dc::HostPool *pool = nullptr;
+    double wall_hz = 0;
+
+    std::vector<int64_t> timeline_ns;
+    bool timeline_valid = false;
+
+    float *dparams() const { return reinterpret_cast<float *>(ws + off_params); }
+    float *dgrads() const { return reinterpret_cast<float *>(ws + off_grads); }
+    float *act(int t) const { return reinterpret_cast<float *>(ws + tensors[t].act); }
+    float *grad(int t) const { return reinterpret_cast<float *>(ws + tensors[t].grad); }
+    void *scratch() const { return ws + off_scratch; }
+    float *dloss() const { return reinterpret_cast<float *>(ws + off_loss); }
+    uint64_t *slots() const { return reinterpret_cast<uint64_t *>(ws + off_slots); }
+};
+
+namespace dc {
+// Enqueue the forward mini-procedures of layer l (and the loss after layer L)
+// on stream s; x is the input batch, y its labels.
+int run_forward_layer(dc_model *m, int l, const float *x, const int32_t *y, hipStream_t s);
+// Enqueue the backward mini-procedures of layer l (x: the input batch).
+int run_backward_layer(dc_model *m, int l, const float *x, hipStream_t s);
+} // namespace dc

@@ -1,0 +1,205 @@
+"""The five synthetic workloads as dc_op_desc lists for dc_model_create.
+
+Each builder returns ``(ops, hwc, classes)``: ``ops`` is a list of 10-tuples
+``(kind, layer, in0, in1, out_ch, r, s, stride, pad, bias)`` in forward order
+(tensor 0 = input batch, tensor i+1 = output of op i).  A planner layer is one
+conv / FC and the parameter-less ops after it, BatchNorm joins its conv, and
+a residual projection shares the layer of its block's first conv (the layer
+decomposition of Sec. III-A).
+
+Workloads (inputs NHWC; batch and link are chosen by the caller):
+  tiny      conv3x3 3->8 +ReLU+pool2, conv3x3 8->16 +ReLU+pool2, FC 1024->64 +ReLU, FC 64->10   (L=4)
+  alexnet   conv11x11/4 64, conv5x5 192, conv3x3 384/256/256, pools 3/2, FC 9216->4096->4096->1000 (L=8)
+  resnet18  32x32 ResNet-18 with BN and 1x1/2 projections, FC 512->10                         (L=18)
+  vgg16     13 conv3x3 + 3 FC, 224x224                                                        (L=16)
+  resnet50  bottleneck [3,4,6,3], stride on the 3x3 conv, FC 2048->1000                        (L=50)
+"""
+from __future__ import annotations
+
+from ._lib import DC_OP_ADD, DC_OP_BN, DC_OP_CONV, DC_OP_FC, DC_OP_GAP, DC_OP_MAXPOOL, DC_OP_RELU
+
+
+class NetBuilder:
+    def __init__(self):
+        self.ops = []
+        self.layer = 0
+
+    def _emit(self, kind, src, other=-1, out_ch=0, r=0, s=0, stride=0, pad=0, bias=0):
+        self.ops.append((kind, self.layer, src, other, out_ch, r, s, stride, pad, bias))
+        return len(self.ops)
+
+    def conv(self, src, out_ch, k, stride=1, pad=0, bias=True, new_layer=True):
+        if new_layer:
+            self.layer += 1
+        return self._emit(DC_OP_CONV, src, out_ch=out_ch, r=k, s=k, stride=stride, pad=pad, bias=int(bias))
+
+    def fc(self, src, out, bias=True):
+        self.layer += 1
+        return self._emit(DC_OP_FC, src, out_ch=out, bias=int(bias))
+
+    def bn(self, src):
+        return self._emit(DC_OP_BN, src)
+
+    def relu(self, src):
+        return self._emit(DC_OP_RELU, src)
+
+    def maxpool(self, src, k, stride, pad=0):
+        return self._emit(DC_OP_MAXPOOL, src, r=k, s=k, stride=stride, pad=pad)
+
+    def gap(self, src):
+        return self._emit(DC_OP_GAP, src)
+
+    def add(self, a, b):
+        return self._emit(DC_OP_ADD, a, other=b)
+
+
+def tiny():
+    n = NetBuilder()
+    t = n.maxpool(n.relu(n.conv(0, 8, 3, pad=1)), 2, 2)
+    t = n.maxpool(n.relu(n.conv(t, 16, 3, pad=1)), 2, 2)
+    t = n.relu(n.fc(t, 64))
+    n.fc(t, 10)
+    return n.ops, (32, 32, 3), 10
+
+
+def alexnet():
+    n = NetBuilder()
+    t = n.maxpool(n.relu(n.conv(0, 64, 11, stride=4, pad=2)), 3, 2)
+    t = n.maxpool(n.relu(n.conv(t, 192, 5, pad=2)), 3, 2)
+    t = n.relu(n.conv(t, 384, 3, pad=1))
+    t = n.relu(n.conv(t, 256, 3, pad=1))
+    t = n.maxpool(n.relu(n.conv(t, 256, 3, pad=1)), 3, 2)
+    t = n.relu(n.fc(t, 4096))
+    t = n.relu(n.fc(t, 4096))
+    n.fc(t, 1000)
+    return n.ops, (224, 224, 3), 1000
+
+
+def vgg16():
+    n = NetBuilder()
+    t = 0
+    for width, reps in ((64, 2), (128, 2), (256, 3), (512, 3), (512, 3)):
+        for _ in range(reps):
+            t = n.relu(n.conv(t, width, 3, pad=1))
+        t = n.maxpool(t, 2, 2)
+    t = n.relu(n.fc(t, 4096))
+    t = n.relu(n.fc(t, 4096))
+    n.fc(t, 1000)
+    return n.ops, (224, 224, 3), 1000
+
+
+def _basic_block(n, x, cin, cout, stride):
+    u = n.relu(n.bn(n.conv(x, cout, 3, stride=stride, pad=1, bias=False)))
+    short = x
+    if stride != 1 or cin != cout:  # projection at the depth of the first conv
+        short = n.bn(n.conv(x, cout, 1, stride=stride, bias=False, new_layer=False))
+    u = n.bn(n.conv(u, cout, 3, pad=1, bias=False))
+    return n.relu(n.add(u, short))
+
+
+def resnet18():
+    n = NetBuilder()
+    t = n.relu(n.bn(n.conv(0, 64, 3, pad=1, bias=False)))
+    cin = 64
+    for cout, stride in ((64, 1), (128, 2), (256, 2), (512, 2)):
+        t = _basic_block(n, t, cin, cout, stride)
+        t = _basic_block(n, t, cout, cout, 1)
+        cin = cout
+    t = n.gap(t)
+    n.fc(t, 10)
+    return n.ops, (32, 32, 3), 10
+
+
+def _bottleneck(n, x, width, stride, project):
+    out = 4 * width
+    u = n.relu(n.bn(n.conv(x, width, 1, bias=False)))
+    short = x
+    if project:
+        short = n.bn(n.conv(x, out, 1, stride=stride, bias=False, new_layer=False))
+    u = n.relu(n.bn(n.conv(u, width, 3, stride=stride, pad=1, bias=False)))
+    u = n.bn(n.conv(u, out, 1, bias=False))
+    return n.relu(n.add(u, short))
+
+
+def resnet50():
+    n = NetBuilder()
+    t = n.relu(n.bn(n.conv(0, 64, 7, stride=2, pad=3, bias=False)))
+    t = n.maxpool(t, 3, 2, pad=1)
+    for width, blocks, stride in ((64, 3, 1), (128, 4, 2), (256, 6, 2), (512, 3, 2)):
+        for i in range(blocks):
+            t = _bottleneck(n, t, width, stride if i == 0 else 1, i == 0)
+    t = n.gap(t)
+    n.fc(t, 1000)
+    return n.ops, (224, 224, 3), 1000
+
+
+BUILDERS = {"tiny": tiny, "alexnet": alexnet, "resnet18": resnet18, "vgg16": vgg16, "resnet50": resnet50}
+
+# The workloads' batch size, emulated link rate (bytes/s; 1 Gb/s = 1.25e8 B/s)
+# and input seed.
+WORKLOADS = {
+    "tiny": {"batch": 4, "link": 1e9, "seed": 0},
+    "alexnet": {"batch": 32, "link": 100e6 / 8, "seed": 1},
+    "resnet18": {"batch": 128, "link": 1e9 / 8, "seed": 2},
+    "vgg16": {"batch": 32, "link": 10e9 / 8, "seed": 3},
+    "resnet50": {"batch": 64, "link": 10e9 / 8, "seed": 4},
+}
+
+
+def build(name):
+    return BUILDERS[name]()
+
+
+def param_specs(ops, hwc):
+    """Initialisation kinds of the parameter tensors in parameter-server order.
+
+    He-normal for conv / FC weights (fan-in = r*s*c or in-features), zeros for
+    biases and BN beta, ones for BN gamma - the argument list of
+    ``synth.cnn_inputs``.
+    """
+    shapes = [(hwc[0], hwc[1], hwc[2])]
+    specs = []
+    for (kind, _layer, src, _other, out_ch, r, s, stride, pad, bias) in ops:
+        h, w, c = shapes[src]
+        if kind == DC_OP_CONV:
+            specs.append(("he", out_ch * r * s * c, r * s * c))
+            if bias:
+                specs.append(("zeros", out_ch))
+            shapes.append(((h + 2 * pad - r) // stride + 1, (w + 2 * pad - s) // stride + 1, out_ch))
+        elif kind == DC_OP_FC:
+            specs.append(("he", out_ch * h * w * c, h * w * c))
+            if bias:
+                specs.append(("zeros", out_ch))
+            shapes.append((1, 1, out_ch))
+        elif kind == DC_OP_BN:
+            specs.append(("ones", c))
+            specs.append(("zeros", c))
+            shapes.append((h, w, c))
+        elif kind == DC_OP_MAXPOOL:
+            shapes.append(((h + 2 * pad - r) // stride + 1, (w + 2 * pad - s) // stride + 1, c))
+        elif kind == DC_OP_GAP:
+            shapes.append((1, 1, c))
+        else:
+            shapes.append((h, w, c))
+    return specs
+
+
+def conv_geoms(ops, hwc, batch):
+    """(op index, dc_conv_shape fields, reads_input_batch) of every conv / FC op; FC as a 1x1 conv."""
+    shapes = [(hwc[0], hwc[1], hwc[2])]
+    out = []
+    for i, (kind, _layer, src, _other, out_ch, r, s, stride, pad, bias) in enumerate(ops):
+        h, w, c = shapes[src]
+        if kind == DC_OP_CONV:
+            out.append((i, (batch, h, w, c, out_ch, r, s, stride, pad), src == 0))
+            shapes.append(((h + 2 * pad - r) // stride + 1, (w + 2 * pad - s) // stride + 1, out_ch))
+        elif kind == DC_OP_FC:
+            out.append((i, (batch, 1, 1, h * w * c, out_ch, 1, 1, 1, 0), src == 0))
+            shapes.append((1, 1, out_ch))
+        elif kind == DC_OP_MAXPOOL:
+            shapes.append(((h + 2 * pad - r) // stride + 1, (w + 2 * pad - s) // stride + 1, c))
+        elif kind == DC_OP_GAP:
+            shapes.append((1, 1, c))
+        else:
+            shapes.append((h, w, c))
+    return out

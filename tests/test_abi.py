@@ -1,0 +1,146 @@
+"""The C-ABI library on the host: exported symbols and the planner.
+
+libdc.so must export every function that include/dc.h and
+include/dc_kernels.h declare.  dc_plan is pure host code, so it is checked
+here, without a GPU, against the oracle's transcription of Eq. 8 / Algorithm 3
+and Eq. 9 / Algorithm 4: the decisions must be bit-identical and the model
+times equal, for random profiles, the tiny workload's fixture and deep
+networks.  Error paths of the planner and of model validation are exercised
+too (validation fails before any HIP call).
+"""
+import ctypes
+import json
+import os
+import re
+
+import numpy as np
+import pytest
+
+import synth
+from oracle import plan as OP
+from paper_2101_07968_amd import _lib as D
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_functions():
+    names = set()
+    for h in ("dc.h", "dc_kernels.h"):
+        text = open(os.path.join(ROOT, "include", h)).read()
+        text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+        for m in re.finditer(r"\b(dc_[a-z0-9_]+)\s*\(", text):
+            names.add(m.group(1))
+    return sorted(names)
+
+
+def test_library_exports_every_declared_function():
+    lib = D.lib()
+    names = declared_functions()
+    assert len(names) >= 30
+    missing = [n for n in names if not hasattr(lib, n)]
+    assert not missing, missing
+    assert set(D._SIGS) == set(names), set(D._SIGS) ^ set(names)
+
+
+def test_strerror():
+    lib = D.lib()
+    assert lib.dc_strerror(0) == b"ok"
+    assert lib.dc_strerror(D.DC_ETIMEOUT) == b"watchdog timeout"
+
+
+def _check_against_oracle(pt, fc, bc, gt, dt):
+    prof = D.Profile(pt, fc, bc, gt, dt)
+    plan = D.dc_plan(prof)
+    p, g = plan.decisions()
+    op, tf, _, _ = OP.forward_dp(pt, fc, dt)
+    og, tb, _, _ = OP.backward_dp(bc, gt, dt)
+    assert p == op and g == og
+    assert plan.t_fwd_ns == tf and plan.t_bwd_ns == tb
+    return plan
+
+
+@pytest.mark.parametrize("block", range(20))
+def test_plan_bit_exact_random(block):
+    for i in range(150):
+        seed = block * 1000 + i
+        L = 1 + seed % 20
+        hi = (10, 60, 1000, 10 ** 6)[seed % 4]
+        pt, fc, bc, gt, dt = synth.random_profile(seed, L, hi=hi, dt_hi=hi // 2 + 1)
+        _check_against_oracle(pt, fc, bc, gt, dt)
+
+
+@pytest.mark.parametrize("L", [50, 75, 120])
+def test_plan_bit_exact_deep(L):
+    for seed in range(3):
+        pt, fc, bc, gt, dt = synth.random_profile(50000 + L * 10 + seed, L, hi=10 ** 7, dt_hi=10 ** 6)
+        _check_against_oracle(pt, fc, bc, gt, dt)
+
+
+def test_plan_tiny_fixture():
+    d = json.load(open(os.path.join(ROOT, "tests", "golden", "tiny_plan.json")))
+    pr = d["profile"]
+    plan = _check_against_oracle(pr["pt"], pr["fc"], pr["bc"], pr["gt"], pr["dt"])
+    assert plan.decisions() == (d["p"], d["g"])
+    seq = D.dc_plan_sequential(D.Profile(pr["pt"], pr["fc"], pr["bc"], pr["gt"], pr["dt"]))
+    assert (seq.t_fwd_ns, seq.t_bwd_ns) == (d["T_fwd_sequential"], d["T_bwd_sequential"])
+    lbl = D.dc_plan_lbl(D.Profile(pr["pt"], pr["fc"], pr["bc"], pr["gt"], pr["dt"]))
+    assert (lbl.t_fwd_ns, lbl.t_bwd_ns) == (d["T_fwd_lbl"], d["T_bwd_lbl"])
+
+
+@pytest.mark.parametrize("seed", range(50))
+def test_plan_eval_matches_fm(seed):
+    L = 2 + seed % 12
+    pt, fc, bc, gt, dt = synth.random_profile(70000 + seed, L, hi=5000, dt_hi=3000)
+    rng = np.random.default_rng(seed)
+    p = rng.integers(0, 2, L - 1).tolist()
+    g = rng.integers(0, 2, L - 1).tolist()
+    plan = D.dc_plan_eval(D.Profile(pt, fc, bc, gt, dt), p, g)
+    assert plan.t_fwd_ns == OP.fm_forward(pt, fc, dt, p)
+    assert plan.t_bwd_ns == OP.fm_backward(bc, gt, dt, g)
+
+
+def test_plan_single_layer():
+    plan = D.dc_plan(D.Profile([5], [7], [3], [2], 4))
+    assert (plan.t_fwd_ns, plan.t_bwd_ns) == (4 + 5 + 7, 3 + 4 + 2)
+
+
+def test_plan_rejects_bad_input():
+    with pytest.raises(D.DcError) as e:
+        D.dc_plan(D.Profile([1, -2], [1, 1], [1, 1], [1, 1], 0))
+    assert e.value.status == D.DC_EINVAL
+    with pytest.raises(D.DcError) as e:
+        D.dc_plan(D.Profile([1, 1], [1, 1], [1, 1], [1, 1], -1))
+    assert e.value.status == D.DC_EINVAL
+    big = 2 ** 62
+    with pytest.raises(D.DcError) as e:
+        D.dc_plan(D.Profile([big, big], [1, 1], [1, 1], [1, 1], 0))
+    assert e.value.status == D.DC_EINVAL
+    # L = 0
+    prof = D.Profile([], [], [], [], 0)
+    pc, plan = prof.c(), D.PlanT(0, None, None, 0, 0)
+    assert D.lib().dc_plan(ctypes.byref(pc), ctypes.byref(plan)) == D.DC_EINVAL
+
+
+def _create(ops, batch=2, hwc=(8, 8, 3), classes=10):
+    arr = (D.OpDesc * len(ops))(*[D.OpDesc(*o) for o in ops])
+    h = ctypes.c_void_p()
+    st = D.lib().dc_model_create(arr, len(ops), batch, hwc[0], hwc[1], hwc[2], classes, ctypes.byref(h))
+    return st, h
+
+
+def test_model_validation_rejects_bad_descriptions():
+    conv = (D.DC_OP_CONV, 1, 0, -1, 4, 3, 3, 1, 1, 1)
+    # layer must start with a weighted op
+    assert _create([(D.DC_OP_RELU, 1, 0, -1, 0, 0, 0, 0, 0, 0)])[0] == D.DC_EINVAL
+    # input tensor from the future
+    assert _create([conv, (D.DC_OP_RELU, 1, 5, -1, 0, 0, 0, 0, 0, 0)])[0] == D.DC_EINVAL
+    # layers skip a number
+    assert _create([conv, (D.DC_OP_FC, 3, 1, -1, 10, 0, 0, 0, 0, 1)])[0] == D.DC_EINVAL
+    # logits of the wrong width
+    assert _create([conv, (D.DC_OP_FC, 2, 1, -1, 7, 0, 0, 0, 0, 1)])[0] == D.DC_EINVAL
+    # an output nobody reads
+    assert _create([conv, (D.DC_OP_RELU, 1, 1, -1, 0, 0, 0, 0, 0, 0),
+                    (D.DC_OP_FC, 2, 1, -1, 10, 0, 0, 0, 0, 1)])[0] == D.DC_EINVAL
+    # ADD of different shapes
+    assert _create([conv, (D.DC_OP_ADD, 1, 1, 0, 0, 0, 0, 0, 0, 0)])[0] == D.DC_EINVAL
+    assert b"ADD" in D.lib().dc_last_error()

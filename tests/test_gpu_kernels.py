@@ -1,0 +1,283 @@
+"""GPU parity of the gfx950 kernels against the oracle, through the C ABI.
+
+Tolerances (per tensor, max |gpu - oracle| / max |oracle|): the kernels add
+float32 products, so a sum of K terms carries a relative rounding error of
+order sqrt(number of sequential fp32 additions) * 2^-24.  The bars below are
+1e-5 * max(1, sqrt(K / 256)), capped at 2e-4 for the longest reductions (up to
+1.6 M terms), well inside the 1e-3 the full iteration must meet.  Max-pool
+forward picks values, so it must be bit-exact; its argmax is decided in
+float32 on both sides.
+"""
+import ctypes
+import math
+
+import numpy as np
+import pytest
+
+import synth
+from oracle import cnn as OC
+from oracle import nets as ON
+from paper_2101_07968_amd import _lib as D
+from tests.gpu_helpers import dev, host, rel_err, scratch, stream, zeros
+
+pytestmark = pytest.mark.gpu
+
+
+def tol(k_terms):
+    return min(2e-4, 1e-5 * max(1.0, math.sqrt(k_terms / 256.0)))
+
+
+def conv_shape(n, h, w, c, k, r, st, pad):
+    return D.ConvShape(n, h, w, c, k, r, r, st, pad)
+
+
+def out_hw(h, r, st, pad):
+    return (h + 2 * pad - r) // st + 1
+
+
+def run_conv(shape, x, w, b, dy, relu, acc_init):
+    """All three passes on the GPU; returns (y, dx, dw, db) as numpy."""
+    sh = conv_shape(*shape)
+    n, h, wd, c, k, r, st, pad = shape
+    P, Q = out_hw(h, r, st, pad), out_hw(wd, r, st, pad)
+    ws_t, ws, wsb = scratch(D.lib().dc_conv2d_workspace_bytes(ctypes.byref(sh)))
+    xd, wd_, bd, dyd = dev(x), dev(w), dev(b), dev(dy)
+    y = zeros((n, P, Q, k))
+    D.call("dc_conv2d_forward", ctypes.byref(sh), xd.data_ptr(), wd_.data_ptr(), bd.data_ptr(), relu,
+           y.data_ptr(), ws, wsb, stream())
+    dx = dev(acc_init) if acc_init is not None else zeros((n, h, wd, c))
+    D.call("dc_conv2d_backward_data", ctypes.byref(sh), dyd.data_ptr(), wd_.data_ptr(),
+           1 if acc_init is not None else 0, dx.data_ptr(), ws, wsb, stream())
+    dw = zeros((k, r, r, c))
+    db = zeros((k,))
+    D.call("dc_conv2d_backward_filter", ctypes.byref(sh), xd.data_ptr(), dyd.data_ptr(), dw.data_ptr(),
+           db.data_ptr(), ws, wsb, stream())
+    return host(y), host(dx), host(dw), host(db)
+
+
+SMALL = [
+    # n, h, w, c, k, r, stride, pad
+    (2, 13, 11, 8, 20, 3, 1, 1),
+    (2, 9, 9, 3, 70, 3, 1, 1),
+    (3, 15, 15, 16, 33, 3, 2, 1),
+    (2, 12, 12, 12, 24, 1, 2, 0),
+    (1, 31, 31, 3, 16, 11, 4, 2),
+    (2, 14, 14, 3, 8, 7, 2, 3),
+    (2, 7, 7, 64, 130, 3, 1, 1),
+    (2, 28, 28, 64, 64, 3, 1, 1),
+    (4, 1, 1, 1024, 64, 1, 1, 0),
+    (4, 1, 1, 64, 10, 1, 1, 0),
+    (3, 1, 1, 300, 130, 1, 1, 0),
+    (2, 5, 5, 6, 5, 5, 1, 2),
+    (2, 6, 6, 4, 4, 3, 3, 1),
+    (5, 17, 17, 40, 136, 3, 1, 1),
+]
+
+
+@pytest.mark.parametrize("shape", SMALL, ids=[str(s) for s in SMALL])
+@pytest.mark.parametrize("variant", ["plain", "relu_acc"])
+def test_conv_small(shape, variant):
+    n, h, w, c, k, r, st, pad = shape
+    P, Q = out_hw(h, r, st, pad), out_hw(w, r, st, pad)
+    seed = sum(shape) * 7 + (variant == "relu_acc")
+    x = synth.random_tensor(seed, (n, h, w, c))
+    wt = synth.random_tensor(seed + 1, (k, r, r, c))
+    b = synth.random_tensor(seed + 2, (k,))
+    dy = synth.random_tensor(seed + 3, (n, P, Q, k))
+    relu = 1 if variant == "relu_acc" else 0
+    acc0 = synth.random_tensor(seed + 4, (n, h, w, c)) if variant == "relu_acc" else None
+    y, dx, dw, db = run_conv(shape, x, wt, b, dy, relu, acc0)
+    y_ref = OC.conv2d_forward(x, wt, b, st, pad)
+    if relu:
+        y_ref = np.maximum(y_ref, 0)
+    dx_ref = OC.conv2d_backward_data(dy, wt, (h, w), st, pad)
+    if acc0 is not None:
+        dx_ref = dx_ref + acc0
+    dw_ref = OC.conv2d_backward_filter(x, dy, (r, r), st, pad)
+    db_ref = dy.astype(np.float64).sum(axis=(0, 1, 2))
+    assert rel_err(y, y_ref) <= tol(r * r * c)
+    assert rel_err(dx, dx_ref) <= tol(r * r * k)
+    assert rel_err(dw, dw_ref) <= tol(n * P * Q)
+    assert rel_err(db, db_ref) <= tol(n * P * Q)
+
+
+def _full_size_geoms():
+    """Every distinct conv / FC geometry of the five workloads at their own batch."""
+    seen, out = set(), []
+    for name, batch in (("tiny", 4), ("alexnet", 32), ("resnet18", 128), ("vgg16", 32), ("resnet50", 64)):
+        net = OC.Net(ON.get(name), batch)
+        for i, op in enumerate(net.ops):
+            if op["op"] not in ("conv", "fc"):
+                continue
+            n, h, w, c = net.shapes[op["in"]]
+            if op["op"] == "conv":
+                g = (n, h, w, c, op["k"], op["r"], op["stride"], op["pad"])
+            else:
+                g = (n, 1, 1, h * w * c, op["out"], 1, 1, 0)
+            if g not in seen:
+                seen.add(g)
+                out.append((name, g))
+    return out
+
+
+FULL = _full_size_geoms()
+
+
+def _sample(rng, shape, count):
+    idx = [np.zeros(len(shape), dtype=int), np.array(shape) - 1]
+    for _ in range(count):
+        idx.append(np.array([rng.integers(0, s) for s in shape]))
+    return np.stack(idx)
+
+
+@pytest.mark.parametrize("case", FULL, ids=[f"{n}-{g}" for n, g in FULL])
+def test_conv_full_size_sampled(case):
+    name, shape = case
+    n, h, w, c, k, r, st, pad = shape
+    P, Q = out_hw(h, r, st, pad), out_hw(w, r, st, pad)
+    seed = abs(hash(shape)) % 10000
+    x = synth.random_tensor(seed, (n, h, w, c))
+    wt = synth.random_tensor(seed + 1, (k, r, r, c), scale=math.sqrt(2.0 / (r * r * c)))
+    b = synth.random_tensor(seed + 2, (k,))
+    dy = synth.random_tensor(seed + 3, (n, P, Q, k), scale=1e-3)
+    print(f"conv {name} {shape}", flush=True)
+    y, dx, dw, db = run_conv(shape, x, wt, b, dy, 0, None)
+    rng = np.random.default_rng(seed)
+    geom = (n, h, w, c, k, r, r, st, pad)
+    i = _sample(rng, y.shape, 48)
+    ref = OC.conv2d_samples("fwd", geom, x, wt, i, b)
+    got = y[tuple(i.T)]
+    assert np.abs(got - ref).max() <= tol(r * r * c) * np.abs(y).max()
+    i = _sample(rng, dx.shape, 48)
+    ref = OC.conv2d_samples("dgrad", geom, dy, wt, i)
+    got = dx[tuple(i.T)]
+    assert np.abs(got - ref).max() <= tol(r * r * k) * np.abs(dx).max()
+    i = _sample(rng, dw.shape, 32)
+    ref = OC.conv2d_samples("wgrad", geom, x, dy, i)
+    got = dw[tuple(i.T)]
+    assert np.abs(got - ref).max() <= tol(n * P * Q) * np.abs(dw).max()
+    db_ref = dy.astype(np.float64).sum(axis=(0, 1, 2))
+    assert rel_err(db, db_ref) <= tol(n * P * Q)
+
+
+def test_conv_rejects_bad_shapes_and_accepts_empty():
+    sh = conv_shape(2, 4, 4, 3, 5, 3, 1, 3)  # pad >= r
+    assert D.lib().dc_conv2d_forward(ctypes.byref(sh), 1, 1, None, 0, 1, None, 0, None) == D.DC_EINVAL
+    sh = conv_shape(0, 4, 4, 3, 5, 3, 1, 1)  # empty batch: nothing to do
+    assert D.lib().dc_conv2d_forward(ctypes.byref(sh), None, None, None, 0, None, None, 0, stream()) == D.DC_OK
+    # the bias gradient needs scratch: a missing workspace is an error, not a fault
+    sh = conv_shape(2, 40, 40, 64, 64, 3, 1, 1)
+    assert D.lib().dc_conv2d_workspace_bytes(ctypes.byref(sh)) > 0
+    x, dy, dw, db = zeros((2, 40, 40, 64)), zeros((2, 40, 40, 64)), zeros((64, 3, 3, 64)), zeros((64,))
+    assert D.lib().dc_conv2d_backward_filter(ctypes.byref(sh), x.data_ptr(), dy.data_ptr(), dw.data_ptr(),
+                                             db.data_ptr(), None, 0, stream()) == D.DC_EINVAL
+
+
+# ---------------------------------------------------------------- elementwise
+
+@pytest.mark.parametrize("n,offset", [(1000, 0), (1003, 1), (4 * 1024 * 1024 + 3, 0)])
+def test_relu_add_copy(n, offset):
+    a = synth.random_tensor(1, (n + offset,))
+    b = synth.random_tensor(2, (n + offset,))
+    g = synth.random_tensor(3, (n + offset,))
+    ad, bd, gd = dev(a), dev(b), dev(g)
+    y = zeros((n + offset,))
+    D.call("dc_relu_forward", ad.data_ptr() + 4 * offset, y.data_ptr() + 4 * offset, n, stream())
+    yh = host(y)[offset:]
+    np.testing.assert_array_equal(yh, np.maximum(a[offset:], 0))
+    dx = dev(b)
+    D.call("dc_relu_backward", gd.data_ptr() + 4 * offset, y.data_ptr() + 4 * offset, 1,
+           dx.data_ptr() + 4 * offset, n, stream())
+    ref = b[offset:] + np.where(yh > 0, g[offset:], 0)
+    np.testing.assert_array_equal(host(dx)[offset:], ref.astype(np.float32))
+    z = zeros((n + offset,))
+    D.call("dc_add_forward", ad.data_ptr() + 4 * offset, bd.data_ptr() + 4 * offset, 1, z.data_ptr() + 4 * offset,
+           n, stream())
+    np.testing.assert_array_equal(host(z)[offset:], np.maximum(a[offset:] + b[offset:], 0))
+    D.call("dc_copy_grad", gd.data_ptr(), 1, ad.data_ptr(), n + offset, stream())
+    np.testing.assert_array_equal(host(ad), (a + g).astype(np.float32))
+
+
+POOLS = [(2, 8, 8, 5, 2, 2, 0), (3, 13, 13, 16, 3, 2, 0), (2, 12, 12, 7, 3, 2, 1), (32, 55, 55, 64, 3, 2, 0),
+         (64, 112, 112, 64, 3, 2, 1), (32, 224, 224, 64, 2, 2, 0)]
+
+
+@pytest.mark.parametrize("cfg", POOLS, ids=[str(p) for p in POOLS])
+def test_maxpool(cfg):
+    n, h, w, c, r, st, pad = cfg
+    x = synth.random_tensor(11, (n, h, w, c))
+    P, Q = out_hw(h, r, st, pad), out_hw(w, r, st, pad)
+    dy = synth.random_tensor(12, (n, P, Q, c))
+    sh = D.PoolShape(n, h, w, c, r, r, st, pad)
+    xd, dyd = dev(x), dev(dy)
+    y = zeros((n, P, Q, c))
+    arg = zeros((n, P, Q, c), "uint8")
+    D.call("dc_maxpool_forward", ctypes.byref(sh), xd.data_ptr(), y.data_ptr(), arg.data_ptr(), stream())
+    dx = zeros((n, h, w, c))
+    D.call("dc_maxpool_backward", ctypes.byref(sh), dyd.data_ptr(), arg.data_ptr(), 0, dx.data_ptr(), stream())
+    y_ref, arg_ref = OC.maxpool_forward(x, r, r, st, pad)
+    np.testing.assert_array_equal(host(y), y_ref.astype(np.float32))
+    np.testing.assert_array_equal(host(arg).astype(np.int32), arg_ref)
+    dx_ref = OC.maxpool_backward(dy, arg_ref, x.shape, r, r, st, pad)
+    assert rel_err(host(dx), dx_ref) <= 1e-7
+
+
+@pytest.mark.parametrize("cfg", [(3, 4, 4, 10), (128, 4, 4, 512), (64, 7, 7, 2048)])
+def test_gap(cfg):
+    n, h, w, c = cfg
+    x = synth.random_tensor(13, (n, h, w, c))
+    dy = synth.random_tensor(14, (n, 1, 1, c))
+    y = zeros((n, 1, 1, c))
+    xd, dyd = dev(x), dev(dy)
+    D.call("dc_gap_forward", n, h * w, c, xd.data_ptr(), y.data_ptr(), stream())
+    assert rel_err(host(y), x.astype(np.float64).mean(axis=(1, 2), keepdims=True)) <= 1e-6
+    dx = zeros((n, h, w, c))
+    D.call("dc_gap_backward", n, h * w, c, dyd.data_ptr(), 0, dx.data_ptr(), stream())
+    assert rel_err(host(dx), np.broadcast_to(dy.astype(np.float64) / (h * w), x.shape)) <= 1e-7
+
+
+BNS = [(2, 5, 5, 64), (4, 9, 9, 130), (128, 32, 32, 64), (64, 112, 112, 64), (64, 7, 7, 2048), (1, 7, 7, 512)]
+
+
+@pytest.mark.parametrize("cfg", BNS, ids=[str(b) for b in BNS])
+def test_batchnorm(cfg):
+    n, h, w, c = cfg
+    rows = n * h * w
+    x = (synth.random_tensor(15, (n, h, w, c)) * 2 + 0.5).astype(np.float32)
+    gamma = synth.random_tensor(16, (c,))
+    beta = synth.random_tensor(17, (c,))
+    dy = synth.random_tensor(18, (n, h, w, c))
+    acc0 = synth.random_tensor(19, (n, h, w, c))
+    ws_t, ws, wsb = scratch(D.lib().dc_batchnorm_workspace_bytes(rows, c))
+    xd, gd, bd, dyd = dev(x), dev(gamma), dev(beta), dev(dy)
+    y, mean, invstd = zeros((n, h, w, c)), zeros((c,)), zeros((c,))
+    D.call("dc_batchnorm_forward", rows, c, xd.data_ptr(), gd.data_ptr(), bd.data_ptr(), ctypes.c_float(1e-5),
+           y.data_ptr(), mean.data_ptr(), invstd.data_ptr(), ws, wsb, stream())
+    dx = dev(acc0)
+    dg, db = zeros((c,)), zeros((c,))
+    D.call("dc_batchnorm_backward", rows, c, dyd.data_ptr(), xd.data_ptr(), gd.data_ptr(), mean.data_ptr(),
+           invstd.data_ptr(), 1, dx.data_ptr(), dg.data_ptr(), db.data_ptr(), ws, wsb, stream())
+    y_ref, xhat, inv_ref = OC.batchnorm_forward(x.astype(np.float64), gamma.astype(np.float64),
+                                                beta.astype(np.float64))
+    dx_ref, dg_ref, db_ref = OC.batchnorm_backward(dy.astype(np.float64), xhat, inv_ref, gamma.astype(np.float64))
+    t = tol(rows)
+    assert rel_err(host(y), y_ref) <= t
+    assert rel_err(host(invstd), inv_ref) <= t
+    assert rel_err(host(dg), dg_ref) <= t
+    assert rel_err(host(db), db_ref) <= t
+    assert rel_err(host(dx), dx_ref + acc0) <= 10 * t
+
+
+@pytest.mark.parametrize("n,classes", [(4, 10), (32, 1000), (128, 10), (3, 257)])
+def test_softmax_xent(n, classes):
+    z = synth.random_tensor(20, (n, classes)) * 3
+    y = np.random.default_rng(n).integers(0, classes, n).astype(np.int32)
+    ws_t, ws, wsb = scratch(D.lib().dc_softmax_xent_workspace_bytes(n))
+    loss = zeros((1,))
+    dz = zeros((n, classes))
+    zd, yd = dev(z), dev(y)  # keep the inputs alive until the kernel has run
+    D.call("dc_softmax_xent", n, classes, zd.data_ptr(), yd.data_ptr(), loss.data_ptr(), dz.data_ptr(),
+           ws, wsb, stream())
+    l_ref, dz_ref = OC.softmax_xent(z.astype(np.float64), y)
+    assert abs(host(loss)[0] - l_ref) <= 1e-6 * abs(l_ref)
+    assert rel_err(host(dz), dz_ref) <= 1e-6

@@ -201,40 +201,9 @@ def test_parameter_counts(name, count):
 
 
 def _torch_loss(spec, net, x, y, p):
-    """The same network evaluated with torch float64 library routines (NCHW inside)."""
-    pt = torch.from_numpy(np.asarray(p, dtype=np.float64)).requires_grad_(True)
-
-    def prm(i, name):
-        off, shape = net.pslots[i][name]
-        return pt[off:off + int(np.prod(shape))].reshape(shape)
-
-    F = torch.nn.functional
-    t = [_nchw(np.asarray(x, dtype=np.float64))]
-    for i, op in enumerate(spec["ops"]):
-        a = t[op["in"]]
-        k = op["op"]
-        if k == "conv":
-            w = prm(i, "w").permute(0, 3, 1, 2)
-            b = prm(i, "b") if op["bias"] else None
-            o = F.conv2d(a, w, b, stride=op["stride"], padding=op["pad"])
-        elif k == "fc":
-            flat = a.permute(0, 2, 3, 1).reshape(a.shape[0], -1)   # NHWC flatten
-            o = F.linear(flat, prm(i, "w"), prm(i, "b") if op["bias"] else None)
-            o = o.reshape(a.shape[0], -1, 1, 1)
-        elif k == "bn":
-            o = F.batch_norm(a, None, None, prm(i, "gamma"), prm(i, "beta"), training=True, eps=cnn.BN_EPS)
-        elif k == "relu":
-            o = F.relu(a)
-        elif k == "maxpool":
-            o = F.max_pool2d(a, op["r"], op["stride"], op["pad"])
-        elif k == "gap":
-            o = F.adaptive_avg_pool2d(a, 1)
-        elif k == "add":
-            o = a + t[op["other"]]
-        t.append(o)
-    loss = F.cross_entropy(t[-1].reshape(net.batch, -1), torch.from_numpy(np.asarray(y, dtype=np.int64)))
-    loss.backward()
-    return loss.item(), pt.grad.numpy()
+    """The same network evaluated with torch float64 library routines."""
+    from tests import torch_ref
+    return torch_ref.loss_and_grads(spec, net, x, y, p, torch.float64)
 
 
 @pytest.mark.parametrize("which", ["tiny", "mini"])
@@ -258,3 +227,24 @@ def test_resnet18_against_torch():
     lt, gt = _torch_loss(spec, net, x, y, p)
     assert abs(loss - lt) <= 1e-11 * max(1.0, abs(lt))
     np.testing.assert_allclose(g, gt, rtol=1e-8, atol=1e-11 * np.abs(gt).max())
+
+
+@pytest.mark.parametrize("shape", [(2, 9, 7, 3, 5, 3, 1, 1), (2, 11, 11, 4, 6, 3, 2, 1), (1, 23, 23, 3, 4, 11, 4, 2),
+                                   (3, 8, 8, 6, 7, 1, 2, 0)])
+def test_conv_samples_match_whole_tensors(shape):
+    """The one-output-at-a-time sums equal the whole-tensor ones at every index."""
+    N, H, W, C, K, R, st, pad = shape
+    x = synth.random_tensor(21, (N, H, W, C))
+    w = synth.random_tensor(22, (K, R, R, C))
+    b = synth.random_tensor(23, (K,))
+    y = cnn.conv2d_forward(x, w, b, st, pad)
+    dy = synth.random_tensor(24, y.shape)
+    geom = (N, H, W, C, K, R, R, st, pad)
+    idx = np.argwhere(np.ones(y.shape, dtype=bool))
+    np.testing.assert_allclose(cnn.conv2d_samples("fwd", geom, x, w, idx, b), y.reshape(-1), rtol=1e-14, atol=1e-13)
+    dx = cnn.conv2d_backward_data(dy, w, (H, W), st, pad)
+    idx = np.argwhere(np.ones(dx.shape, dtype=bool))
+    np.testing.assert_allclose(cnn.conv2d_samples("dgrad", geom, dy, w, idx), dx.reshape(-1), rtol=1e-14, atol=1e-13)
+    dw = cnn.conv2d_backward_filter(x, dy, (R, R), st, pad)
+    idx = np.argwhere(np.ones(dw.shape, dtype=bool))
+    np.testing.assert_allclose(cnn.conv2d_samples("wgrad", geom, x, dy, idx), dw.reshape(-1), rtol=1e-14, atol=1e-13)
