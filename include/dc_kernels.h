@@ -47,6 +47,11 @@ int dc_conv2d_backward_data(const dc_conv_shape *sh, const float *dy, const floa
 int dc_conv2d_backward_filter(const dc_conv_shape *sh, const float *x, const float *dy,
                               float *dw, float *dbias, void *ws, size_t ws_bytes, void *stream);
 
+/* Launch plan the conv passes use for this shape (pass: 0 forward, 1 data
+ * gradient, 2 filter gradient).  out[0..6] = workgroup tile M, tile N, split-K
+ * factor, GEMM M, GEMM N, GEMM K, stride phases.  For inspection and tuning. */
+int dc_conv2d_plan_info(const dc_conv_shape *sh, int pass, int32_t *out);
+
 /* y = max(x, 0) over n floats. */
 int dc_relu_forward(const float *x, float *y, int64_t n, void *stream);
 /* dx (+)= dy where y > 0, else 0 (relu'(0) = 0). */

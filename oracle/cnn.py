@@ -208,6 +208,11 @@ def sgd(params, grads, lr=LR):
 class Net:
     """Shapes, parameter layout and the training iteration of one oracle network."""
 
+    # Test hook: when set, perturb(i, y) replaces the output y of every conv,
+    # FC and BN op i in the forward pass.  None (the default) leaves the
+    # arithmetic untouched; tests use it to emulate float32 storage error.
+    perturb = None
+
     def __init__(self, spec, batch):
         self.spec = spec
         self.ops = spec["ops"]
@@ -305,6 +310,8 @@ class Net:
                 y = a.mean(axis=(1, 2), keepdims=True)
             elif kind == "add":
                 y = a + t[op["other"]]
+            if self.perturb is not None and kind in ("conv", "fc", "bn"):
+                y = self.perturb(i, y)
             t.append(y)
         return t, cache
 

@@ -93,6 +93,7 @@ _SIGS = {
     "dc_step": (ctypes.c_int, [c_vp, _P(Batch), _P(PlanT), _P(Link), c_vp, _P(StepStats)]),
     "dc_timeline": (ctypes.c_int, [c_vp, _P(c_i64), ctypes.c_int]),
     "dc_conv2d_workspace_bytes": (c_sz, [_P(ConvShape)]),
+    "dc_conv2d_plan_info": (ctypes.c_int, [_P(ConvShape), ctypes.c_int, _P(c_i32)]),
     "dc_conv2d_forward": (ctypes.c_int, [_P(ConvShape), c_vp, c_vp, c_vp, ctypes.c_int, c_vp, c_vp, c_sz, c_vp]),
     "dc_conv2d_backward_data": (ctypes.c_int, [_P(ConvShape), c_vp, c_vp, ctypes.c_int, c_vp, c_vp, c_sz, c_vp]),
     "dc_conv2d_backward_filter": (ctypes.c_int, [_P(ConvShape), c_vp, c_vp, c_vp, c_vp, c_vp, c_sz, c_vp]),
@@ -236,6 +237,14 @@ def dc_plan_eval(prof, p, g):
 
 
 # ---------------------------------------------------------------- model
+
+def conv_plan_info(shape, pas):
+    """(tile M, tile N, splits, GEMM M, GEMM N, GEMM K, phases) of one conv pass."""
+    out = (c_i32 * 7)()
+    sh = ConvShape(*shape)
+    call("dc_conv2d_plan_info", ctypes.byref(sh), pas, out)
+    return tuple(out)
+
 
 def link(bytes_per_s=1e9, dt_emul_ns=0, paced=True):
     return Link(float(bytes_per_s), int(dt_emul_ns), 1 if paced else 0)

@@ -132,6 +132,19 @@ extern "C" size_t dc_conv2d_workspace_bytes(const dc_conv_shape *sh) {
     return std::max(w, colsum_ws_bytes((int64_t)g.N * g.P * g.Q, g.K));
 }
 
+extern "C" int dc_conv2d_plan_info(const dc_conv_shape *sh, int pass, int32_t *out) {
+    clear_error();
+    ConvGeom g;
+    DC_TRY(conv_setup(sh, &g));
+    if (pass < 0 || pass > 2 || !out)
+        return fail(DC_EINVAL, "pass must be 0, 1 or 2 and out non-NULL");
+    GemmPlan pl = plan_gemm(g, pass);
+    const int32_t v[7] = {pl.mt, pl.nt, pl.splits, pl.M, pl.Ng, pl.Kg, pl.phases};
+    for (int i = 0; i < 7; ++i)
+        out[i] = v[i];
+    return DC_OK;
+}
+
 extern "C" int dc_conv2d_forward(const dc_conv_shape *sh, const float *x, const float *w, const float *bias, int relu,
                                  float *y, void *ws, size_t ws_bytes, void *stream) {
     clear_error();

@@ -26,6 +26,7 @@
 
 #include <algorithm>
 #include <climits>
+#include <cmath>
 
 namespace dc {
 namespace {
@@ -675,32 +676,37 @@ GemmPlan plan_gemm(const ConvGeom &g, int pass) {
         pl.av = g.K % 4 == 0;
         pl.bv = g.C % 4 == 0;
     }
-    // Pick the tile and split-K factor with the least estimated time: a
-    // workgroup's time grows with its tile area and K range (smaller tiles
-    // run at lower MFMA efficiency), workgroups run ~2 per CU at once on 256
-    // CUs, and a split pays the partial-sum traffic of its reduction.
+    // Pick the tile and split-K factor with the least estimated time.  A CU
+    // that holds c workgroups of this kernel at once keeps its matrix cores
+    // busy a fraction util(c) of the time (one workgroup cannot hide its own
+    // global-load latency); a tile holds at most `occ` workgroups per CU
+    // (registers and LDS); smaller tiles move more bytes per flop (eff); a
+    // split pays for writing and re-reading its partial sums.
     static const int cand[4][2] = {{128, 128}, {128, 64}, {64, 128}, {64, 64}};
-    static const double eff[4] = {1.0, 0.85, 0.85, 0.7};
+    static const double eff[4] = {1.0, 0.9, 0.9, 0.75};
+    static const int occ[4] = {3, 4, 4, 6};
+    auto util = [](double c) { return c >= 3 ? 0.95 : c >= 2 ? 0.75 + 0.2 * (c - 2) : 0.45 + 0.3 * (c - 1); };
     const int ktiles = std::max(1, (pl.Kg + KT - 1) / KT);
     double best = 1e300;
     for (int c = 0; c < 4; ++c) {
         int mt = cand[c][0], nt = cand[c][1];
         int tm = (pl.M + mt - 1) / mt, tn = (pl.Ng + nt - 1) / nt;
         int64_t tiles = (int64_t)tm * tn * pl.phases;
-        for (int sp = 1; sp <= 512; sp *= 2) {
-            if (sp > 1 && (ktiles / sp) < 8)
+        for (int sp = 1; sp <= 1024; sp *= 2) {
+            if (sp > 1 && (ktiles / sp) < 4)
                 break;
             int kps = (ktiles + sp - 1) / sp;
             int spe = (ktiles + kps - 1) / kps;
             int64_t wgs = tiles * spe;
-            int64_t rounds = (wgs + 511) / 512;
-            // cycles: 2*mt*nt*KT*kps flops at 256 flop/clk per CU, 2 WGs sharing a CU
-            double t_main = rounds * 2.0 * (2.0 * mt * nt * KT * kps) / (256.0 * eff[c]) / 2.4e3; // ns
+            double per_cu = std::ceil((double)wgs / 256.0); // workgroups one CU works through
+            double conc = std::min<double>(per_cu, occ[c]);
+            double wg_cycles = 2.0 * mt * nt * KT * kps / (256.0 * eff[c]);
+            double t_main = per_cu * wg_cycles / util(conc) / 2.4; // ns at 2.4 GHz
             double t_red = 0;
             if (spe > 1)
-                t_red = 3000.0 + (double)(spe + 2) * pl.M * pl.Ng * pl.phases * 4.0 / 3000.0; // ns at ~3 TB/s
+                t_red = 4000.0 + 2.0 * (double)(spe + 1) * pl.M * pl.Ng * pl.phases * 4.0 / 4000.0; // ns
             double cost = t_main + t_red;
-            if (cost < best * 0.98) {
+            if (cost < best * 0.97) {
                 best = cost;
                 pl.mt = mt; pl.nt = nt; pl.splits = spe; pl.kt_per_split = kps;
                 pl.tiles_m = tm; pl.tiles_n = tn;

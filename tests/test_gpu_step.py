@@ -55,26 +55,33 @@ def plans_for(L, seed=0):
 PARITY = [("tiny", 4), ("alexnet", 2), ("resnet18", 8), ("resnet50", 2), ("vgg16", 1)]
 
 
-def fp32_spread(spec, onet, x, y, params, g_ref, runs=3):
-    """Per tensor, how far ordinary float32 evaluations of this iteration land from the oracle.
+def fp32_spread(spec, onet, x, y, params, g_ref):
+    """Per tensor, how far float32-grade evaluations of this iteration land from the oracle.
 
-    The yardstick is torch's CPU float32 (an independent library evaluation of
-    the same network), once as is and then with every parameter scaled by
-    (1 + 2^-24 * xi), xi ~ N(0, 1) - a float32 round-off-sized nudge.  Deep
-    ReLU / max-pool / BatchNorm stacks turn such nudges into large gradient
-    changes, because decisions near their thresholds flip; spread[t] is the
-    largest per-tensor distance from the float64 oracle over the runs.
+    Members of the yardstick ensemble:
+    * torch's CPU float32 (an independent library evaluation of the network);
+    * the same with every parameter scaled by (1 + 2^-24 xi), xi ~ N(0, 1);
+    * the float64 oracle with every conv / FC / BN output scaled by
+      (1 + eps xi), eps = 2^-23 and 2^-21: the relative storage and
+      accumulation error of a float32 implementation.
+    Deep ReLU / max-pool / BatchNorm stacks turn such nudges into large,
+    discrete gradient changes (a decision near its threshold flips), so the
+    float64 result is only determined to within this spread.  Returns the
+    per-tensor largest distance from the oracle, for gradients and for the
+    post-step weights w - 0.01 g.
     """
     import torch
     from tests import torch_ref
     rng = np.random.default_rng(1234)
-    runs_g = []
-    for k in range(runs):
-        pp = params.astype(np.float64)
-        if k:
-            pp = pp * (1.0 + 2.0 ** -24 * rng.standard_normal(params.size))
-        runs_g.append(torch_ref.loss_and_grads(spec, onet, x, y, pp, torch.float32)[1])
-    # the same runs' post-step weights, w - 0.01 g, against the oracle's
+    runs_g = [torch_ref.loss_and_grads(spec, onet, x, y, params, torch.float32)[1]]
+    pp = params.astype(np.float64) * (1.0 + 2.0 ** -24 * rng.standard_normal(params.size))
+    runs_g.append(torch_ref.loss_and_grads(spec, onet, x, y, pp, torch.float32)[1])
+    for eps in (2.0 ** -23, 2.0 ** -21):
+        onet.perturb = lambda i, t, eps=eps: t * (1.0 + eps * rng.standard_normal(t.shape))
+        try:
+            runs_g.append(onet.loss_and_grads(x, y, params)[1])
+        finally:
+            onet.perturb = None
     w_ref = params.astype(np.float64) - 0.01 * g_ref
     runs_w = [params.astype(np.float64) - 0.01 * r for r in runs_g]
     spread, spread_w = {}, {}
