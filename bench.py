@@ -45,7 +45,40 @@ def parse():
     ap.add_argument("--compare", default="sequential,lbl", help="other plans to time ('' for none)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-roofline", action="store_true")
+    ap.add_argument("--kernels-only", action="store_true",
+                    help="run each conv / FC pass of the workload once plus a 256 MiB calibration copy "
+                         "(for rocprofv3 --pmc), then exit")
     return ap.parse_args()
+
+
+def calibration_copy(D, nbytes=256 << 20):
+    """dc_copy_grad over nbytes: reads and writes exactly nbytes each (counter scale)."""
+    import torch
+    n = nbytes // 4
+    a = torch.ones(n, device="cuda")
+    b = torch.empty(n, device="cuda")
+    torch.cuda.synchronize()
+    D.call("dc_copy_grad", a.data_ptr(), 0, b.data_ptr(), n, torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+
+
+def traffic_from_profiles(name, batch):
+    """HBM bytes per igemm launch from the committed rocprofv3 counter summary, if it
+    was taken on the current kernel source; else None."""
+    import hashlib
+    src = os.path.join(ROOT, "paper_2101_07968_amd", "csrc", "igemm.hip")
+    path = os.path.join(ROOT, "profiles", f"igemm_{name}_b{batch}_traffic.txt")
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    for line in open(path):
+        if "=" in line and not line.startswith("#"):
+            k, v = line.strip().split("=", 1)
+            kv[k.strip()] = v.strip()
+    sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
+    if kv.get("igemm_source_sha256") != sha:
+        return None
+    return float(kv["hbm_bytes_per_launch"]), float(kv["algorithmic_bytes_per_launch"])
 
 
 def measure_convs(D, PN, ops, hwc, batch, reps=3):
@@ -145,6 +178,12 @@ def main():
     wl = PN.WORKLOADS[name]
     batch = args.batch or wl["batch"]
     ops, hwc, classes = PN.build(name)
+    if args.kernels_only:
+        torch.cuda.set_device(0)
+        calibration_copy(D)
+        measure_convs(D, PN, ops, hwc, batch, reps=1)
+        log("[bench] kernels-only pass done")
+        return
     specs = PN.param_specs(ops, hwc)
     x, y, params = synth.cnn_inputs(wl["seed"], batch, hwc, classes, specs)
     torch.cuda.set_device(0)
@@ -203,6 +242,10 @@ def main():
                 "achieved": round(achieved, 2), "peak": FP32_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(achieved / FP32_MFMA_PEAK_TFLOPS, 4), "traffic": None,
                 "gflop_per_step": round(flops / 1e9, 1), "conv_ms_per_step": round(ms, 3)}
+        tr = traffic_from_profiles(name, batch)
+        if tr is not None:
+            roof["traffic"] = round(tr[0])
+            roof["traffic_algorithmic"] = round(tr[1])
         log(f"[bench] conv GEMMs: {achieved:.1f} TFLOP/s over {flops / 1e9:.0f} GFLOP in {ms:.2f} ms")
         for d in sorted(per, key=lambda d: -d["ms"]):
             log(f"[bench]   {d['pass']:5s} {str(d['shape']):42s} {d['ms']:8.3f} ms {d['tflops']:7.2f} TFLOP/s")

@@ -1,0 +1,135 @@
+"""Summarise rocprofv3 CSV output into the short text reports kept under profiles/.
+
+  python -m paper_2101_07968_amd.profsum stats <kernel_trace.csv> <kernel_stats.csv> --passes-per-conv 4 \
+      --cmd "<command>" > profiles/igemm_<workload>_kernel_stats.md
+  python -m paper_2101_07968_amd.profsum traffic <fetch counter_collection.csv> <write counter_collection.csv> \
+      --workload vgg16 --batch 32 --cmd "<commands>" > profiles/igemm_<workload>_b<batch>_traffic.txt
+
+stats: per-kernel totals from --stats, and the implicit-GEMM window that bench.py
+times live (every igemm / split-K dispatch after the last link-pacing kernel,
+i.e. the per-pass timing loop: 1 warm-up + 3 timed launches per pass) reduced
+to one iteration's worth, for comparison with the bench's conv_ms_per_step.
+
+traffic: FETCH_SIZE / WRITE_SIZE (KiB per dispatch) of the igemm dispatches of a
+`bench.py --kernels-only` run, scaled by what the same counters read for the
+256 MiB calibration copy, against the algorithmic bytes of those launches.
+"""
+from __future__ import annotations
+
+import argparse
+import csv
+import hashlib
+import os
+import re
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+
+
+def short(name):
+    name = name.replace("dc::(anonymous namespace)::", "")
+    name = re.sub(r"\(.*$", "", name) if "igemm" not in name and "splitk" not in name else name.split("(")[0]
+    return name.replace("void ", "")[:80]
+
+
+def is_gemm(name):
+    return "igemm_kernel" in name or "splitk_reduce_kernel" in name
+
+
+def cmd_stats(a):
+    rows = list(csv.DictReader(open(a.stats)))
+    out = ["# rocprofv3 kernel statistics", "", f"Command: `{a.cmd}`", "",
+           "| kernel | calls | total ms | avg us | % |", "|---|---|---|---|---|"]
+    for r in rows[:a.top]:
+        out.append(f"| `{short(r['Name'])}` | {r['Calls']} | {float(r['TotalDurationNs']) / 1e6:.2f} | "
+                   f"{float(r['AverageNs']) / 1e3:.1f} | {float(r['Percentage']):.2f} |")
+    gemm_total = sum(float(r["TotalDurationNs"]) for r in rows if is_gemm(r["Name"]))
+    gemm_calls = sum(int(r["Calls"]) for r in rows if is_gemm(r["Name"]))
+    out += ["", f"All implicit-GEMM + split-K dispatches: {gemm_calls} calls, {gemm_total / 1e6:.2f} ms."]
+    trace = list(csv.DictReader(open(a.trace)))
+    trace.sort(key=lambda r: int(r["Start_Timestamp"]))
+    last_pace = max((i for i, r in enumerate(trace) if "pace_" in r["Kernel_Name"]), default=-1)
+    win = [r for r in trace[last_pace + 1:] if is_gemm(r["Kernel_Name"])]
+    dur = sum(int(r["End_Timestamp"]) - int(r["Start_Timestamp"]) for r in win)
+    per_iter = dur / a.passes_per_conv / 1e6
+    out += ["", "Roofline window (the per-pass timing loop of bench.py, after the last pacing kernel):",
+            f"{len(win)} GEMM dispatches, {dur / 1e6:.2f} ms in all, {per_iter:.3f} ms per iteration "
+            f"({a.passes_per_conv} launches per pass).",
+            f"Mean duration per launch: {dur / max(len(win), 1) / 1e3:.1f} us."]
+    if a.flops:
+        out.append(f"Algorithmic GEMM work per iteration {a.flops:.1f} GFLOP -> "
+                   f"{a.flops / per_iter:.1f} TFLOP/s from these durations.")
+    print("\n".join(out))
+
+
+def read_counter(path, counter):
+    rows = [r for r in csv.DictReader(open(path)) if r["Counter_Name"] == counter]
+    rows.sort(key=lambda r: int(r["Dispatch_Id"]))
+    return rows
+
+
+def conv_bytes(geoms):
+    """Algorithmic bytes of each conv pass launch: every operand read once, the result written once."""
+    out = []
+    for _i, g, first in geoms:
+        n, h, w, c, k, r, s, st, pad = g
+        P, Q = (h + 2 * pad - r) // st + 1, (w + 2 * pad - s) // st + 1
+        x, y, wt = n * h * w * c * 4, n * P * Q * k * 4, k * r * s * c * 4
+        out.append(("fwd", x + wt + y))
+        out.append(("wgrad", x + y + wt))
+        if not first:
+            out.append(("dgrad", y + wt + x))
+    return out
+
+
+def cmd_traffic(a):
+    from . import nets as PN
+    fetch = read_counter(a.fetch, "FETCH_SIZE")
+    write = read_counter(a.write, "WRITE_SIZE")
+    cal_f = [float(r["Counter_Value"]) for r in fetch if "copy_grad_kernel" in r["Kernel_Name"]]
+    cal_w = [float(r["Counter_Value"]) for r in write if "copy_grad_kernel" in r["Kernel_Name"]]
+    known_kib = a.cal_bytes / 1024.0
+    sf, sw = known_kib / cal_f[0], known_kib / cal_w[0]
+    gf = [float(r["Counter_Value"]) for r in fetch if "igemm_kernel" in r["Kernel_Name"]]
+    gw = [float(r["Counter_Value"]) for r in write if "igemm_kernel" in r["Kernel_Name"]]
+    n = len(gf)
+    hbm = (sum(gf) * sf + sum(gw) * sw) * 1024.0 / n
+    ops, hwc, _ = PN.build(a.workload)
+    passes = conv_bytes(PN.conv_geoms(ops, hwc, a.batch))
+    algo = sum(b for _, b in passes) / len(passes)
+    sha = hashlib.sha256(open(os.path.join(HERE, "csrc", "igemm.hip"), "rb").read()).hexdigest()
+    print(f"# HBM traffic of the implicit-GEMM kernel, {a.workload} batch {a.batch}")
+    print(f"# commands: {a.cmd}")
+    print(f"# calibration: {a.cal_bytes} B copy read as FETCH_SIZE {cal_f[0]:.1f} KiB, WRITE_SIZE {cal_w[0]:.1f} KiB")
+    print(f"# igemm dispatches: {n} ({len(passes)} conv/FC passes, each launched twice)")
+    print(f"# raw FETCH_SIZE {sum(gf):.0f} KiB, WRITE_SIZE {sum(gw):.0f} KiB over those dispatches")
+    print(f"fetch_scale={sf:.4f}")
+    print(f"write_scale={sw:.4f}")
+    print(f"hbm_bytes_per_launch={hbm:.0f}")
+    print(f"algorithmic_bytes_per_launch={algo:.0f}")
+    print(f"hbm_over_algorithmic={hbm / algo:.3f}")
+    print(f"igemm_source_sha256={sha}")
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    sub = ap.add_subparsers(dest="what", required=True)
+    s = sub.add_parser("stats")
+    s.add_argument("trace")
+    s.add_argument("stats")
+    s.add_argument("--passes-per-conv", type=int, default=4)
+    s.add_argument("--flops", type=float, default=0.0, help="GFLOP of one iteration's GEMM passes")
+    s.add_argument("--top", type=int, default=25)
+    s.add_argument("--cmd", default="")
+    t = sub.add_parser("traffic")
+    t.add_argument("fetch")
+    t.add_argument("write")
+    t.add_argument("--workload", default="vgg16")
+    t.add_argument("--batch", type=int, default=32)
+    t.add_argument("--cal-bytes", type=int, default=256 << 20)
+    t.add_argument("--cmd", default="")
+    a = ap.parse_args()
+    cmd_stats(a) if a.what == "stats" else cmd_traffic(a)
+
+
+if __name__ == "__main__":
+    main()
