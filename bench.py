@@ -42,7 +42,7 @@ def parse():
     ap.add_argument("--batch", type=int, default=0, help="0 = the workload's own batch")
     ap.add_argument("--link-gbps", default="100", help="emulated link in Gb/s, or 'pcie' for unpaced copies")
     ap.add_argument("--dt-emul-ms", type=float, default=0.0)
-    ap.add_argument("--compare", default="sequential,lbl", help="other plans to time ('' for none)")
+    ap.add_argument("--compare", default="sequential,lbl,ibatch", help="other plans to time ('' for none)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-roofline", action="store_true")
     ap.add_argument("--kernels-only", action="store_true",
@@ -228,7 +228,7 @@ def main():
             f"t_iter {res['t_iter_ms']:.2f} ms vs model {res['t_model_ms']:.2f} ms")
         return res
 
-    fixed = {"sequential": D.dc_plan_sequential(prof), "lbl": D.dc_plan_lbl(prof)}
+    fixed = {"sequential": D.dc_plan_sequential(prof), "lbl": D.dc_plan_lbl(prof), "ibatch": D.dc_plan_ibatch(prof)}
     main_res = run("dp", args.steps, args.warmup)
     others = {}
     for kind in [k for k in args.compare.split(",") if k]:

@@ -216,6 +216,11 @@ int dc_plan(const dc_profile_t *prof, dc_plan_t *out);
  * (every position enabled) decisions, with f_m filled from prof. */
 int dc_plan_sequential(const dc_profile_t *prof, dc_plan_t *out);
 int dc_plan_lbl(const dc_profile_t *prof, dc_plan_t *out);
+/* iBatch, the greedy baseline of Sec. III-C: Algorithm 1 (front-to-back
+ * forward batching; its reverse twin is not given in the paper) and
+ * Algorithm 2 (gradient batching over every second position, keeping the
+ * candidate of least f_m), with f_m filled in.  Same errors as dc_plan. */
+int dc_plan_ibatch(const dc_profile_t *prof, dc_plan_t *out);
 /* Fill t_fwd_ns / t_bwd_ns of a given decision with the cost function f_m. */
 int dc_plan_eval(const dc_profile_t *prof, dc_plan_t *plan);
 
@@ -232,6 +237,10 @@ typedef struct dc_step_stats {
     int64_t t_link_ns;     /* sum of the pull and push segment durations */
     int64_t t_sgd_tail_ns; /* server update after the last push ended (outside t_iter) */
     int64_t t_host_ns;     /* wall time of the whole dc_step call */
+    int64_t t_plan_bwd_ns; /* dc_step_dynamic: host time of the backward DP (0 otherwise) */
+    int64_t t_plan_fwd_ns; /* dc_step_dynamic: host time of the next forward DP (0 otherwise) */
+    int32_t plan_hidden;   /* dc_step_dynamic: bit 0 set if the backward DP ended before the first
+                              pull did, bit 1 if the next forward DP ended before the last push did */
 } dc_step_stats;
 
 /*
@@ -249,6 +258,20 @@ typedef struct dc_step_stats {
  */
 int dc_step(dc_model *m, const dc_batch *b, const dc_plan_t *plan, const dc_link *link,
             void *stream, dc_step_stats *out);
+
+/*
+ * One iteration in DynaComm's run-time mode with the idle-event trigger
+ * (Sec. IV-C): this iteration's pulls and forward pass use plan->p; the
+ * backward decision is computed by the backward DP (Eq. 9, Algorithm 4) on
+ * `prof` while the first pull is in flight, and the forward decision of the
+ * next iteration (Eq. 8, Algorithm 3) while the last push is in flight, so
+ * planning stays off the critical path.  On return plan->g holds the
+ * backward decision that was used and plan->p the decision for the next
+ * call (with t_fwd_ns / t_bwd_ns from f_m).  `prof` is typically refreshed by
+ * dc_profile once per epoch.  Errors as dc_step, plus those of dc_plan.
+ */
+int dc_step_dynamic(dc_model *m, const dc_batch *b, const dc_profile_t *prof, const dc_link *link,
+                    void *stream, dc_plan_t *plan, dc_step_stats *out);
 
 /*
  * Per-layer timestamps of the last dc_step run with DC_OPT_TIMELINE on, in

@@ -285,3 +285,91 @@ def sequential(L):
 def layer_by_layer(L):
     """The layer-by-layer decision [0, 1, ..., L] / [L+1, L, ..., 1]."""
     return [1] * (L - 1)
+
+
+# ---------------------------------------------------------------- iBatch (Sec. III-C)
+#
+# The greedy schedulers DynaComm is compared with.  Readings where the
+# listings leave a case open:
+# * Algorithm 1 fixes D_f[1] by its steps 3-4 (largest first-segment compute,
+#   then cheapest first transfer) but not D_f[2] among the pairs sharing that
+#   D_f[1]; it is chosen by the loop's own rule, least slack
+#   dt + pt(D_f[1]+1..D_f[2]) - fc(1..D_f[1]), ties to the smaller position.
+# * If no pair passes step 2, the whole model is one segment.
+# * If no x qualifies inside the forward loop, the rest of the model is one
+#   segment (j = L); inside the backward loop, the next segment is the single
+#   layer m-1 (its compute is the shortest, so it overruns the least).
+# * Ties of the least-slack choice go to the position met first in the scan
+#   (the smallest x), and ties between Algorithm 2's candidates to the first.
+# * Algorithm 1's reverse twin is not given in the paper; only the printed
+#   front-to-back pass is used.
+
+def ibatch_forward(pt, fc, dt):
+    """Algorithm 1: greedy forward batching.  Returns the decision p (list of L-1 bits)."""
+    L = _check(pt, fc)
+    dt = int(dt)
+    PT, FC = _prefix(pt), _prefix(fc)
+    if L == 1:
+        return []
+    S2 = []
+    for d1 in range(1, L):
+        for d2 in range(d1 + 1, L + 1):
+            if dt + (PT[d2] - PT[d1]) >= FC[d1] - FC[0]:
+                S2.append((d1, d2))
+    if not S2:
+        return [0] * (L - 1)
+    best_fc = max(FC[d1] for d1, _ in S2)
+    S3 = [(d1, d2) for d1, d2 in S2 if FC[d1] == best_fc]
+    best_pull = min(dt + PT[d1] for d1, _ in S3)
+    S4 = [(d1, d2) for d1, d2 in S3 if dt + PT[d1] == best_pull]
+    d1 = S4[0][0]
+    d2 = min((dt + (PT[b] - PT[a]) - (FC[a] - FC[0]), b) for a, b in S4 if a == d1)[1]
+    D = [0, d1, d2]
+    n, m = d1, d2
+    while m != L:
+        opts = [x for x in range(m + 1, L + 1) if dt + (PT[x] - PT[m]) >= FC[m] - FC[n]]
+        if opts:
+            j = min((dt + (PT[x] - PT[m]) - (FC[m] - FC[n]), x) for x in opts)[1]
+        else:
+            j = L
+        n, m = m, j
+        D.append(m)
+    p = [0] * (L - 1)
+    for d in D[1:-1]:
+        p[d - 1] = 1
+    return p
+
+
+def ibatch_backward(bc, gt, dt):
+    """Algorithm 2: greedy gradient batching over every second position n.
+
+    Returns (g, T_backward) with the candidate of least f_m backward time.
+    """
+    L = _check(bc, gt)
+    dt = int(dt)
+    BC, GT = _prefix(bc), _prefix(gt)
+    if L == 1:
+        return [], fm_backward(bc, gt, dt, [])
+    best = None
+    for n in range(2, L + 1):
+        D = [L + 1, n]
+        k, m = 1, n
+        while m != 1:
+            pushed = k * dt + (GT[L] - GT[m - 1])          # gt over layers m..L
+            opts = [x for x in range(1, m) if pushed >= BC[m - 1] - BC[x - 1]]  # bc over x..m-1
+            if opts:
+                j = min((pushed - (BC[m - 1] - BC[x - 1]), x) for x in opts)[1]
+            else:
+                j = m - 1
+            D.append(j)
+            m = j
+            k += 1
+        # positions L+1 > d_1 > ... > 1: segment layers d_{i}-1 .. d_{i+1}; a boundary
+        # between layer d and d-1 (1 < d <= L) is g_k with L - k = d - 1
+        g = [0] * (L - 1)
+        for d in D[1:-1]:
+            g[L - d] = 1
+        t = fm_backward(bc, gt, dt, g)
+        if best is None or t < best[1]:
+            best = (g, t)
+    return best

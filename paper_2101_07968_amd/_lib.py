@@ -63,7 +63,7 @@ class PlanT(ctypes.Structure):
 class StepStats(ctypes.Structure):
     _fields_ = [("loss", c_f32), ("n_pull", c_i32), ("n_push", c_i32), ("t_iter_ns", c_i64), ("t_fwd_ns", c_i64),
                 ("t_bwd_ns", c_i64), ("t_compute_ns", c_i64), ("t_link_ns", c_i64), ("t_sgd_tail_ns", c_i64),
-                ("t_host_ns", c_i64)]
+                ("t_host_ns", c_i64), ("t_plan_bwd_ns", c_i64), ("t_plan_fwd_ns", c_i64), ("plan_hidden", c_i32)]
 
     def as_dict(self):
         return {name: getattr(self, name) for name, _ in self._fields_}
@@ -90,7 +90,9 @@ _SIGS = {
     "dc_plan_sequential": (ctypes.c_int, [_P(ProfileT), _P(PlanT)]),
     "dc_plan_lbl": (ctypes.c_int, [_P(ProfileT), _P(PlanT)]),
     "dc_plan_eval": (ctypes.c_int, [_P(ProfileT), _P(PlanT)]),
+    "dc_plan_ibatch": (ctypes.c_int, [_P(ProfileT), _P(PlanT)]),
     "dc_step": (ctypes.c_int, [c_vp, _P(Batch), _P(PlanT), _P(Link), c_vp, _P(StepStats)]),
+    "dc_step_dynamic": (ctypes.c_int, [c_vp, _P(Batch), _P(ProfileT), _P(Link), c_vp, _P(PlanT), _P(StepStats)]),
     "dc_timeline": (ctypes.c_int, [c_vp, _P(c_i64), ctypes.c_int]),
     "dc_conv2d_workspace_bytes": (c_sz, [_P(ConvShape)]),
     "dc_conv2d_plan_info": (ctypes.c_int, [_P(ConvShape), ctypes.c_int, _P(c_i32)]),
@@ -232,6 +234,10 @@ def dc_plan_lbl(prof):
     return _run_plan("dc_plan_lbl", prof, Plan(prof.L))
 
 
+def dc_plan_ibatch(prof):
+    return _run_plan("dc_plan_ibatch", prof, Plan(prof.L))
+
+
 def dc_plan_eval(prof, p, g):
     return _run_plan("dc_plan_eval", prof, Plan(prof.L, p, g))
 
@@ -317,6 +323,17 @@ class Model:
         c = plan.c()
         call("dc_step", self.h, ctypes.byref(b), ctypes.byref(c), ctypes.byref(lnk), stream_ptr(stream),
              ctypes.byref(st))
+        return st.as_dict()
+
+    def step_dynamic(self, x, y, prof, plan, lnk, stream=None):
+        """dc_step_dynamic: uses plan.p, fills plan.g (used) and plan.p (next call)."""
+        st = StepStats()
+        b = self._batch(x, y)
+        pc = prof.c()
+        c = plan.c()
+        call("dc_step_dynamic", self.h, ctypes.byref(b), ctypes.byref(pc), ctypes.byref(lnk), stream_ptr(stream),
+             ctypes.byref(c), ctypes.byref(st))
+        plan._sync()
         return st.as_dict()
 
     def timeline(self):

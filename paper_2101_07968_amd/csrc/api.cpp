@@ -93,6 +93,15 @@ extern "C" int dc_plan_eval(const dc_profile_t *prof, dc_plan_t *plan) {
     return DC_OK;
 }
 
+extern "C" int dc_plan_ibatch(const dc_profile_t *prof, dc_plan_t *out) {
+    clear_error();
+    DC_TRY(check_profile(prof, out));
+    DC_TRY(plan_ibatch_forward(prof->pt_ns, prof->fc_ns, prof->dt_ns, prof->L, out->p));
+    DC_TRY(plan_ibatch_backward(prof->bc_ns, prof->gt_ns, prof->dt_ns, prof->L, out->g, &out->t_bwd_ns));
+    out->t_fwd_ns = fm_forward(prof->pt_ns, prof->fc_ns, prof->dt_ns, prof->L, out->p);
+    return DC_OK;
+}
+
 static int fixed_plan(const dc_profile_t *prof, dc_plan_t *out, uint8_t v) {
     clear_error();
     DC_TRY(check_profile(prof, out));

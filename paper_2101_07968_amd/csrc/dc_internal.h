@@ -97,6 +97,8 @@ int plan_forward(const int64_t *pt, const int64_t *fc, int64_t dt, int L, uint8_
                  int64_t *t_fwd);
 int plan_backward(const int64_t *bc, const int64_t *gt, int64_t dt, int L, uint8_t *g,
                   int64_t *t_bwd);
+int plan_ibatch_forward(const int64_t *pt, const int64_t *fc, int64_t dt, int L, uint8_t *p);
+int plan_ibatch_backward(const int64_t *bc, const int64_t *gt, int64_t dt, int L, uint8_t *g, int64_t *t_bwd);
 int64_t fm_forward(const int64_t *pt, const int64_t *fc, int64_t dt, int L, const uint8_t *p);
 int64_t fm_backward(const int64_t *bc, const int64_t *gt, int64_t dt, int L, const uint8_t *g);
 

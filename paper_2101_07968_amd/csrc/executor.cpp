@@ -153,9 +153,15 @@ size_t seg_bytes(const dc_model *m, Seg s, size_t *off) {
 
 using namespace dc;
 
-extern "C" int dc_step(dc_model *m, const dc_batch *b, const dc_plan_t *plan, const dc_link *link, void *stream,
-                       dc_step_stats *out) {
-    clear_error();
+namespace dc {
+namespace {
+
+// The body of dc_step and dc_step_dynamic.  With `prof` non-null the backward
+// decision is planned after the forward work is enqueued (while the first
+// pull is in flight) and the next forward decision before the last push is
+// awaited, both written into `plan`.
+int step_impl(dc_model *m, const dc_batch *b, dc_plan_t *plan, const dc_profile_t *prof, const dc_link *link,
+              void *stream, dc_step_stats *out) {
     const auto t_host0 = Clock::now();
     if (!m)
         return fail(DC_EINVAL, "model is NULL");
@@ -165,12 +171,15 @@ extern "C" int dc_step(dc_model *m, const dc_batch *b, const dc_plan_t *plan, co
     DC_TRY(check_link(link));
     if (!plan || plan->L != m->L || (m->L > 1 && (!plan->p || !plan->g)))
         return fail(DC_EINVAL, "plan is for L=%d, the model has L=%d", plan ? plan->L : -1, m->L);
+    if (prof && (prof->L != m->L || !prof->pt_ns || !prof->fc_ns || !prof->bc_ns || !prof->gt_ns))
+        return fail(DC_EINVAL, "profile does not match the model");
     const int L = m->L;
     hipStream_t cs = static_cast<hipStream_t>(stream);
     const auto pulls = pull_segs(plan, L);
-    const auto pushes = push_segs(plan, L);
     const Clock::time_point deadline = t_host0 + std::chrono::microseconds((int64_t)(m->timeout_s * 1e6));
     m->timeline_valid = false;
+    int64_t t_plan_bwd = 0, t_plan_fwd = 0;
+    int32_t hidden = 0;
 
     // pull stream
     DC_HIP(hipEventRecord(m->ev_t0, m->pull_s));
@@ -193,6 +202,15 @@ extern "C" int dc_step(dc_model *m, const dc_batch *b, const dc_plan_t *plan, co
         if (m->timeline || l == L)
             DC_HIP(hipEventRecord(m->ev_fwd_end[l], cs));
     }
+    if (prof) {
+        // idle-event trigger: the backward plan while the first pull is in flight
+        const auto t0 = Clock::now();
+        DC_TRY(plan_backward(prof->bc_ns, prof->gt_ns, prof->dt_ns, L, plan->g, &plan->t_bwd_ns));
+        t_plan_bwd = ns_since(t0);
+        if (hipEventQuery(m->ev_pull_done[0]) == hipErrorNotReady)
+            hidden |= 1;
+    }
+    const auto pushes = push_segs(plan, L);
     // backward, closing push segments as their lowest layer finishes
     size_t k = 0;
     for (int l = L; l >= 1; --l) {
@@ -217,6 +235,16 @@ extern "C" int dc_step(dc_model *m, const dc_batch *b, const dc_plan_t *plan, co
     // parameter server: update each range as soon as it has landed
     Clock::time_point t_last_push{};
     for (size_t i = 0; i < pushes.size(); ++i) {
+        if (prof && i + 1 == pushes.size()) {
+            // idle-event trigger: the next forward plan during the last push
+            const auto t0 = Clock::now();
+            int64_t t_fwd;
+            DC_TRY(plan_forward(prof->pt_ns, prof->fc_ns, prof->dt_ns, L, plan->p, &t_fwd));
+            plan->t_fwd_ns = t_fwd;
+            t_plan_fwd = ns_since(t0);
+            if (hipEventQuery(m->ev_push_done[i]) == hipErrorNotReady)
+                hidden |= 2;
+        }
         DC_TRY(wait_event(m->ev_push_done[i], deadline));
         if (i + 1 == pushes.size())
             t_last_push = Clock::now();
@@ -247,6 +275,9 @@ extern "C" int dc_step(dc_model *m, const dc_batch *b, const dc_plan_t *plan, co
         out->t_link_ns = link_ns;
         out->t_compute_ns = -1;
         out->t_sgd_tail_ns = sgd_tail;
+        out->t_plan_bwd_ns = t_plan_bwd;
+        out->t_plan_fwd_ns = t_plan_fwd;
+        out->plan_hidden = hidden;
     }
     if (m->timeline) {
         m->timeline_ns.assign(8 * (size_t)L, 0);
@@ -286,9 +317,28 @@ extern "C" int dc_step(dc_model *m, const dc_batch *b, const dc_plan_t *plan, co
         if (out)
             out->t_compute_ns = comp;
     }
+    if (prof) // f_m of the decisions now held in plan (p for the next call, g just used)
+        plan->t_bwd_ns = fm_backward(prof->bc_ns, prof->gt_ns, prof->dt_ns, L, plan->g);
     if (out)
         out->t_host_ns = ns_since(t_host0);
     return DC_OK;
+}
+
+} // namespace
+} // namespace dc
+
+extern "C" int dc_step(dc_model *m, const dc_batch *b, const dc_plan_t *plan, const dc_link *link, void *stream,
+                       dc_step_stats *out) {
+    clear_error();
+    return step_impl(m, b, const_cast<dc_plan_t *>(plan), nullptr, link, stream, out);
+}
+
+extern "C" int dc_step_dynamic(dc_model *m, const dc_batch *b, const dc_profile_t *prof, const dc_link *link,
+                               void *stream, dc_plan_t *plan, dc_step_stats *out) {
+    clear_error();
+    if (!prof)
+        return fail(DC_EINVAL, "profile is NULL");
+    return step_impl(m, b, plan, prof, link, stream, out);
 }
 
 extern "C" int dc_timeline(const dc_model *m, int64_t *out, int n) {

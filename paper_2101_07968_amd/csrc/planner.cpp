@@ -10,6 +10,7 @@
 // upwards, so ties keep the smallest split point and the fewest segments.
 #include "dc_internal.h"
 
+#include <algorithm>
 #include <climits>
 #include <vector>
 
@@ -150,6 +151,112 @@ int plan_backward(const int64_t *bc, const int64_t *gt, int64_t dt, int L, uint8
         cl = L - tmp + 1;
     }
     *t_bwd = t;
+    return DC_OK;
+}
+
+// iBatch, the greedy baseline the paper compares against (Sec. III-C,
+// Algorithms 1 and 2).  Open cases are read as follows: the second position of
+// Algorithm 1 is chosen, among the pairs sharing the selected first position,
+// by the loop's least-slack rule; with no qualifying pair the model is one
+// segment; with no qualifying position the forward loop sends the rest as one
+// segment and the backward loop the single next layer; slack ties go to the
+// position met first in the scan, candidate ties to the first candidate.
+int plan_ibatch_forward(const int64_t *pt, const int64_t *fc, int64_t dt, int L, uint8_t *p) {
+    std::vector<int64_t> PT, FC;
+    if (L < 1 || !prefix_sums(pt, L, PT) || !prefix_sums(fc, L, FC) || !bound_ok(L, dt, PT[L], FC[L]))
+        return fail(DC_EINVAL, "invalid forward costs");
+    for (int l = 0; l < L - 1; ++l)
+        p[l] = 0;
+    if (L == 1)
+        return DC_OK;
+    // steps 1-4: the first two positions
+    int d1 = -1;
+    int64_t best_fc = -1, best_pull = INF;
+    for (int a = 1; a < L; ++a) {
+        bool any = false;
+        for (int b = a + 1; b <= L && !any; ++b)
+            any = dt + (PT[b] - PT[a]) >= FC[a];
+        if (!any)
+            continue;
+        const int64_t f = FC[a], pull = dt + PT[a];
+        if (f > best_fc || (f == best_fc && pull < best_pull)) {
+            best_fc = f;
+            best_pull = pull;
+            d1 = a;
+        }
+    }
+    if (d1 < 0)
+        return DC_OK; // nothing qualifies: one segment
+    int d2 = -1;
+    int64_t best_slack = INF;
+    for (int b = d1 + 1; b <= L; ++b) {
+        const int64_t slack = dt + (PT[b] - PT[d1]) - FC[d1];
+        if (slack >= 0 && slack < best_slack) {
+            best_slack = slack;
+            d2 = b;
+        }
+    }
+    if (d1 <= L - 1)
+        p[d1 - 1] = 1;
+    int n = d1, m = d2;
+    while (m != L) {
+        p[m - 1] = 1;
+        const int64_t need = FC[m] - FC[n];
+        int j = L;
+        int64_t bs = INF;
+        for (int x = m + 1; x <= L; ++x) {
+            const int64_t slack = dt + (PT[x] - PT[m]) - need;
+            if (slack >= 0 && slack < bs) {
+                bs = slack;
+                j = x;
+            }
+        }
+        n = m;
+        m = j;
+    }
+    return DC_OK;
+}
+
+int plan_ibatch_backward(const int64_t *bc, const int64_t *gt, int64_t dt, int L, uint8_t *g, int64_t *t_bwd) {
+    std::vector<int64_t> BC, GT;
+    if (L < 1 || !prefix_sums(bc, L, BC) || !prefix_sums(gt, L, GT) || !bound_ok(L, dt, BC[L], GT[L]))
+        return fail(DC_EINVAL, "invalid backward costs");
+    std::vector<uint8_t> cand(L > 1 ? L - 1 : 1), best(L > 1 ? L - 1 : 1, 0);
+    int64_t best_t = INF;
+    if (L == 1) {
+        *t_bwd = fm_backward(bc, gt, dt, L, best.data());
+        return DC_OK;
+    }
+    for (int n = 2; n <= L; ++n) {
+        std::fill(cand.begin(), cand.end(), 0);
+        int m = n, k = 1;
+        // position m (1 < m <= L) is the boundary between layer m and m-1: g_{L-m+1}
+        for (;;) {
+            cand[L - m] = 1;
+            const int64_t pushed = (int64_t)k * dt + (GT[L] - GT[m - 1]);
+            int j = m - 1;
+            int64_t bs = INF;
+            for (int x = 1; x < m; ++x) {
+                const int64_t slack = pushed - (BC[m - 1] - BC[x - 1]);
+                if (slack >= 0 && slack < bs) {
+                    bs = slack;
+                    j = x;
+                }
+            }
+            m = j;
+            ++k;
+            if (m == 1)
+                break;
+        }
+        const int64_t t = fm_backward(bc, gt, dt, L, cand.data());
+        if (t < best_t) {
+            best_t = t;
+            best = cand;
+        }
+    }
+    for (int l = 0; l < L - 1; ++l)
+        g[l] = best[l];
+    *t_bwd = best_t;
     return DC_OK;
 }
 

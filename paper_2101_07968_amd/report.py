@@ -31,7 +31,8 @@ def run_case(D, PN, synth, torch, name, rate_bps, paced, steps, lbl_limit_s=6.0)
     t0 = time.perf_counter()
     dp = D.dc_plan(prof)
     t_plan = (time.perf_counter() - t0) * 1e6
-    plans = {"dp": dp, "sequential": D.dc_plan_sequential(prof), "lbl": D.dc_plan_lbl(prof)}
+    plans = {"dp": dp, "sequential": D.dc_plan_sequential(prof), "lbl": D.dc_plan_lbl(prof),
+             "ibatch": D.dc_plan_ibatch(prof)}
     res = {"workload": name, "batch": wl["batch"], "L": model.L,
            "link": f"{rate_bps * 8 / 1e9:g} Gb/s" if paced else "unpaced",
            "p": dp.decisions()[0], "g": dp.decisions()[1], "t_plan_us": round(t_plan, 1),
@@ -39,7 +40,7 @@ def run_case(D, PN, synth, torch, name, rate_bps, paced, steps, lbl_limit_s=6.0)
            "pt_ms": round(float(prof.pt.sum()) / 1e6, 3), "dt_us": round(prof.dt / 1e3, 1)}
     for key, pl in plans.items():
         t_model_s = (pl.t_fwd_ns + pl.t_bwd_ns) / 1e9
-        if key == "lbl" and t_model_s > lbl_limit_s:
+        if key in ("lbl", "ibatch") and t_model_s > lbl_limit_s:
             res[key] = {"t_model_ms": round(t_model_s * 1e3, 3), "skipped": True}
             continue
         model.ps_write(params)
@@ -67,6 +68,76 @@ def run_case(D, PN, synth, torch, name, rate_bps, paced, steps, lbl_limit_s=6.0)
     return res
 
 
+def adapt(D, PN, synth, torch, name, rates_gbps, steps):
+    """Dynamic adaptation: the link changes mid-run; compare keeping the old
+    profile and plan with re-profiling and re-planning (Sec. IV-C cadence).
+    Runs through dc_step_dynamic (planning in the idle windows)."""
+    wl = PN.WORKLOADS[name]
+    ops, hwc, classes = PN.build(name)
+    x, y, params = synth.cnn_inputs(wl["seed"], wl["batch"], hwc, classes, PN.param_specs(ops, hwc))
+    model = D.Model(ops, wl["batch"], hwc, classes)
+    model.ps_write(params)
+    xd, yd = torch.from_numpy(x).cuda(), torch.from_numpy(y).cuda()
+    out = []
+    prof = None
+    for phase, g in enumerate(rates_gbps):
+        lnk = D.link(g * 1e9 / 8, 0, paced=True)
+        for fresh in ((False, True) if phase else (True,)):
+            if fresh:
+                t0 = time.perf_counter()
+                prof = model.profile(xd, yd, lnk, reps=2)
+                t_prof = time.perf_counter() - t0
+            plan = D.dc_plan(prof)
+            its = []
+            for _ in range(steps):
+                st = model.step_dynamic(xd, yd, prof, plan, lnk)
+                its.append(st["t_iter_ns"])
+            # what the plan in use costs on the link actually present
+            truth = model.profile(xd, yd, lnk, reps=1) if not fresh else prof
+            ev = D.dc_plan_eval(truth, *plan.decisions())
+            best = D.dc_plan(truth)
+            out.append({"link_gbps": g, "profile": "re-profiled" if fresh else "stale", "p": plan.decisions()[0],
+                        "g": plan.decisions()[1], "t_iter_ms": round(float(np.mean(its)) / 1e6, 2),
+                        "f_m_ms": round((ev.t_fwd_ns + ev.t_bwd_ns) / 1e6, 2),
+                        "best_f_m_ms": round((best.t_fwd_ns + best.t_bwd_ns) / 1e6, 2),
+                        "plan_hidden": st["plan_hidden"], "t_plan_us": round((st["t_plan_fwd_ns"] +
+                                                                            st["t_plan_bwd_ns"]) / 1e3, 1),
+                        "t_profile_s": round(t_prof, 3) if fresh else None})
+            print(json.dumps(out[-1]), file=sys.stderr, flush=True)
+    model.close()
+    lines = ["| link (Gb/s) | profile | pull / push segments | measured t_iter (ms) | f_m of plan in use (ms) | "
+             "f_m of the best plan (ms) | planning (us, hidden) |", "|---|---|---|---|---|---|---|"]
+    for o in out:
+        lines.append(f"| {o['link_gbps']:g} | {o['profile']} | {sum(o['p']) + 1} / {sum(o['g']) + 1} | "
+                     f"{o['t_iter_ms']:.2f} | {o['f_m_ms']:.2f} | {o['best_f_m_ms']:.2f} | "
+                     f"{o['t_plan_us']:.0f} ({'yes' if o['plan_hidden'] == 3 else 'no'}) |")
+    return "\n".join(lines)
+
+
+def planner_scaling(D, synth, Ls, reps=20):
+    """Host time of the DP (Eq. 8 + 9) and of iBatch (Algorithms 1 + 2) against L on
+    generated profiles (the study of Fig. 12 / Table I), median of `reps` calls,
+    minus the median time of a one-layer call (the ctypes round trip)."""
+    def med(f, prof):
+        ts = []
+        for _ in range(reps):
+            t0 = time.perf_counter_ns()
+            f(prof)
+            ts.append(time.perf_counter_ns() - t0)
+        return float(np.median(ts))
+    one = D.Profile(*synth.random_profile(0, 1)[:4], 0)
+    base = min(med(D.dc_plan, one), med(D.dc_plan_ibatch, one))
+    lines = ["| L | DP forward + backward (us) | iBatch forward + backward (us) |", "|---|---|---|"]
+    for L in Ls:
+        pt, fc, bc, gt, dt = synth.random_profile(1000 + L, L, hi=10 ** 7, dt_hi=10 ** 6)
+        prof = D.Profile(pt, fc, bc, gt, dt)
+        a = max(0.0, med(D.dc_plan, prof) - base) / 1e3
+        b = max(0.0, med(D.dc_plan_ibatch, prof) - base) / 1e3
+        lines.append(f"| {L} | {a:.1f} | {b:.1f} |")
+        print(lines[-1], file=sys.stderr, flush=True)
+    return "\n".join(lines)
+
+
 def row(r):
     def cell(k):
         v = r.get(k, {})
@@ -74,13 +145,14 @@ def row(r):
             return f"model {v['t_model_ms']:.1f}"
         return f"{v['t_iter_ms']:.1f} / {v['t_model_ms']:.1f}"
     return (f"| {r['workload']} | {r['batch']} | {r['link']} | {cell('dp')} | {cell('sequential')} | {cell('lbl')} | "
+            f"{cell('ibatch')} | "
             f"{r['dp']['images_per_s']:.2f} | {100 * r['reduced_vs_sequential']:.1f}% | {r['dp']['model_err'] * 100:.2f}% | "
             f"{r['dp']['n_pull']}/{r['dp']['n_push']} | {r['fc_ms']:.1f}+{r['bc_ms']:.1f} | {r['dt_us']:.0f} |")
 
 
-HEADER = ("| workload | batch | link | DP t_iter / f_m (ms) | sequential (ms) | LBL (ms) | DP img/s | "
+HEADER = ("| workload | batch | link | DP t_iter / f_m (ms) | sequential (ms) | LBL (ms) | iBatch (ms) | DP img/s | "
           "time saved vs sequential | DP model error | pull/push segments | fc+bc (ms) | dt (us) |\n"
-          "|---|---|---|---|---|---|---|---|---|---|---|---|")
+          "|---|---|---|---|---|---|---|---|---|---|---|---|---|")
 
 
 def main():
@@ -88,6 +160,10 @@ def main():
     ap.add_argument("--only", default="tiny,alexnet,resnet18,vgg16,resnet50")
     ap.add_argument("--vgg-sweep", action="store_true", help="VGG-16 at 0.1, 1, 10, 100 Gb/s and unpaced")
     ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--adapt", default="", help="workload for the link-change scenario, e.g. resnet50")
+    ap.add_argument("--adapt-rates", default="100,10,100", help="Gb/s of the successive phases")
+    ap.add_argument("--planner-scaling", action="store_true", help="DP vs iBatch planning time against L")
+    ap.add_argument("--batch-sweep", default="", help="workload:b1,b2,... at its own link, e.g. resnet50:16,32,64")
     ap.add_argument("--out", default="")
     a = ap.parse_args()
     import torch
@@ -99,12 +175,27 @@ def main():
     if a.vgg_sweep:
         cases = [c for c in cases if c[0] != "vgg16"]
         cases += [("vgg16", g * 1e9 / 8, True) for g in (0.1, 1, 10, 100)] + [("vgg16", 0, False)]
+    if a.adapt or a.planner_scaling:
+        cases = []
     rows = []
     for name, rate, paced in cases:
         r = run_case(D, PN, synth, torch, name, rate, paced, a.steps)
         print(json.dumps(r), file=sys.stderr, flush=True)
         rows.append(r)
-    text = HEADER + "\n" + "\n".join(row(r) for r in rows)
+    if a.batch_sweep:
+        name, bs = a.batch_sweep.split(":")
+        base = dict(PN.WORKLOADS[name])
+        for b in bs.split(","):
+            PN.WORKLOADS[name] = dict(base, batch=int(b))
+            r = run_case(D, PN, synth, torch, name, base["link"], True, a.steps)
+            print(json.dumps(r), file=sys.stderr, flush=True)
+            rows.append(r)
+        PN.WORKLOADS[name] = base
+    text = HEADER + "\n" + "\n".join(row(r) for r in rows) if rows else ""
+    if a.planner_scaling:
+        text = planner_scaling(D, synth, [4, 8, 16, 18, 50, 100, 160, 200, 300])
+    if a.adapt:
+        text = adapt(D, PN, synth, torch, a.adapt, [float(g) for g in a.adapt_rates.split(",")], a.steps)
     print(text)
     if a.out:
         with open(a.out, "w") as f:

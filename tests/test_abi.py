@@ -144,3 +144,26 @@ def test_model_validation_rejects_bad_descriptions():
     # ADD of different shapes
     assert _create([conv, (D.DC_OP_ADD, 1, 1, 0, 0, 0, 0, 0, 0, 0)])[0] == D.DC_EINVAL
     assert b"ADD" in D.lib().dc_last_error()
+
+
+@pytest.mark.parametrize("block", range(10))
+def test_ibatch_bit_exact(block):
+    for i in range(100):
+        seed = 90000 + block * 1000 + i
+        L = 1 + seed % 18
+        hi = (10, 80, 1000, 10 ** 6)[seed % 4]
+        pt, fc, bc, gt, dt = synth.random_profile(seed, L, hi=hi, dt_hi=hi // 2 + 1)
+        plan = D.dc_plan_ibatch(D.Profile(pt, fc, bc, gt, dt))
+        p, g = plan.decisions()
+        assert p == OP.ibatch_forward(pt, fc, dt)
+        og, tb = OP.ibatch_backward(bc, gt, dt)
+        assert g == og and plan.t_bwd_ns == tb
+        assert plan.t_fwd_ns == OP.fm_forward(pt, fc, dt, p)
+
+
+def test_ibatch_hand_fixture_through_abi():
+    d = json.load(open(os.path.join(ROOT, "tests", "golden", "ibatch_hand.json")))
+    f, b = d["forward"], d["backward"]
+    plan = D.dc_plan_ibatch(D.Profile(f["pt"], f["fc"], b["bc"], b["gt"], 3))
+    assert plan.decisions() == (f["p"], b["g"])
+    assert (plan.t_fwd_ns, plan.t_bwd_ns) == (f["T"], b["T"])

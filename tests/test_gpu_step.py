@@ -241,3 +241,48 @@ def test_watchdog_times_out_and_gpu_drains():
     model.set_option(D.DC_OPT_TIMEOUT_S, 60)
     st = model.step(xd, yd, D.Plan(4), UNPACED)
     assert np.isfinite(st["loss"])
+
+
+def test_dynamic_step_plans_in_idle_windows():
+    """dc_step_dynamic (idle-event trigger, Sec. IV-C): same decisions as dc_plan,
+    same numbers as dc_step, and planning finished while a transfer was in flight."""
+    model, onet, xd, yd, x, y, params = setup_model("resnet18", 16, seed=5)
+    lnk = D.link(5e8, 0, paced=True)
+    prof = model.profile(xd, yd, lnk, reps=2)
+    ref = D.dc_plan(prof)
+    model.ps_write(params)
+    st_ref = model.step(xd, yd, ref, lnk)
+    p_ref, g_ref = model.ps_read()
+    plan = D.Plan(model.L)                      # first call: sequential forward, backward planned on the fly
+    plan.p[:] = ref.p
+    model.ps_write(params)
+    st = model.step_dynamic(xd, yd, prof, plan, lnk)
+    p_dyn, g_dyn = model.ps_read()
+    assert plan.decisions() == ref.decisions()
+    assert st["loss"] == st_ref["loss"]
+    np.testing.assert_array_equal(g_dyn, g_ref)
+    np.testing.assert_array_equal(p_dyn, p_ref)
+    assert st["plan_hidden"] == 3, st
+    assert 0 < st["t_plan_bwd_ns"] and 0 < st["t_plan_fwd_ns"]
+    # a second call reuses the decision the first one planned for it
+    st2 = model.step_dynamic(xd, yd, prof, plan, lnk)
+    assert plan.decisions() == ref.decisions() and st2["n_pull"] == st["n_pull"]
+
+
+def test_replanning_follows_the_link():
+    """Re-profiling after the link changes (once-per-epoch cadence, Sec. IV-C) re-plans
+    exactly as the oracle does on the new profile."""
+    model, onet, xd, yd, x, y, params = setup_model("resnet18", 32, seed=6)
+    plans = {}
+    for rate in (1.25e10 / 8 * 8, 1.25e8):
+        lnk = D.link(rate, 0, paced=True)
+        prof = model.profile(xd, yd, lnk, reps=2)
+        plan = D.dc_plan(prof)
+        p_ref, _, _, _ = OP.forward_dp(prof.pt.tolist(), prof.fc.tolist(), prof.dt)
+        g_ref, _, _, _ = OP.backward_dp(prof.bc.tolist(), prof.gt.tolist(), prof.dt)
+        assert plan.decisions() == (p_ref, g_ref)
+        ratio = prof.pt.sum() / np.array(model.layer_bytes()).sum()
+        assert abs(ratio * rate / 1e9 - 1) < 1e-3
+        plans[rate] = plan.decisions()
+    # the fast link is worth splitting, the slow one barely
+    assert sum(plans[1.25e10 / 8 * 8][0]) >= sum(plans[1.25e8][0])

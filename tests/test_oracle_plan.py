@@ -199,3 +199,33 @@ def test_planted_mistakes_are_caught():
     for bad in (fm_no_dt, fm_off_by_one):
         assert any(bad(pt, fc, dt, list(b)) != closed_form_forward(pt, fc, dt, list(b))
                    for b in itertools.product((0, 1), repeat=2))
+
+
+def test_ibatch_hand_worked():
+    d = _load("ibatch_hand.json")
+    f = d["forward"]
+    p = P.ibatch_forward(f["pt"], f["fc"], f["dt"])
+    assert p == f["p"] and P.fm_forward(f["pt"], f["fc"], f["dt"], p) == f["T"]
+    assert P.forward_dp(f["pt"], f["fc"], f["dt"])[1] == f["dp_T"]
+    b = d["backward"]
+    g, t = P.ibatch_backward(b["bc"], b["gt"], b["dt"])
+    assert g == b["g"] and t == b["T"]
+
+
+@pytest.mark.parametrize("seed", range(150))
+def test_ibatch_never_beats_the_dp(seed):
+    """The DP is optimal (Sec. IV-B-3), so a greedy decision can only tie or lose."""
+    L = 1 + seed % 14
+    pt, fc, bc, gt, dt = synth.random_profile(20000 + seed, L, hi=500, dt_hi=200)
+    p = P.ibatch_forward(pt, fc, dt)
+    g, tb = P.ibatch_backward(bc, gt, dt)
+    assert len(p) == L - 1 and len(g) == L - 1
+    assert P.forward_dp(pt, fc, dt)[1] <= P.fm_forward(pt, fc, dt, p)
+    assert P.backward_dp(bc, gt, dt)[1] <= tb == P.fm_backward(bc, gt, dt, g)
+
+
+def test_ibatch_fallbacks():
+    # no pair passes step 2 (transfers are free, compute is not): one segment
+    assert P.ibatch_forward([0, 0, 0], [5, 5, 5], 0) == [0, 0]
+    # a single layer has nothing to decide
+    assert P.ibatch_forward([3], [4], 1) == [] and P.ibatch_backward([3], [4], 1) == ([], 8)
