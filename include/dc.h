@@ -239,8 +239,8 @@ typedef struct dc_step_stats {
     int64_t t_host_ns;     /* wall time of the whole dc_step call */
     int64_t t_plan_bwd_ns; /* dc_step_dynamic: host time of the backward DP (0 otherwise) */
     int64_t t_plan_fwd_ns; /* dc_step_dynamic: host time of the next forward DP (0 otherwise) */
-    int32_t plan_hidden;   /* dc_step_dynamic: bit 0 set if the backward DP ended before the first
-                              pull did, bit 1 if the next forward DP ended before the last push did */
+    int32_t plan_hidden;   /* dc_step_dynamic: bit 0 set if the backward DP ended before the forward
+                              pass did, bit 1 if the next forward DP ended before the last push did */
 } dc_step_stats;
 
 /*
@@ -263,7 +263,8 @@ int dc_step(dc_model *m, const dc_batch *b, const dc_plan_t *plan, const dc_link
  * One iteration in DynaComm's run-time mode with the idle-event trigger
  * (Sec. IV-C): this iteration's pulls and forward pass use plan->p; the
  * backward decision is computed by the backward DP (Eq. 9, Algorithm 4) on
- * `prof` while the first pull is in flight, and the forward decision of the
+ * `prof` while the pulls and the forward pass are in flight (the host has
+ * already enqueued them), and the forward decision of the
  * next iteration (Eq. 8, Algorithm 3) while the last push is in flight, so
  * planning stays off the critical path.  On return plan->g holds the
  * backward decision that was used and plan->p the decision for the next

@@ -157,9 +157,9 @@ namespace dc {
 namespace {
 
 // The body of dc_step and dc_step_dynamic.  With `prof` non-null the backward
-// decision is planned after the forward work is enqueued (while the first
-// pull is in flight) and the next forward decision before the last push is
-// awaited, both written into `plan`.
+// decision is planned after the forward work is enqueued (while the pulls and
+// the forward pass are in flight) and the next forward decision before the
+// last push is awaited, both written into `plan`.
 int step_impl(dc_model *m, const dc_batch *b, dc_plan_t *plan, const dc_profile_t *prof, const dc_link *link,
               void *stream, dc_step_stats *out) {
     const auto t_host0 = Clock::now();
@@ -207,7 +207,9 @@ int step_impl(dc_model *m, const dc_batch *b, dc_plan_t *plan, const dc_profile_
         const auto t0 = Clock::now();
         DC_TRY(plan_backward(prof->bc_ns, prof->gt_ns, prof->dt_ns, L, plan->g, &plan->t_bwd_ns));
         t_plan_bwd = ns_since(t0);
-        if (hipEventQuery(m->ev_pull_done[0]) == hipErrorNotReady)
+        // the backward kernels are needed once the forward pass (already
+        // enqueued) ends; planning before that costs the GPU nothing
+        if (hipEventQuery(m->ev_fwd_end[L]) == hipErrorNotReady)
             hidden |= 1;
     }
     const auto pushes = push_segs(plan, L);
