@@ -61,7 +61,8 @@ enum {
     DC_OP_RELU = 4,
     DC_OP_MAXPOOL = 5, /* r x s window, stride, padding; padded positions never win */
     DC_OP_GAP = 6,     /* global average pooling to N x 1 x 1 x C */
-    DC_OP_ADD = 7      /* elementwise sum of in0 and in1 (residual connection) */
+    DC_OP_ADD = 7,     /* elementwise sum of in0 and in1 (residual connection) */
+    DC_OP_CONCAT = 8   /* channel concatenation of in0, in1 and, if not -1, in2 and in3 */
 };
 
 /*
@@ -70,8 +71,8 @@ enum {
  * layer (1-based): layers are contiguous and non-decreasing along the list,
  * and each layer's first operation is a CONV or FC.  Following Sec. III-A, a
  * layer is one weighted operation with the parameter-less operations that
- * follow it; branches at the same depth (a residual block's projection) may
- * share a layer.  A layer's parameters are one contiguous byte range of the
+ * follow it; branches at the same depth (a residual block's projection, the
+ * parallel convs of an Inception module) may share a layer.  A layer's parameters are one contiguous byte range of the
  * parameter server: its operations in order, each weight then bias
  * (CONV/FC) or gamma then beta (BN).  The last operation must produce
  * N x 1 x 1 x classes logits; the loss is the batch mean of the softmax
@@ -81,12 +82,14 @@ typedef struct dc_op_desc {
     int32_t kind;    /* DC_OP_* */
     int32_t layer;   /* planner layer, 1..L */
     int32_t in0;     /* input tensor id (< own id) */
-    int32_t in1;     /* DC_OP_ADD: second input tensor id; otherwise -1 */
+    int32_t in1;     /* DC_OP_ADD / DC_OP_CONCAT: second input tensor id; otherwise -1 */
     int32_t out_ch;  /* CONV: output channels; FC: output features */
     int32_t r, s;    /* CONV / MAXPOOL window */
     int32_t stride;  /* CONV / MAXPOOL */
     int32_t pad;     /* CONV / MAXPOOL */
     int32_t bias;    /* CONV / FC: 1 if the op has a bias */
+    int32_t in2;     /* DC_OP_CONCAT: third input tensor id or -1; otherwise -1 */
+    int32_t in3;     /* DC_OP_CONCAT: fourth input tensor id or -1; otherwise -1 */
 } dc_op_desc;
 
 typedef struct dc_model dc_model;

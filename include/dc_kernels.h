@@ -80,6 +80,14 @@ int dc_add_forward(const float *a, const float *b, int relu, float *y, int64_t n
 /* dx (+)= dy over n floats. */
 int dc_copy_grad(const float *dy, int accumulate, float *dx, int64_t n, void *stream);
 
+/* Channel concatenation of NHWC tensors viewed as [rows][channels]:
+ * forward y[m][off + c] = x[m][c] for c < c_in, y having c_out channels;
+ * backward dx[m][c] (+)= dy[m][off + c]. */
+int dc_concat_forward(int64_t rows, int32_t c_in, int32_t c_out, int32_t off, const float *x, float *y,
+                      void *stream);
+int dc_concat_backward(int64_t rows, int32_t c_in, int32_t c_out, int32_t off, const float *dy,
+                       int accumulate, float *dx, void *stream);
+
 /* BatchNorm over rows = n*h*w rows of c channels (NHWC viewed as [rows][c]). */
 size_t dc_batchnorm_workspace_bytes(int64_t rows, int32_t c);
 /* mean, invstd (c floats each, outputs) = batch statistics with the biased

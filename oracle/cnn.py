@@ -5,7 +5,8 @@ parameters and pushing the gradients in the parameter-server iteration of
 Sec. III-A (pull, forward, backward, push), and of the server's update:
 
 * forward: convolution, FC, BatchNorm (training mode, batch statistics),
-  ReLU, max-pooling, global average pooling, residual add;
+  ReLU, max-pooling, global average pooling, residual add, channel
+  concatenation;
 * loss: mean over the batch of the softmax cross-entropy;
 * backward by the chain rule, giving the gradient of every parameter;
 * the server's SGD update w <- w - lr * g.
@@ -257,6 +258,12 @@ class Net:
                 if kind == "add":
                     assert shapes[op["other"]] == (n, h, w, c)
                 out = (n, h, w, c)
+            elif kind == "concat":
+                cs = c
+                for o in op["others"]:
+                    assert shapes[o][:3] == (n, h, w)
+                    cs += shapes[o][3]
+                out = (n, h, w, cs)
             elif kind == "maxpool":
                 out = (n, conv_out(h, op["r"], op["stride"], op["pad"]),
                        conv_out(w, op["s"], op["stride"], op["pad"]), c)
@@ -310,6 +317,8 @@ class Net:
                 y = a.mean(axis=(1, 2), keepdims=True)
             elif kind == "add":
                 y = a + t[op["other"]]
+            elif kind == "concat":
+                y = np.concatenate([a] + [t[o] for o in op["others"]], axis=3)
             if self.perturb is not None and kind in ("conv", "fc", "bn"):
                 y = self.perturb(i, y)
             t.append(y)
@@ -373,6 +382,12 @@ class Net:
             elif kind == "add":
                 acc(op["in"], dy)
                 acc(op["other"], dy)
+            elif kind == "concat":
+                lo = 0
+                for tid in [op["in"]] + list(op["others"]):
+                    ci = t[tid].shape[3]
+                    acc(tid, dy[..., lo:lo + ci])
+                    lo += ci
         return loss, grads
 
     def loss(self, x, y, params):

@@ -172,7 +172,51 @@ def resnet50():
     return {"name": "resnet50", "ops": b.ops, "hwc": (224, 224, 3), "classes": 1000}
 
 
-NETS = {"tiny": tiny, "alexnet": alexnet, "resnet18": resnet18_small, "vgg16": vgg16, "resnet50": resnet50}
+def googlenet():
+    """GoogLeNet (Inception v1, 5x5 convs in the third branch, no LRN / dropout / auxiliary heads).
+
+    Each Inception module is two planner layers (branches at the same depth
+    form one layer): its four depth-1 convs (1x1, 3x3-reduce, 5x5-reduce and
+    the projection after the 3x3/1 max-pool) and its two depth-2 convs (3x3,
+    5x5) followed by the channel concatenation of the four branches.
+    """
+    b = _Builder()
+    b.new_layer()
+    t = b.conv(0, 64, 7, stride=2, pad=3)
+    t = b.add("relu", t)
+    t = b.add("maxpool", t, r=3, s=3, stride=2, pad=1)
+    b.new_layer()
+    t = b.add("relu", b.conv(t, 64, 1))
+    b.new_layer()
+    t = b.add("relu", b.conv(t, 192, 3, pad=1))
+    t = b.add("maxpool", t, r=3, s=3, stride=2, pad=1)
+    spec = [(64, 96, 128, 16, 32, 32), (128, 128, 192, 32, 96, 64), "M",
+            (192, 96, 208, 16, 48, 64), (160, 112, 224, 24, 64, 64), (128, 128, 256, 24, 64, 64),
+            (112, 144, 288, 32, 64, 64), (256, 160, 320, 32, 128, 128), "M",
+            (256, 160, 320, 32, 128, 128), (384, 192, 384, 48, 128, 128)]
+    for m in spec:
+        if m == "M":
+            t = b.add("maxpool", t, r=3, s=3, stride=2, pad=1)
+            continue
+        c1, r3, c3, r5, c5, pp = m
+        b.new_layer()
+        b1 = b.add("relu", b.conv(t, c1, 1))
+        b3 = b.add("relu", b.conv(t, r3, 1))
+        b5 = b.add("relu", b.conv(t, r5, 1))
+        bp = b.add("maxpool", t, r=3, s=3, stride=1, pad=1)
+        bp = b.add("relu", b.conv(bp, pp, 1))
+        b.new_layer()
+        b3 = b.add("relu", b.conv(b3, c3, 3, pad=1))
+        b5 = b.add("relu", b.conv(b5, c5, 5, pad=2))
+        t = b.add("concat", b1, others=[b3, b5, bp])
+    t = b.add("gap", t)
+    b.new_layer()
+    b.fc(t, 1000)
+    return {"name": "googlenet", "ops": b.ops, "hwc": (224, 224, 3), "classes": 1000}
+
+
+NETS = {"tiny": tiny, "alexnet": alexnet, "resnet18": resnet18_small, "vgg16": vgg16, "resnet50": resnet50,
+        "googlenet": googlenet}
 
 
 def get(name):

@@ -273,6 +273,22 @@ extern "C" int dc_copy_grad(const float *dy, int accumulate, float *dx, int64_t 
     return copy_grad(dy, accumulate, dx, n, static_cast<hipStream_t>(stream));
 }
 
+extern "C" int dc_concat_forward(int64_t rows, int32_t c_in, int32_t c_out, int32_t off, const float *x, float *y,
+                                 void *stream) {
+    clear_error();
+    if (rows < 0 || c_in < 1 || off < 0 || off + c_in > c_out || (rows > 0 && (!x || !y)))
+        return fail(DC_EINVAL, "bad concat arguments");
+    return concat_forward(rows, c_in, c_out, off, x, y, static_cast<hipStream_t>(stream));
+}
+
+extern "C" int dc_concat_backward(int64_t rows, int32_t c_in, int32_t c_out, int32_t off, const float *dy,
+                                  int accumulate, float *dx, void *stream) {
+    clear_error();
+    if (rows < 0 || c_in < 1 || off < 0 || off + c_in > c_out || (rows > 0 && (!dy || !dx)))
+        return fail(DC_EINVAL, "bad concat arguments");
+    return concat_backward(rows, c_in, c_out, off, dy, accumulate, dx, static_cast<hipStream_t>(stream));
+}
+
 extern "C" size_t dc_batchnorm_workspace_bytes(int64_t rows, int32_t c) {
     return rows > 0 && c > 0 ? bn_ws_bytes(rows, c) : 0;
 }

@@ -74,6 +74,9 @@ int relu_backward(const float *dy, const float *y, int accumulate, float *dx, in
                   hipStream_t s);
 int add_forward(const float *a, const float *b, int relu, float *y, int64_t n, hipStream_t s);
 int copy_grad(const float *dy, int accumulate, float *dx, int64_t n, hipStream_t s);
+int concat_forward(int64_t rows, int c_in, int c_out, int off, const float *x, float *y, hipStream_t s);
+int concat_backward(int64_t rows, int c_in, int c_out, int off, const float *dy, int accumulate, float *dx,
+                    hipStream_t s);
 int maxpool_forward(const dc_pool_shape &sh, const float *x, float *y, uint8_t *arg,
                     hipStream_t s);
 int maxpool_backward(const dc_pool_shape &sh, const float *dy, const uint8_t *arg, int accumulate,

@@ -92,6 +92,46 @@ __global__ void copy_grad_kernel(const float *__restrict__ dy, int acc, float *_
         dx[i] = acc ? dx[i] + dy[i] : dy[i];
 }
 
+// Channel slice copies: a thread per float4 (or float) of the slice, rows
+// outermost, so consecutive threads touch consecutive channels of one row.
+template <int V>
+__global__ void concat_kernel(int64_t rows, int c_in, int c_out, int off, const float *__restrict__ x,
+                              float *__restrict__ y) {
+    const int cv = c_in / V;
+    const int64_t total = rows * cv;
+    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total; e += (int64_t)gridDim.x * blockDim.x) {
+        int64_t m = e / cv;
+        int c = (int)(e - m * cv) * V;
+        if (V == 4)
+            *reinterpret_cast<float4 *>(y + m * c_out + off + c) = *reinterpret_cast<const float4 *>(x + m * c_in + c);
+        else
+            y[m * c_out + off + c] = x[m * c_in + c];
+    }
+}
+
+template <int V>
+__global__ void concat_bwd_kernel(int64_t rows, int c_in, int c_out, int off, const float *__restrict__ dy, int acc,
+                                  float *__restrict__ dx) {
+    const int cv = c_in / V;
+    const int64_t total = rows * cv;
+    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total; e += (int64_t)gridDim.x * blockDim.x) {
+        int64_t m = e / cv;
+        int c = (int)(e - m * cv) * V;
+        if (V == 4) {
+            float4 g = *reinterpret_cast<const float4 *>(dy + m * c_out + off + c);
+            float4 *o = reinterpret_cast<float4 *>(dx + m * c_in + c);
+            if (acc) {
+                float4 p = *o;
+                g.x += p.x; g.y += p.y; g.z += p.z; g.w += p.w;
+            }
+            *o = g;
+        } else {
+            float g = dy[m * c_out + off + c];
+            dx[m * c_in + c] = acc ? dx[m * c_in + c] + g : g;
+        }
+    }
+}
+
 // ---------------------------------------------------------------- pooling
 
 __global__ void maxpool_fwd_kernel(dc_pool_shape sh, int P, int Q, const float *__restrict__ x,
@@ -436,6 +476,37 @@ int copy_grad(const float *dy, int accumulate, float *dx, int64_t n, hipStream_t
         return DC_OK;
     hipLaunchKernelGGL(copy_grad_kernel, dim3(ew_blocks(n, 4)), dim3(EW_THREADS), 0, s, dy, accumulate, dx, n,
                        vec4(n, dy, dx));
+    DC_HIP(hipGetLastError());
+    return DC_OK;
+}
+
+static bool concat_vec(int c_in, int c_out, int off, const void *a, const void *b) {
+    return c_in % 4 == 0 && c_out % 4 == 0 && off % 4 == 0 && al16(a) && al16(b);
+}
+
+int concat_forward(int64_t rows, int c_in, int c_out, int off, const float *x, float *y, hipStream_t s) {
+    if (rows <= 0 || c_in <= 0)
+        return DC_OK;
+    if (concat_vec(c_in, c_out, off, x, y))
+        hipLaunchKernelGGL(concat_kernel<4>, dim3(ew_blocks(rows * c_in, 4)), dim3(EW_THREADS), 0, s, rows, c_in,
+                           c_out, off, x, y);
+    else
+        hipLaunchKernelGGL(concat_kernel<1>, dim3(ew_blocks(rows * c_in)), dim3(EW_THREADS), 0, s, rows, c_in, c_out,
+                           off, x, y);
+    DC_HIP(hipGetLastError());
+    return DC_OK;
+}
+
+int concat_backward(int64_t rows, int c_in, int c_out, int off, const float *dy, int accumulate, float *dx,
+                    hipStream_t s) {
+    if (rows <= 0 || c_in <= 0)
+        return DC_OK;
+    if (concat_vec(c_in, c_out, off, dy, dx))
+        hipLaunchKernelGGL(concat_bwd_kernel<4>, dim3(ew_blocks(rows * c_in, 4)), dim3(EW_THREADS), 0, s, rows, c_in,
+                           c_out, off, dy, accumulate, dx);
+    else
+        hipLaunchKernelGGL(concat_bwd_kernel<1>, dim3(ew_blocks(rows * c_in)), dim3(EW_THREADS), 0, s, rows, c_in,
+                           c_out, off, dy, accumulate, dx);
     DC_HIP(hipGetLastError());
     return DC_OK;
 }

@@ -106,12 +106,16 @@ int check_desc(const dc_op_desc *ops, int n_ops, int batch, int in_h, int in_w, 
     int prev_layer = 0;
     for (int i = 0; i < n_ops; ++i) {
         const dc_op_desc &d = ops[i];
-        if (d.kind < DC_OP_CONV || d.kind > DC_OP_ADD)
+        if (d.kind < DC_OP_CONV || d.kind > DC_OP_CONCAT)
             return fail(DC_EINVAL, "op %d: unknown kind %d", i, d.kind);
         if (d.in0 < 0 || d.in0 > i)
             return fail(DC_EINVAL, "op %d: input tensor %d is not an earlier tensor", i, d.in0);
-        if (d.kind == DC_OP_ADD && (d.in1 < 0 || d.in1 > i))
+        if ((d.kind == DC_OP_ADD || d.kind == DC_OP_CONCAT) && (d.in1 < 0 || d.in1 > i))
             return fail(DC_EINVAL, "op %d: second input tensor %d is not an earlier tensor", i, d.in1);
+        if (d.kind == DC_OP_CONCAT) {
+            if (d.in2 < -1 || d.in2 > i || d.in3 < -1 || d.in3 > i || (d.in2 < 0 && d.in3 >= 0))
+                return fail(DC_EINVAL, "op %d: concat inputs in2 / in3 must be earlier tensors or -1", i);
+        }
         if (d.layer != prev_layer && d.layer != prev_layer + 1)
             return fail(DC_EINVAL, "op %d: layers must be contiguous and non-decreasing", i);
         bool weighted = d.kind == DC_OP_CONV || d.kind == DC_OP_FC;
@@ -140,6 +144,18 @@ static int build_model(dc_model *m, const dc_op_desc *ops, int n_ops) {
         OpInfo &o = m->ops[i];
         o.d = ops[i];
         o.out = i + 1;
+        o.in[0] = o.d.in0;
+        o.n_in = 1;
+        if (o.d.kind == DC_OP_ADD || o.d.kind == DC_OP_CONCAT) {
+            o.in[1] = o.d.in1;
+            o.n_in = 2;
+        }
+        if (o.d.kind == DC_OP_CONCAT) {
+            if (o.d.in2 >= 0)
+                o.in[o.n_in++] = o.d.in2;
+            if (o.d.in3 >= 0)
+                o.in[o.n_in++] = o.d.in3;
+        }
         const TensorInfo in = m->tensors[o.d.in0];
         TensorInfo out = in;
         int l = o.d.layer;
@@ -200,6 +216,18 @@ static int build_model(dc_model *m, const dc_op_desc *ops, int n_ops) {
                 return fail(DC_EINVAL, "op %d: ADD inputs differ in shape", i);
             break;
         }
+        case DC_OP_CONCAT: {
+            int c = 0;
+            for (int k = 0; k < o.n_in; ++k) {
+                const TensorInfo &b = m->tensors[o.in[k]];
+                if (b.n != in.n || b.h != in.h || b.w != in.w)
+                    return fail(DC_EINVAL, "op %d: CONCAT inputs differ in n, h or w", i);
+                o.ch_off[k] = c;
+                c += b.c;
+            }
+            out.c = c;
+            break;
+        }
         }
         m->layer_cnt[l] += poff - start;
         m->tensors[o.out] = out;
@@ -216,15 +244,12 @@ static int build_model(dc_model *m, const dc_op_desc *ops, int n_ops) {
     std::vector<char> written(n_ops + 1, 0);
     for (int i = n_ops - 1; i >= 0; --i) {
         OpInfo &o = m->ops[i];
-        int ins[2] = {o.d.in0, o.d.kind == DC_OP_ADD ? o.d.in1 : -1};
-        for (int k = 0; k < 2; ++k) {
-            int t = ins[k];
+        for (int k = 0; k < o.n_in; ++k) {
+            int t = o.in[k];
             if (t <= 0)
                 continue; // the input batch needs no gradient
-            bool &g = k == 0 ? o.grad_in0 : o.grad_in1;
-            int &acc = k == 0 ? o.acc_in0 : o.acc_in1;
-            g = true;
-            acc = written[t] ? 1 : 0;
+            o.grad_in[k] = true;
+            o.acc_in[k] = written[t] ? 1 : 0;
             written[t] = 1;
         }
     }
@@ -302,6 +327,15 @@ int run_forward_layer(dc_model *m, int l, const float *x, const int32_t *y, hipS
         case DC_OP_ADD:
             DC_TRY(add_forward(in, m->act(o.d.in1), 0, out, ti.size(), s));
             break;
+        case DC_OP_CONCAT: {
+            const TensorInfo &to = m->tensors[o.out];
+            for (int k = 0; k < o.n_in; ++k) {
+                const TensorInfo &tk = m->tensors[o.in[k]];
+                const float *src = o.in[k] == 0 ? x : m->act(o.in[k]);
+                DC_TRY(concat_forward((int64_t)tk.n * tk.h * tk.w, tk.c, to.c, o.ch_off[k], src, out, s));
+            }
+            break;
+        }
         }
     }
     if (l == m->L) {
@@ -318,7 +352,7 @@ int run_backward_layer(dc_model *m, int l, const float *x, hipStream_t s) {
         OpInfo &o = m->ops[i];
         const float *in = o.d.in0 == 0 ? x : m->act(o.d.in0);
         const float *dy = m->grad(o.out);
-        float *dx = o.grad_in0 ? m->grad(o.d.in0) : nullptr;
+        float *dx = o.grad_in[0] ? m->grad(o.d.in0) : nullptr;
         const TensorInfo &ti = m->tensors[o.d.in0];
         const TensorInfo &to = m->tensors[o.out];
         switch (o.d.kind) {
@@ -328,26 +362,35 @@ int run_backward_layer(dc_model *m, int l, const float *x, hipStream_t s) {
             if (o.b_off != NONE)
                 DC_TRY(colsum((int64_t)to.n * to.h * to.w, to.c, dy, G + o.b_off, m->scratch(), s));
             if (dx)
-                DC_TRY(conv_dgrad(o.geom, o.dgrad, dy, P + o.w_off, o.acc_in0, dx, m->scratch(), s));
+                DC_TRY(conv_dgrad(o.geom, o.dgrad, dy, P + o.w_off, o.acc_in[0], dx, m->scratch(), s));
             break;
         case DC_OP_BN: {
             const float *mean = reinterpret_cast<const float *>(m->ws + o.aux);
-            DC_TRY(bn_backward((int64_t)ti.n * ti.h * ti.w, ti.c, dy, in, P + o.w_off, mean, mean + ti.c, o.acc_in0,
+            DC_TRY(bn_backward((int64_t)ti.n * ti.h * ti.w, ti.c, dy, in, P + o.w_off, mean, mean + ti.c, o.acc_in[0],
                                dx, G + o.w_off, G + o.b_off, m->scratch(), s));
             break;
         }
         case DC_OP_RELU:
-            DC_TRY(relu_backward(dy, m->act(o.out), o.acc_in0, dx, ti.size(), s));
+            DC_TRY(relu_backward(dy, m->act(o.out), o.acc_in[0], dx, ti.size(), s));
             break;
         case DC_OP_MAXPOOL:
-            DC_TRY(maxpool_backward(o.pool, dy, reinterpret_cast<const uint8_t *>(m->ws + o.aux), o.acc_in0, dx, s));
+            DC_TRY(maxpool_backward(o.pool, dy, reinterpret_cast<const uint8_t *>(m->ws + o.aux), o.acc_in[0], dx, s));
             break;
         case DC_OP_GAP:
-            DC_TRY(gap_backward(ti.n, ti.h * ti.w, ti.c, dy, o.acc_in0, dx, s));
+            DC_TRY(gap_backward(ti.n, ti.h * ti.w, ti.c, dy, o.acc_in[0], dx, s));
             break;
         case DC_OP_ADD:
-            DC_TRY(copy_grad(dy, o.acc_in0, dx, ti.size(), s));
-            DC_TRY(copy_grad(dy, o.acc_in1, m->grad(o.d.in1), ti.size(), s));
+            DC_TRY(copy_grad(dy, o.acc_in[0], dx, ti.size(), s));
+            DC_TRY(copy_grad(dy, o.acc_in[1], m->grad(o.d.in1), ti.size(), s));
+            break;
+        case DC_OP_CONCAT:
+            for (int k = 0; k < o.n_in; ++k) {
+                if (!o.grad_in[k])
+                    continue;
+                const TensorInfo &tk = m->tensors[o.in[k]];
+                DC_TRY(concat_backward((int64_t)tk.n * tk.h * tk.w, tk.c, to.c, o.ch_off[k], dy, o.acc_in[k],
+                                       m->grad(o.in[k]), s));
+            }
             break;
         }
     }

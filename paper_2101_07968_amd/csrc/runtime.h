@@ -28,8 +28,11 @@ struct OpInfo {
     GemmPlan fwd{}, dgrad{}, wgrad{};
     dc_pool_shape pool{};
     size_t aux = NONE;               // BN: mean then invstd; MAXPOOL: argmax bytes
-    bool grad_in0 = false, grad_in1 = false;
-    int acc_in0 = 0, acc_in1 = 0;    // backward adds into the input gradient
+    int n_in = 1;                    // inputs: in0, in1, in2, in3 (ADD 2, CONCAT 2-4)
+    int in[4] = {-1, -1, -1, -1};
+    int ch_off[4] = {0, 0, 0, 0};    // CONCAT: channel offset of each input in the output
+    bool grad_in[4] = {false, false, false, false};
+    int acc_in[4] = {0, 0, 0, 0};    // backward adds into the input gradient
 };
 
 // Small persistent pool for the server-side SGD update.

@@ -1,7 +1,7 @@
 """The five synthetic workloads as dc_op_desc lists for dc_model_create.
 
-Each builder returns ``(ops, hwc, classes)``: ``ops`` is a list of 10-tuples
-``(kind, layer, in0, in1, out_ch, r, s, stride, pad, bias)`` in forward order
+Each builder returns ``(ops, hwc, classes)``: ``ops`` is a list of 12-tuples
+``(kind, layer, in0, in1, out_ch, r, s, stride, pad, bias, in2, in3)`` in forward order
 (tensor 0 = input batch, tensor i+1 = output of op i).  A planner layer is one
 conv / FC and the parameter-less ops after it, BatchNorm joins its conv, and
 a residual projection shares the layer of its block's first conv (the layer
@@ -13,10 +13,11 @@ Workloads (inputs NHWC; batch and link are chosen by the caller):
   resnet18  32x32 ResNet-18 with BN and 1x1/2 projections, FC 512->10                         (L=18)
   vgg16     13 conv3x3 + 3 FC, 224x224                                                        (L=16)
   resnet50  bottleneck [3,4,6,3], stride on the 3x3 conv, FC 2048->1000                        (L=50)
+  googlenet Inception v1 (5x5 third branch, no LRN / dropout / auxiliary heads), FC 1024->1000  (L=22)
 """
 from __future__ import annotations
 
-from ._lib import DC_OP_ADD, DC_OP_BN, DC_OP_CONV, DC_OP_FC, DC_OP_GAP, DC_OP_MAXPOOL, DC_OP_RELU
+from ._lib import DC_OP_ADD, DC_OP_BN, DC_OP_CONCAT, DC_OP_CONV, DC_OP_FC, DC_OP_GAP, DC_OP_MAXPOOL, DC_OP_RELU
 
 
 class NetBuilder:
@@ -24,8 +25,8 @@ class NetBuilder:
         self.ops = []
         self.layer = 0
 
-    def _emit(self, kind, src, other=-1, out_ch=0, r=0, s=0, stride=0, pad=0, bias=0):
-        self.ops.append((kind, self.layer, src, other, out_ch, r, s, stride, pad, bias))
+    def _emit(self, kind, src, other=-1, out_ch=0, r=0, s=0, stride=0, pad=0, bias=0, in2=-1, in3=-1):
+        self.ops.append((kind, self.layer, src, other, out_ch, r, s, stride, pad, bias, in2, in3))
         return len(self.ops)
 
     def conv(self, src, out_ch, k, stride=1, pad=0, bias=True, new_layer=True):
@@ -51,6 +52,9 @@ class NetBuilder:
 
     def add(self, a, b):
         return self._emit(DC_OP_ADD, a, other=b)
+
+    def concat(self, a, b, c=-1, d=-1):
+        return self._emit(DC_OP_CONCAT, a, other=b, in2=c, in3=d)
 
 
 def tiny():
@@ -133,7 +137,34 @@ def resnet50():
     return n.ops, (224, 224, 3), 1000
 
 
-BUILDERS = {"tiny": tiny, "alexnet": alexnet, "resnet18": resnet18, "vgg16": vgg16, "resnet50": resnet50}
+def _inception(n, x, c1, r3, c3, r5, c5, pool_proj):
+    """Four branches; the depth-1 convs form one planner layer, the depth-2 convs and the concat the next."""
+    b1 = n.relu(n.conv(x, c1, 1))
+    b3 = n.relu(n.conv(x, r3, 1, new_layer=False))
+    b5 = n.relu(n.conv(x, r5, 1, new_layer=False))
+    bp = n.maxpool(x, 3, 1, pad=1)
+    bp = n.relu(n.conv(bp, pool_proj, 1, new_layer=False))
+    b3 = n.relu(n.conv(b3, c3, 3, pad=1))
+    b5 = n.relu(n.conv(b5, c5, 5, pad=2, new_layer=False))
+    return n.concat(b1, b3, b5, bp)
+
+
+def googlenet():
+    n = NetBuilder()
+    t = n.maxpool(n.relu(n.conv(0, 64, 7, stride=2, pad=3)), 3, 2, pad=1)
+    t = n.relu(n.conv(t, 64, 1))
+    t = n.maxpool(n.relu(n.conv(t, 192, 3, pad=1)), 3, 2, pad=1)
+    for m in ((64, 96, 128, 16, 32, 32), (128, 128, 192, 32, 96, 64), None,
+              (192, 96, 208, 16, 48, 64), (160, 112, 224, 24, 64, 64), (128, 128, 256, 24, 64, 64),
+              (112, 144, 288, 32, 64, 64), (256, 160, 320, 32, 128, 128), None,
+              (256, 160, 320, 32, 128, 128), (384, 192, 384, 48, 128, 128)):
+        t = n.maxpool(t, 3, 2, pad=1) if m is None else _inception(n, t, *m)
+    t = n.gap(t)
+    n.fc(t, 1000)
+    return n.ops, (224, 224, 3), 1000
+
+
+BUILDERS = {"tiny": tiny, "alexnet": alexnet, "resnet18": resnet18, "vgg16": vgg16, "resnet50": resnet50, "googlenet": googlenet}
 
 # The workloads' batch size, emulated link rate (bytes/s; 1 Gb/s = 1.25e8 B/s)
 # and input seed.
@@ -143,6 +174,7 @@ WORKLOADS = {
     "resnet18": {"batch": 128, "link": 1e9 / 8, "seed": 2},
     "vgg16": {"batch": 32, "link": 10e9 / 8, "seed": 3},
     "resnet50": {"batch": 64, "link": 10e9 / 8, "seed": 4},
+    "googlenet": {"batch": 32, "link": 10e9 / 8, "seed": 5},
 }
 
 
@@ -159,8 +191,11 @@ def param_specs(ops, hwc):
     """
     shapes = [(hwc[0], hwc[1], hwc[2])]
     specs = []
-    for (kind, _layer, src, _other, out_ch, r, s, stride, pad, bias) in ops:
+    for (kind, _layer, src, other, out_ch, r, s, stride, pad, bias, in2, in3) in ops:
         h, w, c = shapes[src]
+        if kind == DC_OP_CONCAT:
+            shapes.append((h, w, sum(shapes[t][2] for t in (src, other, in2, in3) if t >= 0)))
+            continue
         if kind == DC_OP_CONV:
             specs.append(("he", out_ch * r * s * c, r * s * c))
             if bias:
@@ -188,8 +223,11 @@ def conv_geoms(ops, hwc, batch):
     """(op index, dc_conv_shape fields, reads_input_batch) of every conv / FC op; FC as a 1x1 conv."""
     shapes = [(hwc[0], hwc[1], hwc[2])]
     out = []
-    for i, (kind, _layer, src, _other, out_ch, r, s, stride, pad, bias) in enumerate(ops):
+    for i, (kind, _layer, src, other, out_ch, r, s, stride, pad, bias, in2, in3) in enumerate(ops):
         h, w, c = shapes[src]
+        if kind == DC_OP_CONCAT:
+            shapes.append((h, w, sum(shapes[t][2] for t in (src, other, in2, in3) if t >= 0)))
+            continue
         if kind == DC_OP_CONV:
             out.append((i, (batch, h, w, c, out_ch, r, s, stride, pad), src == 0))
             shapes.append(((h + 2 * pad - r) // stride + 1, (w + 2 * pad - s) // stride + 1, out_ch))

@@ -104,7 +104,8 @@ def test_conv_small(shape, variant):
 def _full_size_geoms():
     """Every distinct conv / FC geometry of the five workloads at their own batch."""
     seen, out = set(), []
-    for name, batch in (("tiny", 4), ("alexnet", 32), ("resnet18", 128), ("vgg16", 32), ("resnet50", 64)):
+    for name, batch in (("tiny", 4), ("alexnet", 32), ("resnet18", 128), ("vgg16", 32), ("resnet50", 64),
+                        ("googlenet", 32)):
         net = OC.Net(ON.get(name), batch)
         for i, op in enumerate(net.ops):
             if op["op"] not in ("conv", "fc"):
@@ -281,3 +282,27 @@ def test_softmax_xent(n, classes):
     l_ref, dz_ref = OC.softmax_xent(z.astype(np.float64), y)
     assert abs(host(loss)[0] - l_ref) <= 1e-6 * abs(l_ref)
     assert rel_err(host(dz), dz_ref) <= 1e-6
+
+
+@pytest.mark.parametrize("cfg", [(10, (4, 8, 12, 4)), (7, (3, 5, 2)), (32 * 28 * 28, (64, 128, 32, 32))])
+def test_concat(cfg):
+    rows, parts = cfg
+    cout = sum(parts)
+    xs = [synth.random_tensor(30 + i, (rows, c)) for i, c in enumerate(parts)]
+    xds = [dev(x) for x in xs]
+    y = zeros((rows, cout))
+    off = 0
+    for c, xd in zip(parts, xds):
+        D.call("dc_concat_forward", rows, c, cout, off, xd.data_ptr(), y.data_ptr(), stream())
+        off += c
+    np.testing.assert_array_equal(host(y), np.concatenate(xs, axis=1))
+    dy = synth.random_tensor(40, (rows, cout))
+    dyd = dev(dy)
+    off = 0
+    for i, c in enumerate(parts):
+        acc0 = synth.random_tensor(50 + i, (rows, c))
+        dx = dev(acc0)
+        D.call("dc_concat_backward", rows, c, cout, off, dyd.data_ptr(), 1, dx.data_ptr(), stream())
+        np.testing.assert_array_equal(host(dx), (acc0 + dy[:, off:off + c]).astype(np.float32))
+        off += c
+    assert D.lib().dc_concat_forward(rows, parts[0], cout, cout, None, None, None) == D.DC_EINVAL

@@ -52,7 +52,7 @@ def plans_for(L, seed=0):
     }
 
 
-PARITY = [("tiny", 4), ("alexnet", 2), ("resnet18", 8), ("resnet50", 2), ("vgg16", 1)]
+PARITY = [("tiny", 4), ("alexnet", 2), ("resnet18", 8), ("resnet50", 2), ("vgg16", 1), ("googlenet", 2)]
 
 
 def fp32_spread(spec, onet, x, y, params, g_ref):
@@ -127,7 +127,7 @@ def test_step_matches_oracle(name, batch):
           + ", ".join(f"({i},{p},{e:.1e},{s:.1e})" for i, p, e, s in rows[:4]), flush=True)
 
 
-@pytest.mark.parametrize("name,batch", [("tiny", 4), ("resnet18", 16), ("resnet50", 2)])
+@pytest.mark.parametrize("name,batch", [("tiny", 4), ("resnet18", 16), ("resnet50", 2), ("googlenet", 2)])
 def test_results_do_not_depend_on_segmentation(name, batch):
     model, onet, xd, yd, x, y, params = setup_model(name, batch, seed=3)
     outs = []
@@ -142,7 +142,8 @@ def test_results_do_not_depend_on_segmentation(name, batch):
         np.testing.assert_array_equal(g, outs[0][3], err_msg=key)
 
 
-FULL = [("tiny", 4, 0), ("alexnet", 32, 1), ("resnet18", 128, 2), ("vgg16", 32, 3), ("resnet50", 64, 4)]
+FULL = [("tiny", 4, 0), ("alexnet", 32, 1), ("resnet18", 128, 2), ("vgg16", 32, 3), ("resnet50", 64, 4),
+        ("googlenet", 32, 5)]
 
 
 @pytest.mark.parametrize("name,batch,seed", FULL, ids=[f"{n}-b{b}" for n, b, _ in FULL])

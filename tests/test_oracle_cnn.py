@@ -141,6 +141,48 @@ def _mini_resnet():
     return {"name": "mini", "ops": ops, "hwc": (10, 10, 3), "classes": 5}
 
 
+def _mini_inception():
+    """Two Inception-style modules (four branches, concat) at small size."""
+    ops = []
+
+    def add(kind, inp, layer, **kw):
+        d = {"op": kind, "in": inp, "layer": layer}
+        d.update(kw)
+        ops.append(d)
+        return len(ops)
+
+    t = add("relu", add("conv", 0, 1, k=6, r=3, s=3, stride=1, pad=1, bias=True), 1)
+    layer = 1
+    for c1, r3, c3, r5, c5, pp in ((3, 2, 4, 2, 3, 2), (2, 3, 3, 1, 2, 3)):
+        layer += 1
+        b1 = add("relu", add("conv", t, layer, k=c1, r=1, s=1, stride=1, pad=0, bias=True), layer)
+        b3 = add("relu", add("conv", t, layer, k=r3, r=1, s=1, stride=1, pad=0, bias=True), layer)
+        b5 = add("relu", add("conv", t, layer, k=r5, r=1, s=1, stride=1, pad=0, bias=True), layer)
+        bp = add("maxpool", t, layer, r=3, s=3, stride=1, pad=1)
+        bp = add("relu", add("conv", bp, layer, k=pp, r=1, s=1, stride=1, pad=0, bias=True), layer)
+        layer += 1
+        b3 = add("relu", add("conv", b3, layer, k=c3, r=3, s=3, stride=1, pad=1, bias=True), layer)
+        b5 = add("relu", add("conv", b5, layer, k=c5, r=5, s=5, stride=1, pad=2, bias=True), layer)
+        t = add("concat", b1, layer, others=[b3, b5, bp])
+    t = add("gap", t, layer)
+    add("fc", t, layer + 1, out=4, bias=True)
+    return {"name": "mini_inception", "ops": ops, "hwc": (7, 7, 3), "classes": 4}
+
+
+def test_finite_differences_inception():
+    _fd_check(_mini_inception(), 2, 4, 80, 1e-6)
+
+
+def test_inception_against_torch():
+    spec = _mini_inception()
+    net = cnn.Net(spec, 3)
+    x, y, p = synth.cnn_inputs(5, 3, spec["hwc"], spec["classes"], net.param_specs)
+    loss, g = net.loss_and_grads(x, y, p)
+    lt, gt = _torch_loss(spec, net, x, y, p)
+    assert abs(loss - lt) <= 1e-12 * max(1.0, abs(lt))
+    np.testing.assert_allclose(g, gt, rtol=1e-9, atol=1e-12 * np.abs(gt).max())
+
+
 def _fd_check(spec, batch, seed, n_probe, rel):
     net = cnn.Net(spec, batch)
     x, y, p = synth.cnn_inputs(seed, batch, spec["hwc"], spec["classes"], net.param_specs)
@@ -192,12 +234,12 @@ def test_sgd_closed_form():
 
 
 @pytest.mark.parametrize("name,count", [("tiny", 67642), ("alexnet", 61100840), ("resnet18", 11173962),
-                                        ("vgg16", 138357544), ("resnet50", 25557032)])
+                                        ("vgg16", 138357544), ("resnet50", 25557032), ("googlenet", 6998552)])
 def test_parameter_counts(name, count):
     net = cnn.Net(nets.get(name), 1)
     assert net.n_params == count
     assert sum(c for _, c in net.layer_ranges.values()) == count
-    assert {"tiny": 4, "alexnet": 8, "resnet18": 18, "vgg16": 16, "resnet50": 50}[name] == net.L
+    assert {"tiny": 4, "alexnet": 8, "resnet18": 18, "vgg16": 16, "resnet50": 50, "googlenet": 22}[name] == net.L
 
 
 def _torch_loss(spec, net, x, y, p):

@@ -43,6 +43,8 @@ def loss_and_grads(spec, net, x, y, p, dtype=torch.float64):
             o = F.adaptive_avg_pool2d(a, 1)
         elif k == "add":
             o = a + t[op["other"]]
+        elif k == "concat":
+            o = torch.cat([a] + [t[j] for j in op["others"]], dim=1)
         t.append(o)
     loss = F.cross_entropy(t[-1].reshape(net.batch, -1), torch.from_numpy(np.asarray(y, dtype=np.int64)))
     loss.backward()
