@@ -43,11 +43,15 @@ struct GemmPlan {
     int M, Ng, Kg;        // GEMM sizes (DGRAD: maxima over the stride phases)
     int phases;           // DGRAD: stride^2, otherwise 1
     int mt, nt;           // workgroup tile
+    int kt;               // K depth of one LDS stage (16 or 32)
     int tiles_m, tiles_n; // tiles per phase
     int splits;           // split-K factor (1 = no split)
-    int kt_per_split;     // K tiles (of the kernel's K step) per split
+    int kt_per_split;     // K stages (of depth kt) per split
     bool av, bv;          // float4 operand loads possible
-    size_t ws_bytes;      // split-K partial sums
+    int cpad;             // FWD / WGRAD with C % 4 != 0: padded channel count, else 0
+    size_t pad_x_off;     // workspace offsets of the padded x and of the padded w (FWD) or dw (WGRAD)
+    size_t pad_w_off;
+    size_t ws_bytes;      // split-K partial sums, then the padded copies
 };
 
 bool conv_geom_from_shape(const dc_conv_shape &sh, ConvGeom *g);

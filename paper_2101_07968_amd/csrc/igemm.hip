@@ -27,13 +27,14 @@
 #include <algorithm>
 #include <climits>
 #include <cmath>
+#include <cstdint>
+#include <type_traits>
 
 namespace dc {
 namespace {
 
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
-constexpr int KT = 16;   // K depth of one LDS stage
 constexpr int NTHR = 256;
 constexpr int PADK = 4;  // padding of k-contiguous LDS rows (floats)
 constexpr int PADR = 4;  // padding of row-contiguous LDS rows (floats)
@@ -66,7 +67,7 @@ struct Args {
     int N, H, W, C, K, R, S, st, pad, P, Q;
     int M, Ng, Kg;          // FWD / WGRAD sizes; DGRAD: maxima over phases
     int tiles_m, tiles_n, tiles;
-    int splits, kt_per_split;
+    int splits, kt_per_split, phases;
     const float *A;         // FWD: x   DGRAD: dy   WGRAD: dy
     const float *B;         // FWD: w   DGRAD: w    WGRAD: x
     float *out;             // FWD: y   DGRAD: dx   WGRAD: dw
@@ -132,7 +133,7 @@ __device__ __forceinline__ float epilogue(const Args &a, int pass, float v, int 
     return v;
 }
 
-template <int PASS, int MT, int NT, bool AV, bool BV>
+template <int PASS, int MT, int NT, int KT, bool AV, bool BV>
 __global__ __launch_bounds__(NTHR) void igemm_kernel(Args a) {
     constexpr bool A_KC = (PASS != PASS_WGRAD); // A tile stored [row][k]
     constexpr bool B_KC = (PASS == PASS_FWD);   // B tile stored [col][k]
@@ -148,18 +149,23 @@ __global__ __launch_bounds__(NTHR) void igemm_kernel(Args a) {
     __shared__ __attribute__((aligned(16))) float lds[2 * (A_SZ + B_SZ)];
 
     const int t = threadIdx.x;
-    // XCD-aware tile order: consecutive ids of one XCD get consecutive tiles.
-    int bid = blockIdx.x;
-    {
-        int per = gridDim.x >> 3;
-        bid = (bid & 7) * per + (bid >> 3);
-    }
-    if (bid >= a.tiles)
+    // XCD-aware order: workgroups are dealt to the 8 XCDs round-robin by
+    // linear id.  Each stride phase owns a range of ids padded to a multiple
+    // of 8 (phase-major dispatch); inside it, id -> (id % 8) * (range / 8) +
+    // id / 8 gives each XCD one contiguous run of (split, tile): neighbouring
+    // tiles of the same split, which share operand rows in that XCD's L2, and
+    // the splits of a GEMM with few tiles spread over every XCD.
+    const int per_phase = a.tiles * a.splits;
+    const int range = (per_phase + 7) & ~7;
+    const int z = blockIdx.x / range;
+    int bid = blockIdx.x - z * range;
+    bid = (bid & 7) * (range >> 3) + (bid >> 3);
+    if (bid >= per_phase)
         return;
-    const int tm = bid / a.tiles_n;
-    const int tn = bid - tm * a.tiles_n;
-    const int z = blockIdx.z;
-    const int split = blockIdx.y;
+    const int split = bid / a.tiles;
+    const int tile = bid - split * a.tiles;
+    const int tm = tile / a.tiles_n;
+    const int tn = tile - tm * a.tiles_n;
 
     Phase ph{};
     int M = a.M, Kg = a.Kg;
@@ -544,10 +550,17 @@ __global__ __launch_bounds__(NTHR) void igemm_kernel(Args a) {
     }
 }
 
-// Adds the split-K partial sums of each output in split order, then applies
-// the pass's epilogue.
-template <int PASS>
-__global__ __launch_bounds__(256) void splitk_reduce_kernel(Args a) {
+// Adds the split-K partial sums of each output, then applies the pass's
+// epilogue.  A workgroup owns G = 256 / R consecutive output groups (four
+// elements when VEC, else one); the R lanes of a group each sum the slots
+// s = lane, lane + R, ... into four independent accumulators (many loads in
+// flight), and lane 0 then adds the R lane sums in ascending lane order.  R
+// depends on the plan alone, so every result is deterministic.
+template <int PASS, bool VEC>
+__global__ __launch_bounds__(256) void splitk_reduce_kernel(Args a, int lg_r) {
+    using V = typename std::conditional<VEC, float4, float>::type;
+    constexpr int W = VEC ? 4 : 1;
+    __shared__ V part[256];
     const int z = blockIdx.y;
     Phase ph{};
     int M = a.M;
@@ -555,46 +568,137 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(Args a) {
         ph = make_phase(a, z);
         M = ph.M;
     }
-    const size_t total = (size_t)M * a.Ng;
-    for (size_t e = (size_t)blockIdx.x * blockDim.x + threadIdx.x; e < total;
-         e += (size_t)gridDim.x * blockDim.x) {
-        int m = (int)(e / a.Ng);
-        int n = (int)(e - (size_t)m * a.Ng);
-        float v = 0.f;
-        for (int s = 0; s < a.splits; ++s)
-            v += a.partial[((size_t)(z * a.splits + s) * a.M + m) * a.Ng + n];
-        float *dst = a.out + out_row(a, PASS, ph, z, m) + n;
-        *dst = epilogue(a, PASS, v, n, dst);
+    const int R = 1 << lg_r, G = 256 >> lg_r;
+    const int col = threadIdx.x & (G - 1), lane = threadIdx.x >> (8 - lg_r);
+    const size_t groups = (size_t)M * a.Ng / W;
+    const size_t slab = (size_t)a.M * a.Ng; // elements per split slot
+    const float *base = a.partial + (size_t)z * a.splits * slab;
+    auto ld = [&](const float *p) -> V {
+        if constexpr (VEC)
+            return *reinterpret_cast<const float4 *>(p);
+        else
+            return *p;
+    };
+    for (size_t g0 = (size_t)blockIdx.x * G; g0 < groups; g0 += (size_t)gridDim.x * G) {
+        const size_t g = g0 + col;
+        V s0{}, s1{}, s2{}, s3{};
+        if (g < groups) {
+            const float *p = base + g * W;
+            int s = lane;
+            for (; s + 3 * R < a.splits; s += 4 * R) {
+                s0 += ld(p + (size_t)s * slab);
+                s1 += ld(p + (size_t)(s + R) * slab);
+                s2 += ld(p + (size_t)(s + 2 * R) * slab);
+                s3 += ld(p + (size_t)(s + 3 * R) * slab);
+            }
+            for (; s < a.splits; s += R)
+                s0 += ld(p + (size_t)s * slab);
+        }
+        part[threadIdx.x] = (s0 + s1) + (s2 + s3);
+        __syncthreads();
+        if (lane == 0 && g < groups) {
+            V v = part[col];
+            for (int r = 1; r < R; ++r)
+                v += part[r * G + col];
+            const size_t e = g * W;
+            const int m = (int)(e / a.Ng);
+            const int n = (int)(e - (size_t)m * a.Ng);
+            float *dst = a.out + out_row(a, PASS, ph, z, m) + n;
+            if constexpr (VEC) {
+                dst[0] = epilogue(a, PASS, v.x, n, dst);
+                dst[1] = epilogue(a, PASS, v.y, n + 1, dst + 1);
+                dst[2] = epilogue(a, PASS, v.z, n + 2, dst + 2);
+                dst[3] = epilogue(a, PASS, v.w, n + 3, dst + 3);
+            } else {
+                dst[0] = epilogue(a, PASS, v, n, dst);
+            }
+        }
+        __syncthreads();
     }
 }
 
-template <int PASS, int MT, int NT, bool AV, bool BV>
-void launch_t(const Args &a, int grid_x, int splits, int phases, hipStream_t s) {
-    hipLaunchKernelGGL((igemm_kernel<PASS, MT, NT, AV, BV>), dim3(grid_x, splits, phases), dim3(NTHR), 0, s, a);
+// Channel padding for C % 4 != 0: with C rounded up to a multiple of 4 every
+// operand of the forward and wgrad GEMMs is read as aligned float4 (one
+// 16-byte load per filter tap instead of four gathered scalars).  Padded
+// channels are zero, so they add nothing to any sum.
+__global__ __launch_bounds__(256) void pad_channels_kernel(const float *in, float4 *out, int64_t rows, int c,
+                                                           int cp4) {
+    const int64_t total = rows * cp4;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t row = i / cp4;
+        const int c0 = 4 * (int)(i - row * cp4);
+        const float *src = in + row * c;
+        float v[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+            v[e] = c0 + e < c ? src[c0 + e] : 0.f;
+        out[i] = make_float4(v[0], v[1], v[2], v[3]);
+    }
 }
 
-template <int PASS, int MT, int NT>
-void launch_v(const Args &a, bool av, bool bv, int grid_x, int splits, int phases, hipStream_t s) {
+__global__ __launch_bounds__(256) void unpad_channels_kernel(const float *in, float *out, int64_t rows, int c,
+                                                             int cp) {
+    const int64_t total = rows * c;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t row = i / c;
+        out[i] = in[row * cp + (i - row * c)];
+    }
+}
+
+int pad_channels(const float *in, float *out, int64_t rows, int c, int cp, hipStream_t s) {
+    const int64_t total = rows * (cp / 4);
+    const int blocks = (int)std::min<int64_t>((total + 255) / 256, 8192);
+    hipLaunchKernelGGL(pad_channels_kernel, dim3(blocks), dim3(256), 0, s, in, reinterpret_cast<float4 *>(out),
+                       rows, c, cp / 4);
+    DC_HIP(hipGetLastError());
+    return DC_OK;
+}
+
+int unpad_channels(const float *in, float *out, int64_t rows, int c, int cp, hipStream_t s) {
+    const int64_t total = rows * c;
+    const int blocks = (int)std::min<int64_t>((total + 255) / 256, 8192);
+    hipLaunchKernelGGL(unpad_channels_kernel, dim3(blocks), dim3(256), 0, s, in, out, rows, c, cp);
+    DC_HIP(hipGetLastError());
+    return DC_OK;
+}
+
+template <int PASS, int MT, int NT, int KT, bool AV, bool BV>
+void launch_t(const Args &a, int grid_x, hipStream_t s) {
+    hipLaunchKernelGGL((igemm_kernel<PASS, MT, NT, KT, AV, BV>), dim3(grid_x), dim3(NTHR), 0, s, a);
+}
+
+template <int PASS, int MT, int NT, int KT>
+void launch_v(const Args &a, bool av, bool bv, int grid_x, hipStream_t s) {
     if (av && bv)
-        launch_t<PASS, MT, NT, true, true>(a, grid_x, splits, phases, s);
+        launch_t<PASS, MT, NT, KT, true, true>(a, grid_x, s);
     else if (av)
-        launch_t<PASS, MT, NT, true, false>(a, grid_x, splits, phases, s);
+        launch_t<PASS, MT, NT, KT, true, false>(a, grid_x, s);
     else if (bv)
-        launch_t<PASS, MT, NT, false, true>(a, grid_x, splits, phases, s);
+        launch_t<PASS, MT, NT, KT, false, true>(a, grid_x, s);
     else
-        launch_t<PASS, MT, NT, false, false>(a, grid_x, splits, phases, s);
+        launch_t<PASS, MT, NT, KT, false, false>(a, grid_x, s);
+}
+
+template <int PASS, int KT>
+void launch_k(const Args &a, const GemmPlan &pl, int grid_x, hipStream_t s) {
+    if (pl.mt == 128 && pl.nt == 128)
+        launch_v<PASS, 128, 128, KT>(a, pl.av, pl.bv, grid_x, s);
+    else if (pl.mt == 128 && pl.nt == 64)
+        launch_v<PASS, 128, 64, KT>(a, pl.av, pl.bv, grid_x, s);
+    else if (pl.mt == 64 && pl.nt == 128)
+        launch_v<PASS, 64, 128, KT>(a, pl.av, pl.bv, grid_x, s);
+    else
+        launch_v<PASS, 64, 64, KT>(a, pl.av, pl.bv, grid_x, s);
 }
 
 template <int PASS>
 void launch_p(const Args &a, const GemmPlan &pl, int grid_x, hipStream_t s) {
-    if (pl.mt == 128 && pl.nt == 128)
-        launch_v<PASS, 128, 128>(a, pl.av, pl.bv, grid_x, pl.splits, pl.phases, s);
-    else if (pl.mt == 128 && pl.nt == 64)
-        launch_v<PASS, 128, 64>(a, pl.av, pl.bv, grid_x, pl.splits, pl.phases, s);
-    else if (pl.mt == 64 && pl.nt == 128)
-        launch_v<PASS, 64, 128>(a, pl.av, pl.bv, grid_x, pl.splits, pl.phases, s);
+    if (pl.kt == 32)
+        launch_k<PASS, 32>(a, pl, grid_x, s);
     else
-        launch_v<PASS, 64, 64>(a, pl.av, pl.bv, grid_x, pl.splits, pl.phases, s);
+        launch_k<PASS, 16>(a, pl, grid_x, s);
 }
 
 Args make_args(const ConvGeom &g, const GemmPlan &pl) {
@@ -603,7 +707,7 @@ Args make_args(const ConvGeom &g, const GemmPlan &pl) {
     a.st = g.st; a.pad = g.pad; a.P = g.P; a.Q = g.Q;
     a.M = pl.M; a.Ng = pl.Ng; a.Kg = pl.Kg;
     a.tiles_m = pl.tiles_m; a.tiles_n = pl.tiles_n; a.tiles = pl.tiles_m * pl.tiles_n;
-    a.splits = pl.splits; a.kt_per_split = pl.kt_per_split;
+    a.splits = pl.splits; a.kt_per_split = pl.kt_per_split; a.phases = pl.phases;
     a.fC = make_fdiv(g.C); a.fS = make_fdiv(g.S); a.fK = make_fdiv(g.K);
     a.fQ = make_fdiv(g.Q); a.fPQ = make_fdiv(g.P * g.Q);
     return a;
@@ -617,8 +721,10 @@ int run(const ConvGeom &g, const GemmPlan &pl, Args a, void *ws, hipStream_t s) 
             return fail(DC_EINVAL, "conv pass %d needs %zu bytes of workspace", pl.pass, pl.ws_bytes);
         a.partial = static_cast<float *>(ws);
     }
-    int tiles = pl.tiles_m * pl.tiles_n;
-    int grid_x = (tiles + 7) / 8 * 8;
+    const int64_t range = ((int64_t)pl.tiles_m * pl.tiles_n * pl.splits + 7) / 8 * 8;
+    if (range * pl.phases > INT_MAX)
+        return fail(DC_EINVAL, "conv pass %d needs %lld workgroups", pl.pass, (long long)(range * pl.phases));
+    const int grid_x = (int)(range * pl.phases);
     switch (pl.pass) {
     case PASS_FWD: launch_p<PASS_FWD>(a, pl, grid_x, s); break;
     case PASS_DGRAD: launch_p<PASS_DGRAD>(a, pl, grid_x, s); break;
@@ -626,12 +732,23 @@ int run(const ConvGeom &g, const GemmPlan &pl, Args a, void *ws, hipStream_t s) 
     }
     DC_HIP(hipGetLastError());
     if (pl.splits > 1) {
-        size_t total = (size_t)pl.M * pl.Ng;
-        int blocks = (int)std::min<size_t>((total + 255) / 256, 4096);
-        switch (pl.pass) {
-        case PASS_FWD: hipLaunchKernelGGL(splitk_reduce_kernel<PASS_FWD>, dim3(blocks, 1), dim3(256), 0, s, a); break;
-        case PASS_DGRAD: hipLaunchKernelGGL(splitk_reduce_kernel<PASS_DGRAD>, dim3(blocks, pl.phases), dim3(256), 0, s, a); break;
-        default: hipLaunchKernelGGL(splitk_reduce_kernel<PASS_WGRAD>, dim3(blocks, 1), dim3(256), 0, s, a); break;
+        // Lanes per output group: about one lane per four slots, at most 16
+        // (so a group row of the partial buffer is read as >= 256 bytes).
+        int lg_r = 0;
+        while (lg_r < 4 && (4 << (lg_r + 1)) <= pl.splits)
+            ++lg_r;
+        const bool vec = pl.Ng % 4 == 0 && (uintptr_t)ws % 16 == 0;
+        const size_t groups = (size_t)pl.M * pl.Ng / (vec ? 4 : 1);
+        const size_t per_wg = (size_t)256 >> lg_r;
+        const int blocks = (int)std::min<size_t>((groups + per_wg - 1) / per_wg, 8192);
+        const dim3 grid(blocks, pl.pass == PASS_DGRAD ? pl.phases : 1);
+        switch (pl.pass * 2 + (vec ? 1 : 0)) {
+        case PASS_FWD * 2: hipLaunchKernelGGL((splitk_reduce_kernel<PASS_FWD, false>), grid, dim3(256), 0, s, a, lg_r); break;
+        case PASS_FWD * 2 + 1: hipLaunchKernelGGL((splitk_reduce_kernel<PASS_FWD, true>), grid, dim3(256), 0, s, a, lg_r); break;
+        case PASS_DGRAD * 2: hipLaunchKernelGGL((splitk_reduce_kernel<PASS_DGRAD, false>), grid, dim3(256), 0, s, a, lg_r); break;
+        case PASS_DGRAD * 2 + 1: hipLaunchKernelGGL((splitk_reduce_kernel<PASS_DGRAD, true>), grid, dim3(256), 0, s, a, lg_r); break;
+        case PASS_WGRAD * 2: hipLaunchKernelGGL((splitk_reduce_kernel<PASS_WGRAD, false>), grid, dim3(256), 0, s, a, lg_r); break;
+        default: hipLaunchKernelGGL((splitk_reduce_kernel<PASS_WGRAD, true>), grid, dim3(256), 0, s, a, lg_r); break;
         }
         DC_HIP(hipGetLastError());
     }
@@ -656,7 +773,14 @@ bool conv_geom_from_shape(const dc_conv_shape &sh, ConvGeom *g) {
     return big < INT_MAX;
 }
 
-GemmPlan plan_gemm(const ConvGeom &g, int pass) {
+// Relative per-stage efficiency of a 32-deep K stage over a 16-deep one
+// (fewer barriers and LDS round trips per MFMA, at lower occupancy).
+static double kt32_gain(int pass) {
+    (void)pass;
+    return 1.0;
+}
+
+static GemmPlan plan_core(const ConvGeom &g, int pass) {
     GemmPlan pl{};
     pl.pass = pass;
     pl.phases = 1;
@@ -684,11 +808,15 @@ GemmPlan plan_gemm(const ConvGeom &g, int pass) {
     // split pays for writing and re-reading its partial sums.
     static const int cand[4][2] = {{128, 128}, {128, 64}, {64, 128}, {64, 64}};
     static const double eff[4] = {1.0, 0.9, 0.9, 0.75};
-    static const int occ[4] = {3, 4, 4, 6};
+    static const int occ16[4] = {3, 4, 4, 6};
+    static const int occ32[4] = {2, 3, 3, 4};
     auto util = [](double c) { return c >= 3 ? 0.95 : c >= 2 ? 0.75 + 0.2 * (c - 2) : 0.45 + 0.3 * (c - 1); };
-    const int ktiles = std::max(1, (pl.Kg + KT - 1) / KT);
     double best = 1e300;
+    for (int KT : {16, 32})
     for (int c = 0; c < 4; ++c) {
+        const int ktiles = std::max(1, (pl.Kg + KT - 1) / KT);
+        const int *occ = KT == 32 ? occ32 : occ16;
+        const double eff_k = KT == 32 ? kt32_gain(pl.pass) : 1.0;
         int mt = cand[c][0], nt = cand[c][1];
         int tm = (pl.M + mt - 1) / mt, tn = (pl.Ng + nt - 1) / nt;
         int64_t tiles = (int64_t)tm * tn * pl.phases;
@@ -700,7 +828,7 @@ GemmPlan plan_gemm(const ConvGeom &g, int pass) {
             int64_t wgs = tiles * spe;
             double per_cu = std::ceil((double)wgs / 256.0); // workgroups one CU works through
             double conc = std::min<double>(per_cu, occ[c]);
-            double wg_cycles = 2.0 * mt * nt * KT * kps / (256.0 * eff[c]);
+            double wg_cycles = 2.0 * mt * nt * KT * kps / (256.0 * eff[c] * eff_k);
             double t_main = per_cu * wg_cycles / util(conc) / 2.4; // ns at 2.4 GHz
             double t_red = 0;
             if (spe > 1)
@@ -708,7 +836,7 @@ GemmPlan plan_gemm(const ConvGeom &g, int pass) {
             double cost = t_main + t_red;
             if (cost < best * 0.97) {
                 best = cost;
-                pl.mt = mt; pl.nt = nt; pl.splits = spe; pl.kt_per_split = kps;
+                pl.mt = mt; pl.nt = nt; pl.kt = KT; pl.splits = spe; pl.kt_per_split = kps;
                 pl.tiles_m = tm; pl.tiles_n = tn;
             }
         }
@@ -717,8 +845,49 @@ GemmPlan plan_gemm(const ConvGeom &g, int pass) {
     return pl;
 }
 
+static size_t round256(size_t b) { return (b + 255) / 256 * 256; }
+
+// Forward and wgrad with C % 4 != 0 run on channel-padded copies of x (and of
+// w, or of dw) held in the workspace after the split-K partial sums.
+static bool pads_channels(const ConvGeom &g, int pass) {
+    if (pass == PASS_DGRAD || g.C % 4 == 0)
+        return false;
+    const int64_t cp = (g.C + 3) / 4 * 4;
+    return (int64_t)g.N * g.H * g.W * cp < INT_MAX && (int64_t)g.K * g.R * g.S * cp < INT_MAX;
+}
+
+static ConvGeom padded(const ConvGeom &g) {
+    ConvGeom gp = g;
+    gp.C = (g.C + 3) / 4 * 4;
+    return gp;
+}
+
+GemmPlan plan_gemm(const ConvGeom &g, int pass) {
+    if (!pads_channels(g, pass))
+        return plan_core(g, pass);
+    const ConvGeom gp = padded(g);
+    GemmPlan pl = plan_core(gp, pass);
+    pl.cpad = gp.C;
+    pl.pad_x_off = round256(pl.ws_bytes);
+    pl.pad_w_off = pl.pad_x_off + round256((size_t)g.N * g.H * g.W * gp.C * sizeof(float));
+    pl.ws_bytes = pl.pad_w_off + round256((size_t)g.K * g.R * g.S * gp.C * sizeof(float));
+    return pl;
+}
+
 int conv_forward(const ConvGeom &g, const GemmPlan &pl, const float *x, const float *w,
                  const float *bias, int relu, float *y, void *ws, hipStream_t s) {
+    if (pl.cpad) {
+        if (!ws)
+            return fail(DC_EINVAL, "conv forward needs %zu bytes of workspace", pl.ws_bytes);
+        float *xp = reinterpret_cast<float *>(static_cast<char *>(ws) + pl.pad_x_off);
+        float *wp = reinterpret_cast<float *>(static_cast<char *>(ws) + pl.pad_w_off);
+        DC_TRY(pad_channels(x, xp, (int64_t)g.N * g.H * g.W, g.C, pl.cpad, s));
+        DC_TRY(pad_channels(w, wp, (int64_t)g.K * g.R * g.S, g.C, pl.cpad, s));
+        const ConvGeom gp = padded(g);
+        Args a = make_args(gp, pl);
+        a.A = xp; a.B = wp; a.out = y; a.bias = bias; a.relu = relu;
+        return run(gp, pl, a, ws, s);
+    }
     Args a = make_args(g, pl);
     a.A = x; a.B = w; a.out = y; a.bias = bias; a.relu = relu;
     return run(g, pl, a, ws, s);
@@ -733,6 +902,18 @@ int conv_dgrad(const ConvGeom &g, const GemmPlan &pl, const float *dy, const flo
 
 int conv_wgrad(const ConvGeom &g, const GemmPlan &pl, const float *x, const float *dy, float *dw,
                void *ws, hipStream_t s) {
+    if (pl.cpad) {
+        if (!ws)
+            return fail(DC_EINVAL, "conv wgrad needs %zu bytes of workspace", pl.ws_bytes);
+        float *xp = reinterpret_cast<float *>(static_cast<char *>(ws) + pl.pad_x_off);
+        float *dwp = reinterpret_cast<float *>(static_cast<char *>(ws) + pl.pad_w_off);
+        DC_TRY(pad_channels(x, xp, (int64_t)g.N * g.H * g.W, g.C, pl.cpad, s));
+        const ConvGeom gp = padded(g);
+        Args a = make_args(gp, pl);
+        a.A = dy; a.B = xp; a.out = dwp;
+        DC_TRY(run(gp, pl, a, ws, s));
+        return unpad_channels(dwp, dw, (int64_t)g.K * g.R * g.S, g.C, pl.cpad, s);
+    }
     Args a = make_args(g, pl);
     a.A = dy; a.B = x; a.out = dw;
     return run(g, pl, a, ws, s);

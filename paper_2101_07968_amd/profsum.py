@@ -6,7 +6,7 @@
       --workload vgg16 --batch 32 --cmd "<commands>" > profiles/igemm_<workload>_b<batch>_traffic.txt
 
 stats: per-kernel totals from --stats, and the implicit-GEMM window that bench.py
-times live (every igemm / split-K dispatch after the last link-pacing kernel,
+times live (every igemm / split-K / channel-padding dispatch after the last pacing kernel,
 i.e. the per-pass timing loop: 1 warm-up + 3 timed launches per pass) reduced
 to one iteration's worth, for comparison with the bench's conv_ms_per_step.
 
@@ -27,12 +27,13 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 
 def short(name):
     name = name.replace("dc::(anonymous namespace)::", "")
-    name = re.sub(r"\(.*$", "", name) if "igemm" not in name and "splitk" not in name else name.split("(")[0]
+    name = re.sub(r"\(.*$", "", name) if not is_gemm(name) else name.split("(")[0]
     return name.replace("void ", "")[:80]
 
 
 def is_gemm(name):
-    return "igemm_kernel" in name or "splitk_reduce_kernel" in name
+    """A dispatch of a conv/FC pass: the GEMM, its split-K reduction or its channel padding."""
+    return any(k in name for k in ("igemm_kernel", "splitk_reduce_kernel", "pad_channels_kernel"))
 
 
 def cmd_stats(a):
@@ -44,7 +45,8 @@ def cmd_stats(a):
                    f"{float(r['AverageNs']) / 1e3:.1f} | {float(r['Percentage']):.2f} |")
     gemm_total = sum(float(r["TotalDurationNs"]) for r in rows if is_gemm(r["Name"]))
     gemm_calls = sum(int(r["Calls"]) for r in rows if is_gemm(r["Name"]))
-    out += ["", f"All implicit-GEMM + split-K dispatches: {gemm_calls} calls, {gemm_total / 1e6:.2f} ms."]
+    out += ["", f"All conv-pass dispatches (implicit GEMM, split-K reduce, channel padding): {gemm_calls} calls, "
+            f"{gemm_total / 1e6:.2f} ms."]
     trace = list(csv.DictReader(open(a.trace)))
     trace.sort(key=lambda r: int(r["Start_Timestamp"]))
     last_pace = max((i for i, r in enumerate(trace) if "pace_" in r["Kernel_Name"]), default=-1)
@@ -52,7 +54,7 @@ def cmd_stats(a):
     dur = sum(int(r["End_Timestamp"]) - int(r["Start_Timestamp"]) for r in win)
     per_iter = dur / a.passes_per_conv / 1e6
     out += ["", "Roofline window (the per-pass timing loop of bench.py, after the last pacing kernel):",
-            f"{len(win)} GEMM dispatches, {dur / 1e6:.2f} ms in all, {per_iter:.3f} ms per iteration "
+            f"{len(win)} conv-pass dispatches, {dur / 1e6:.2f} ms in all, {per_iter:.3f} ms per iteration "
             f"({a.passes_per_conv} launches per pass).",
             f"Mean duration per launch: {dur / max(len(win), 1) / 1e3:.1f} us."]
     if a.flops:
