@@ -188,6 +188,7 @@ def main():
     x, y, params = synth.cnn_inputs(wl["seed"], batch, hwc, classes, specs)
     torch.cuda.set_device(0)
     model = D.Model(ops, batch, hwc, classes)
+    model.set_option(D.DC_OPT_LR, wl["lr"])
     model.ps_write(params)
     xd, yd = torch.from_numpy(x).cuda(), torch.from_numpy(y).cuda()
     paced = args.link_gbps != "pcie"
@@ -270,7 +271,8 @@ def main():
         "data": "synthetic (seeded N(0,1) images, uniform labels, He-normal weights)",
         "config": {"workload": name, "global_batch": batch, "image": list(hwc), "classes": classes,
                    "link": f"{args.link_gbps} Gb/s paced" if paced else "unpaced host interface",
-                   "dt_emul_ms": args.dt_emul_ms, "plan": "dynacomm-dp", "parallelism": "single GPU"},
+                   "dt_emul_ms": args.dt_emul_ms, "lr": wl["lr"], "plan": "dynacomm-dp",
+                   "parallelism": "single GPU"},
         "plan": {"p": plan.decisions()[0], "g": plan.decisions()[1], "t_plan_us": round(t_plan_us, 1),
                  "t_profile_s": round(t_profile, 3)},
         "dynacomm": {k: round(v, 4) if isinstance(v, float) else v for k, v in main_res.items()},

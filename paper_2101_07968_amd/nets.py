@@ -166,15 +166,17 @@ def googlenet():
 
 BUILDERS = {"tiny": tiny, "alexnet": alexnet, "resnet18": resnet18, "vgg16": vgg16, "resnet50": resnet50, "googlenet": googlenet}
 
-# The workloads' batch size, emulated link rate (bytes/s; 1 Gb/s = 1.25e8 B/s)
-# and input seed.
+# The workloads' batch size, emulated link rate (bytes/s; 1 Gb/s = 1.25e8 B/s),
+# input seed and SGD learning rate (1e-3 for the two networks without
+# BatchNorm, whose loss diverges within three steps at 1e-2 from He-normal
+# weights on N(0,1) images).
 WORKLOADS = {
-    "tiny": {"batch": 4, "link": 1e9, "seed": 0},
-    "alexnet": {"batch": 32, "link": 100e6 / 8, "seed": 1},
-    "resnet18": {"batch": 128, "link": 1e9 / 8, "seed": 2},
-    "vgg16": {"batch": 32, "link": 10e9 / 8, "seed": 3},
-    "resnet50": {"batch": 64, "link": 10e9 / 8, "seed": 4},
-    "googlenet": {"batch": 32, "link": 10e9 / 8, "seed": 5},
+    "tiny": {"batch": 4, "link": 1e9, "seed": 0, "lr": 1e-2},
+    "alexnet": {"batch": 32, "link": 100e6 / 8, "seed": 1, "lr": 1e-3},
+    "resnet18": {"batch": 128, "link": 1e9 / 8, "seed": 2, "lr": 1e-2},
+    "vgg16": {"batch": 32, "link": 10e9 / 8, "seed": 3, "lr": 1e-3},
+    "resnet50": {"batch": 64, "link": 10e9 / 8, "seed": 4, "lr": 1e-2},
+    "googlenet": {"batch": 32, "link": 10e9 / 8, "seed": 5, "lr": 1e-2},
 }
 
 

@@ -24,6 +24,7 @@ def run_case(D, PN, synth, torch, name, rate_bps, paced, steps, lbl_limit_s=6.0)
     specs = PN.param_specs(ops, hwc)
     x, y, params = synth.cnn_inputs(wl["seed"], wl["batch"], hwc, classes, specs)
     model = D.Model(ops, wl["batch"], hwc, classes)
+    model.set_option(D.DC_OPT_LR, wl["lr"])
     model.ps_write(params)
     xd, yd = torch.from_numpy(x).cuda(), torch.from_numpy(y).cuda()
     lnk = D.link(rate_bps if paced else 1e9, 0, paced=paced)
@@ -76,6 +77,7 @@ def adapt(D, PN, synth, torch, name, rates_gbps, steps):
     ops, hwc, classes = PN.build(name)
     x, y, params = synth.cnn_inputs(wl["seed"], wl["batch"], hwc, classes, PN.param_specs(ops, hwc))
     model = D.Model(ops, wl["batch"], hwc, classes)
+    model.set_option(D.DC_OPT_LR, wl["lr"])
     model.ps_write(params)
     xd, yd = torch.from_numpy(x).cuda(), torch.from_numpy(y).cuda()
     out = []
