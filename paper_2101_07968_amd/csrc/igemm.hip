@@ -144,7 +144,12 @@ __global__ __launch_bounds__(NTHR) void igemm_kernel(Args a) {
     constexpr int FA = MT * KT / 4 / NTHR; // float4 fragments per thread
     constexpr int FB = NT * KT / 4 / NTHR;
     static_assert(FA >= 1 && FB >= 1, "tile too small");
-    constexpr int BM = MT / 64, BN = NT / 64; // 32x32 blocks per wave
+    // The 4 waves form a WM x WN grid over the tile (4 x 1 for tall tiles,
+    // 1 x 4 for wide ones, 2 x 2 otherwise); each owns BM x BN 32x32 blocks.
+    constexpr int WM = MT >= 4 * NT ? 4 : (NT >= 4 * MT ? 1 : 2);
+    constexpr int WN = 4 / WM;
+    constexpr int BM = MT / (32 * WM), BN = NT / (32 * WN);
+    static_assert(BM >= 1 && BN >= 1 && BM * 32 * WM == MT && BN * 32 * WN == NT, "tile shape");
 
     __shared__ __attribute__((aligned(16))) float lds[2 * (A_SZ + B_SZ)];
 
@@ -435,7 +440,7 @@ __global__ __launch_bounds__(NTHR) void igemm_kernel(Args a) {
     // ------------------------------------------------ MFMA on one stage
     const int wave = t >> 6, lane = t & 63;
     const int lr = lane & 31, lh = lane >> 5;
-    const int wm = (wave & 1) * (MT / 2), wn = (wave >> 1) * (NT / 2);
+    const int wm = (wave % WM) * (MT / WM), wn = (wave / WM) * (NT / WN);
     f32x16 acc[BM][BN];
 #pragma unroll
     for (int i = 0; i < BM; ++i)
@@ -695,10 +700,7 @@ void launch_k(const Args &a, const GemmPlan &pl, int grid_x, hipStream_t s) {
 
 template <int PASS>
 void launch_p(const Args &a, const GemmPlan &pl, int grid_x, hipStream_t s) {
-    if (pl.kt == 32)
-        launch_k<PASS, 32>(a, pl, grid_x, s);
-    else
-        launch_k<PASS, 16>(a, pl, grid_x, s);
+    launch_k<PASS, 16>(a, pl, grid_x, s);
 }
 
 Args make_args(const ConvGeom &g, const GemmPlan &pl) {
@@ -773,13 +775,6 @@ bool conv_geom_from_shape(const dc_conv_shape &sh, ConvGeom *g) {
     return big < INT_MAX;
 }
 
-// Relative per-stage efficiency of a 32-deep K stage over a 16-deep one
-// (fewer barriers and LDS round trips per MFMA, at lower occupancy).
-static double kt32_gain(int pass) {
-    (void)pass;
-    return 1.0;
-}
-
 static GemmPlan plan_core(const ConvGeom &g, int pass) {
     GemmPlan pl{};
     pl.pass = pass;
@@ -801,22 +796,22 @@ static GemmPlan plan_core(const ConvGeom &g, int pass) {
         pl.bv = g.C % 4 == 0;
     }
     // Pick the tile and split-K factor with the least estimated time.  A CU
-    // that holds c workgroups of this kernel at once keeps its matrix cores
-    // busy a fraction util(c) of the time (one workgroup cannot hide its own
-    // global-load latency); a tile holds at most `occ` workgroups per CU
-    // (registers and LDS); smaller tiles move more bytes per flop (eff); a
-    // split pays for writing and re-reading its partial sums.
+    // holds at most occ[c] workgroups of a tile at once (registers and LDS)
+    // and, holding k of them, keeps its matrix cores busy a fraction util(k)
+    // of the time (one workgroup cannot hide its own global-load latency).
+    // A CU that receives n workgroups runs n / occ full rounds and then a
+    // partial round of n % occ at the lower utilisation of that count (the
+    // tail).  Smaller tiles move more operand bytes per flop (eff, fitted to
+    // measured VGG-16 / ResNet-50 / GoogLeNet / AlexNet passes); a split pays
+    // for writing and re-reading its partial sums.
     static const int cand[4][2] = {{128, 128}, {128, 64}, {64, 128}, {64, 64}};
-    static const double eff[4] = {1.0, 0.9, 0.9, 0.75};
-    static const int occ16[4] = {3, 4, 4, 6};
-    static const int occ32[4] = {2, 3, 3, 4};
-    auto util = [](double c) { return c >= 3 ? 0.95 : c >= 2 ? 0.75 + 0.2 * (c - 2) : 0.45 + 0.3 * (c - 1); };
+    static const double eff[4] = {1.0, 0.9, 0.85, 0.85};
+    static const int occ[4] = {3, 4, 4, 6};
+    auto util = [](int k) { return std::min(0.95, 0.35 + 0.3 * k); };
     double best = 1e300;
-    for (int KT : {16, 32})
+    const int KT = 16;
+    const int ktiles = std::max(1, (pl.Kg + KT - 1) / KT);
     for (int c = 0; c < 4; ++c) {
-        const int ktiles = std::max(1, (pl.Kg + KT - 1) / KT);
-        const int *occ = KT == 32 ? occ32 : occ16;
-        const double eff_k = KT == 32 ? kt32_gain(pl.pass) : 1.0;
         int mt = cand[c][0], nt = cand[c][1];
         int tm = (pl.M + mt - 1) / mt, tn = (pl.Ng + nt - 1) / nt;
         int64_t tiles = (int64_t)tm * tn * pl.phases;
@@ -826,10 +821,13 @@ static GemmPlan plan_core(const ConvGeom &g, int pass) {
             int kps = (ktiles + sp - 1) / sp;
             int spe = (ktiles + kps - 1) / kps;
             int64_t wgs = tiles * spe;
-            double per_cu = std::ceil((double)wgs / 256.0); // workgroups one CU works through
-            double conc = std::min<double>(per_cu, occ[c]);
-            double wg_cycles = 2.0 * mt * nt * KT * kps / (256.0 * eff[c] * eff_k);
-            double t_main = per_cu * wg_cycles / util(conc) / 2.4; // ns at 2.4 GHz
+            const int64_t per_cu = (wgs + 255) / 256; // workgroups the busiest CU works through
+            const int64_t full = per_cu / occ[c], rem = per_cu % occ[c];
+            const double wg_cycles = 2.0 * mt * nt * KT * kps / (256.0 * eff[c]);
+            double t_main = (double)full * occ[c] * wg_cycles / util(occ[c]);
+            if (rem)
+                t_main += (double)rem * wg_cycles / util((int)rem);
+            t_main /= 2.4; // ns at 2.4 GHz
             double t_red = 0;
             if (spe > 1)
                 t_red = 4000.0 + 2.0 * (double)(spe + 1) * pl.M * pl.Ng * pl.phases * 4.0 / 4000.0; // ns
