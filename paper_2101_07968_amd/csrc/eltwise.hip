@@ -11,6 +11,9 @@
 #include "dc_internal.h"
 
 #include <algorithm>
+#include <climits>
+#include <cstdint>
+#include <numeric>
 
 namespace dc {
 namespace {
@@ -194,6 +197,86 @@ __global__ void maxpool_bwd_kernel(dc_pool_shape sh, int P, int Q, const float *
     }
 }
 
+// Float4 variants for c % 4 == 0: a thread owns one channel quad of one
+// output (forward) or input (backward) pixel, so the index arithmetic is
+// paid once per four channels and in 32 bits (the host checks the sizes).
+// Per channel they make exactly the decisions and sums of the scalar kernels.
+__global__ void maxpool_fwd4_kernel(dc_pool_shape sh, int P, int Q, int c4, int total4,
+                                    const float4 *__restrict__ x, float4 *__restrict__ y,
+                                    uchar4 *__restrict__ arg) {
+    for (int e = blockIdx.x * blockDim.x + threadIdx.x; e < total4; e += gridDim.x * blockDim.x) {
+        const int q4 = e % c4;
+        const int pix = e / c4;
+        const int q = pix % Q;
+        const int t = pix / Q;
+        const int p = t % P;
+        const int n = t / P;
+        float bv[4] = {0.f, 0.f, 0.f, 0.f};
+        int best[4] = {-1, -1, -1, -1};
+        for (int r = 0; r < sh.r; ++r) {
+            const int h = p * sh.stride + r - sh.pad;
+            if ((unsigned)h >= (unsigned)sh.h)
+                continue;
+            for (int s = 0; s < sh.s; ++s) {
+                const int w = q * sh.stride + s - sh.pad;
+                if ((unsigned)w >= (unsigned)sh.w)
+                    continue;
+                const float4 v = x[((n * sh.h + h) * sh.w + w) * c4 + q4];
+                const float vv[4] = {v.x, v.y, v.z, v.w};
+                const int k = r * sh.s + s;
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    if (best[j] < 0 || vv[j] > bv[j]) {
+                        best[j] = k;
+                        bv[j] = vv[j];
+                    }
+            }
+        }
+        y[e] = make_float4(bv[0], bv[1], bv[2], bv[3]);
+        arg[e] = make_uchar4((unsigned char)max(best[0], 0), (unsigned char)max(best[1], 0),
+                             (unsigned char)max(best[2], 0), (unsigned char)max(best[3], 0));
+    }
+}
+
+__global__ void maxpool_bwd4_kernel(dc_pool_shape sh, int P, int Q, int c4, int total4,
+                                    const float4 *__restrict__ dy, const uchar4 *__restrict__ arg, int acc,
+                                    float4 *__restrict__ dx) {
+    for (int e = blockIdx.x * blockDim.x + threadIdx.x; e < total4; e += gridDim.x * blockDim.x) {
+        const int q4 = e % c4;
+        const int pix = e / c4;
+        const int w = pix % sh.w;
+        const int t = pix / sh.w;
+        const int h = t % sh.h;
+        const int n = t / sh.h;
+        const int hp = h + sh.pad, wp = w + sh.pad;
+        const int p_lo = hp - sh.r + 1 > 0 ? (hp - sh.r + 1 + sh.stride - 1) / sh.stride : 0;
+        const int p_hi = min(P - 1, hp / sh.stride);
+        const int q_lo = wp - sh.s + 1 > 0 ? (wp - sh.s + 1 + sh.stride - 1) / sh.stride : 0;
+        const int q_hi = min(Q - 1, wp / sh.stride);
+        float4 g = make_float4(0.f, 0.f, 0.f, 0.f);
+        for (int p = p_lo; p <= p_hi; ++p)
+            for (int q = q_lo; q <= q_hi; ++q) {
+                const int o = ((n * P + p) * Q + q) * c4 + q4;
+                const int a = (hp - p * sh.stride) * sh.s + (wp - q * sh.stride);
+                const uchar4 ar = arg[o];
+                const float4 d = dy[o];
+                if (ar.x == a)
+                    g.x += d.x;
+                if (ar.y == a)
+                    g.y += d.y;
+                if (ar.z == a)
+                    g.z += d.z;
+                if (ar.w == a)
+                    g.w += d.w;
+            }
+        if (acc) {
+            const float4 o = dx[e];
+            g.x = o.x + g.x; g.y = o.y + g.y; g.z = o.z + g.z; g.w = o.w + g.w;
+        }
+        dx[e] = g;
+    }
+}
+
 __global__ void gap_fwd_kernel(int n, int hw, int c, const float *__restrict__ x, float *__restrict__ y) {
     int64_t total = (int64_t)n * c;
     for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total; e += (int64_t)gridDim.x * blockDim.x) {
@@ -275,18 +358,21 @@ __global__ __launch_bounds__(EW_THREADS) void colred_partial_kernel(
 // Stage 2: one workgroup per channel adds the chunk partials with a fixed
 // tree in double precision.  Output kind: 0 -> out0 = sum; 1 -> out0 = sum/rows
 // (mean); 2 -> out0 = 1/sqrt(sum/rows + eps) (invstd); 3 -> out0 = sum0, out1 = sum1.
+// 4 -> from the shifted sums of mode 1: out0 = K + S1/rows (mean),
+// out1 = 1/sqrt(S2/rows - (S1/rows)^2 + eps) (invstd), K = shift[ch].
 template <int KIND>
 __global__ __launch_bounds__(EW_THREADS) void colred_final_kernel(int nchunks, int c, int64_t rows, float eps,
                                                                   const float *__restrict__ part0,
                                                                   const float *__restrict__ part1,
-                                                                  float *__restrict__ out0, float *__restrict__ out1) {
+                                                                  float *__restrict__ out0, float *__restrict__ out1,
+                                                                  const float *__restrict__ shift) {
     __shared__ double s0[EW_THREADS];
     __shared__ double s1[EW_THREADS];
     const int ch = blockIdx.x;
     double a0 = 0.0, a1 = 0.0;
     for (int i = threadIdx.x; i < nchunks; i += EW_THREADS) {
         a0 += (double)part0[(int64_t)i * c + ch];
-        if (KIND == 3)
+        if (KIND >= 3)
             a1 += (double)part1[(int64_t)i * c + ch];
     }
     s0[threadIdx.x] = a0;
@@ -307,9 +393,14 @@ __global__ __launch_bounds__(EW_THREADS) void colred_final_kernel(int nchunks, i
             out0[ch] = (float)(v / (double)rows);
         } else if (KIND == 2) {
             out0[ch] = (float)(1.0 / sqrt(v / (double)rows + (double)eps));
-        } else {
+        } else if (KIND == 3) {
             out0[ch] = (float)v;
             out1[ch] = (float)s1[0];
+        } else {
+            const double m1 = v / (double)rows;
+            const double var = std::max(0.0, s1[0] / (double)rows - m1 * m1);
+            out0[ch] = (float)((double)shift[ch] + m1);
+            out1[ch] = (float)(1.0 / sqrt(var + (double)eps));
         }
     }
 }
@@ -340,6 +431,147 @@ __global__ void bn_bwd_apply_kernel(int64_t rows, int c, const float *__restrict
     }
 }
 
+// Float4 path of the per-channel reductions, for c % 4 == 0 and 16-byte
+// aligned tensors.  A workgroup's 256 threads are G channel quads x RL row
+// lanes (G = min(c/4, 64), RL = 256 / G rounded down; leftover threads stay
+// idle); it owns rows [chunk*rpc, ...) of channels [blk*4G, ...).  A thread
+// sums rows rl, rl + RL, ... into two independent float4 accumulators, the
+// row lanes are added in lane order through LDS, and the partials go to fixed
+// slots.  Mode 0: sum x.  Mode 1: sum (x - K) and sum (x - K)^2 with K the
+// channel's value in row 0, a shift that keeps the one-pass variance free of
+// cancellation.  Mode 2: sum dy and sum dy * (x - mean) * invstd.
+template <int MODE>
+__device__ __forceinline__ void col4_acc(float4 &a0, float4 &a1, const float4 v, const float4 d, const float4 mu,
+                                         const float4 is) {
+    if (MODE == 0) {
+        a0.x += v.x; a0.y += v.y; a0.z += v.z; a0.w += v.w;
+    } else if (MODE == 1) {
+        const float x0 = v.x - mu.x, x1 = v.y - mu.y, x2 = v.z - mu.z, x3 = v.w - mu.w;
+        a0.x += x0; a0.y += x1; a0.z += x2; a0.w += x3;
+        a1.x += x0 * x0; a1.y += x1 * x1; a1.z += x2 * x2; a1.w += x3 * x3;
+    } else {
+        a0.x += d.x; a0.y += d.y; a0.z += d.z; a0.w += d.w;
+        a1.x += d.x * ((v.x - mu.x) * is.x);
+        a1.y += d.y * ((v.y - mu.y) * is.y);
+        a1.z += d.z * ((v.z - mu.z) * is.z);
+        a1.w += d.w * ((v.w - mu.w) * is.w);
+    }
+}
+
+__device__ __forceinline__ float4 add4(float4 a, float4 b) {
+    return make_float4(a.x + b.x, a.y + b.y, a.z + b.z, a.w + b.w);
+}
+
+template <int MODE>
+__global__ __launch_bounds__(EW_THREADS) void colred4_partial_kernel(
+    int64_t rows, int c, int64_t rpc, int g, int rl_n, const float *__restrict__ x, const float *__restrict__ dy,
+    const float *__restrict__ mean, const float *__restrict__ invstd, float *__restrict__ part0,
+    float *__restrict__ part1) {
+    __shared__ float4 s0[EW_THREADS];
+    __shared__ float4 s1[EW_THREADS];
+    const int t = threadIdx.x;
+    const int q = t % g, rl = t / g;
+    const int ch = (blockIdx.y * g + q) * 4;
+    const int64_t r0 = (int64_t)blockIdx.x * rpc;
+    const int64_t r1 = min(rows, r0 + rpc);
+    const float4 z4 = make_float4(0.f, 0.f, 0.f, 0.f);
+    float4 a0 = z4, a1 = z4, b0 = z4, b1 = z4;
+    if (rl < rl_n && ch < c) {
+        float4 mu = z4, is = z4;
+        if (MODE == 1)
+            mu = *reinterpret_cast<const float4 *>(x + ch);
+        if (MODE == 2) {
+            mu = *reinterpret_cast<const float4 *>(mean + ch);
+            is = *reinterpret_cast<const float4 *>(invstd + ch);
+        }
+        const float *src = MODE == 2 ? dy : x;
+        int64_t r = r0 + rl;
+        for (; r + rl_n < r1; r += 2 * (int64_t)rl_n) {
+            const int64_t o0 = r * c + ch, o1 = (r + rl_n) * c + ch;
+            const float4 v0 = *reinterpret_cast<const float4 *>(x + o0);
+            const float4 v1 = *reinterpret_cast<const float4 *>(x + o1);
+            const float4 d0 = MODE == 2 ? *reinterpret_cast<const float4 *>(src + o0) : z4;
+            const float4 d1 = MODE == 2 ? *reinterpret_cast<const float4 *>(src + o1) : z4;
+            col4_acc<MODE>(a0, a1, v0, d0, mu, is);
+            col4_acc<MODE>(b0, b1, v1, d1, mu, is);
+        }
+        if (r < r1) {
+            const int64_t o0 = r * c + ch;
+            const float4 v0 = *reinterpret_cast<const float4 *>(x + o0);
+            const float4 d0 = MODE == 2 ? *reinterpret_cast<const float4 *>(src + o0) : z4;
+            col4_acc<MODE>(a0, a1, v0, d0, mu, is);
+        }
+    }
+    s0[t] = add4(a0, b0);
+    s1[t] = add4(a1, b1);
+    __syncthreads();
+    if (rl == 0 && ch < c) {
+        float4 t0 = s0[t], t1 = s1[t];
+        for (int i = 1; i < rl_n; ++i) {
+            t0 = add4(t0, s0[i * g + q]);
+            t1 = add4(t1, s1[i * g + q]);
+        }
+        *reinterpret_cast<float4 *>(part0 + (int64_t)blockIdx.x * c + ch) = t0;
+        if (MODE != 0)
+            *reinterpret_cast<float4 *>(part1 + (int64_t)blockIdx.x * c + ch) = t1;
+    }
+}
+
+// y = gamma * (x - mean) * invstd + beta over n4 float4 groups of [rows][c],
+// c % 4 == 0.  The grid's thread count is a multiple of c/4 (bn4_blocks), so
+// a thread keeps one channel quad, and its parameters, for the whole loop.
+__global__ void bn_apply4_kernel(int64_t n4, int c4, const float4 *__restrict__ x, const float4 *__restrict__ gamma,
+                                 const float4 *__restrict__ beta, const float4 *__restrict__ mean,
+                                 const float4 *__restrict__ invstd, int relu, float4 *__restrict__ y) {
+    const int64_t t0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    const int q = (int)(t0 % c4);
+    const float4 g = gamma[q], b = beta[q], m = mean[q], is = invstd[q];
+    for (int64_t i = t0; i < n4; i += stride) {
+        const float4 v = x[i];
+        float4 o;
+        o.x = g.x * ((v.x - m.x) * is.x) + b.x;
+        o.y = g.y * ((v.y - m.y) * is.y) + b.y;
+        o.z = g.z * ((v.z - m.z) * is.z) + b.z;
+        o.w = g.w * ((v.w - m.w) * is.w) + b.w;
+        if (relu) {
+            o.x = fmaxf(o.x, 0.f); o.y = fmaxf(o.y, 0.f); o.z = fmaxf(o.z, 0.f); o.w = fmaxf(o.w, 0.f);
+        }
+        y[i] = o;
+    }
+}
+
+__device__ __forceinline__ float bn_dx(float dy, float x, float g, float m, float is, float dg, float db,
+                                       float inv_rows) {
+    const float xhat = (x - m) * is;
+    return g * is * (dy - db * inv_rows - xhat * dg * inv_rows);
+}
+
+__global__ void bn_bwd_apply4_kernel(int64_t n4, int c4, int64_t rows, const float4 *__restrict__ dy,
+                                     const float4 *__restrict__ x, const float4 *__restrict__ gamma,
+                                     const float4 *__restrict__ mean, const float4 *__restrict__ invstd,
+                                     const float4 *__restrict__ dgamma, const float4 *__restrict__ dbeta, int acc,
+                                     float4 *__restrict__ dx) {
+    const int64_t t0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    const int q = (int)(t0 % c4);
+    const float inv_rows = 1.0f / (float)rows;
+    const float4 g = gamma[q], m = mean[q], is = invstd[q], dg = dgamma[q], db = dbeta[q];
+    for (int64_t i = t0; i < n4; i += stride) {
+        const float4 d = dy[i], v = x[i];
+        float4 o;
+        o.x = bn_dx(d.x, v.x, g.x, m.x, is.x, dg.x, db.x, inv_rows);
+        o.y = bn_dx(d.y, v.y, g.y, m.y, is.y, dg.y, db.y, inv_rows);
+        o.z = bn_dx(d.z, v.z, g.z, m.z, is.z, dg.z, db.z, inv_rows);
+        o.w = bn_dx(d.w, v.w, g.w, m.w, is.w, dg.w, db.w, inv_rows);
+        if (acc) {
+            const float4 p = dx[i];
+            o.x = p.x + o.x; o.y = p.y + o.y; o.z = p.z + o.z; o.w = p.w + o.w;
+        }
+        dx[i] = o;
+    }
+}
+
 struct ColPlan {
     int nchunks;
     int64_t rows_per_chunk;
@@ -355,6 +587,35 @@ ColPlan col_plan(int64_t rows, int c) {
     p.rows_per_chunk = rpc;
     p.nchunks = (int)((rows + rpc - 1) / rpc);
     return p;
+}
+
+struct Col4Plan {
+    int g, rl_n, blocks, nchunks;
+    int64_t rpc;
+};
+
+Col4Plan col4_plan(int64_t rows, int c) {
+    Col4Plan p;
+    p.g = std::min(c / 4, 64);
+    p.rl_n = EW_THREADS / p.g;
+    p.blocks = (c / 4 + p.g - 1) / p.g;
+    // about 2048 workgroups in all, at least 8 rows per row lane
+    int64_t want = std::max<int64_t>(1, 2048 / p.blocks);
+    p.rpc = std::max<int64_t>((rows + want - 1) / want, (int64_t)p.rl_n * 8);
+    p.nchunks = (int)((rows + p.rpc - 1) / p.rpc);
+    return p;
+}
+
+inline bool col4_ok(int c, const void *a, const void *b = nullptr) {
+    return c % 4 == 0 && ((uintptr_t)a & 15) == 0 && ((uintptr_t)b & 15) == 0;
+}
+
+// Blocks for a float4 loop over [rows][c] whose threads each keep one channel
+// quad: the thread count is rounded up to a multiple of c/4.
+int bn4_blocks(int64_t n4, int c4) {
+    int64_t b = std::max<int64_t>(1, std::min<int64_t>((n4 + EW_THREADS - 1) / EW_THREADS, 1 << 16));
+    int64_t m = c4 / std::gcd(c4, EW_THREADS);
+    return (int)((b + m - 1) / m * m);
 }
 
 size_t align256(size_t b) { return (b + 255) / 256 * 256; }
@@ -511,13 +772,27 @@ int concat_backward(int64_t rows, int c_in, int c_out, int off, const float *dy,
     return DC_OK;
 }
 
+// The float4 pooling kernels index in 32 bits: every input and output
+// element count must stay below 2^31, and c % 4 == 0 with aligned pointers.
+static bool pool4_ok(const dc_pool_shape &sh, int P, int Q, const void *a, const void *b, const void *arg) {
+    return sh.c % 4 == 0 && ((uintptr_t)a & 15) == 0 && ((uintptr_t)b & 15) == 0 && ((uintptr_t)arg & 3) == 0 &&
+           (int64_t)sh.n * sh.h * sh.w * sh.c < INT_MAX && (int64_t)sh.n * P * Q * sh.c < INT_MAX;
+}
+
 int maxpool_forward(const dc_pool_shape &sh, const float *x, float *y, uint8_t *arg, hipStream_t s) {
     int P = (sh.h + 2 * sh.pad - sh.r) / sh.stride + 1;
     int Q = (sh.w + 2 * sh.pad - sh.s) / sh.stride + 1;
     int64_t total = (int64_t)sh.n * P * Q * sh.c;
     if (total <= 0)
         return DC_OK;
-    hipLaunchKernelGGL(maxpool_fwd_kernel, dim3(ew_blocks(total)), dim3(EW_THREADS), 0, s, sh, P, Q, x, y, arg);
+    if (pool4_ok(sh, P, Q, x, y, arg)) {
+        const int total4 = (int)(total / 4);
+        hipLaunchKernelGGL(maxpool_fwd4_kernel, dim3(ew_blocks(total4)), dim3(EW_THREADS), 0, s, sh, P, Q, sh.c / 4,
+                           total4, reinterpret_cast<const float4 *>(x), reinterpret_cast<float4 *>(y),
+                           reinterpret_cast<uchar4 *>(arg));
+    } else {
+        hipLaunchKernelGGL(maxpool_fwd_kernel, dim3(ew_blocks(total)), dim3(EW_THREADS), 0, s, sh, P, Q, x, y, arg);
+    }
     DC_HIP(hipGetLastError());
     return DC_OK;
 }
@@ -529,8 +804,15 @@ int maxpool_backward(const dc_pool_shape &sh, const float *dy, const uint8_t *ar
     int64_t total = (int64_t)sh.n * sh.h * sh.w * sh.c;
     if (total <= 0)
         return DC_OK;
-    hipLaunchKernelGGL(maxpool_bwd_kernel, dim3(ew_blocks(total)), dim3(EW_THREADS), 0, s, sh, P, Q, dy, arg,
-                       accumulate, dx);
+    if (pool4_ok(sh, P, Q, dy, dx, arg)) {
+        const int total4 = (int)(total / 4);
+        hipLaunchKernelGGL(maxpool_bwd4_kernel, dim3(ew_blocks(total4)), dim3(EW_THREADS), 0, s, sh, P, Q, sh.c / 4,
+                           total4, reinterpret_cast<const float4 *>(dy), reinterpret_cast<const uchar4 *>(arg),
+                           accumulate, reinterpret_cast<float4 *>(dx));
+    } else {
+        hipLaunchKernelGGL(maxpool_bwd_kernel, dim3(ew_blocks(total)), dim3(EW_THREADS), 0, s, sh, P, Q, dy, arg,
+                           accumulate, dx);
+    }
     DC_HIP(hipGetLastError());
     return DC_OK;
 }
@@ -553,10 +835,9 @@ int gap_backward(int n, int hw, int c, const float *dy, int accumulate, float *d
     return DC_OK;
 }
 
-size_t colsum_ws_bytes(int64_t rows, int c) {
-    ColPlan p = col_plan(rows, c);
-    return align256((size_t)p.nchunks * c * sizeof(float));
-}
+static int col_slots(int64_t rows, int c) { return std::max(col_plan(rows, c).nchunks, c % 4 == 0 ? col4_plan(rows, c).nchunks : 0); }
+
+size_t colsum_ws_bytes(int64_t rows, int c) { return align256((size_t)col_slots(rows, c) * c * sizeof(float)); }
 
 int colsum(int64_t rows, int c, const float *x, float *out, void *ws, hipStream_t s) {
     if (c <= 0)
@@ -565,41 +846,69 @@ int colsum(int64_t rows, int c, const float *x, float *out, void *ws, hipStream_
         DC_HIP(hipMemsetAsync(out, 0, sizeof(float) * c, s));
         return DC_OK;
     }
-    ColPlan p = col_plan(rows, c);
     float *part = static_cast<float *>(ws);
-    dim3 g1(p.nchunks, (c + CG - 1) / CG);
-    hipLaunchKernelGGL(colred_partial_kernel<0>, g1, dim3(EW_THREADS), 0, s, rows, c, p.rows_per_chunk, x,
-                       (const float *)nullptr, (const float *)nullptr, (const float *)nullptr, part, (float *)nullptr);
+    int nchunks;
+    if (col4_ok(c, x, part)) {
+        Col4Plan p = col4_plan(rows, c);
+        hipLaunchKernelGGL(colred4_partial_kernel<0>, dim3(p.nchunks, p.blocks), dim3(EW_THREADS), 0, s, rows, c,
+                           p.rpc, p.g, p.rl_n, x, (const float *)nullptr, (const float *)nullptr,
+                           (const float *)nullptr, part, (float *)nullptr);
+        nchunks = p.nchunks;
+    } else {
+        ColPlan p = col_plan(rows, c);
+        dim3 g1(p.nchunks, (c + CG - 1) / CG);
+        hipLaunchKernelGGL(colred_partial_kernel<0>, g1, dim3(EW_THREADS), 0, s, rows, c, p.rows_per_chunk, x,
+                           (const float *)nullptr, (const float *)nullptr, (const float *)nullptr, part,
+                           (float *)nullptr);
+        nchunks = p.nchunks;
+    }
     DC_HIP(hipGetLastError());
-    hipLaunchKernelGGL(colred_final_kernel<0>, dim3(c), dim3(EW_THREADS), 0, s, p.nchunks, c, rows, 0.f, part,
-                       (const float *)nullptr, out, (float *)nullptr);
+    hipLaunchKernelGGL(colred_final_kernel<0>, dim3(c), dim3(EW_THREADS), 0, s, nchunks, c, rows, 0.f, part,
+                       (const float *)nullptr, out, (float *)nullptr, (const float *)nullptr);
     DC_HIP(hipGetLastError());
     return DC_OK;
 }
 
-size_t bn_ws_bytes(int64_t rows, int c) {
-    ColPlan p = col_plan(rows, c);
-    return 2 * align256((size_t)p.nchunks * c * sizeof(float));
-}
+size_t bn_ws_bytes(int64_t rows, int c) { return 2 * align256((size_t)col_slots(rows, c) * c * sizeof(float)); }
 
 int bn_forward(int64_t rows, int c, const float *x, const float *gamma, const float *beta, float eps, int relu,
                float *y, float *mean, float *invstd, void *ws, hipStream_t s) {
     if (rows <= 0 || c <= 0)
         return DC_OK;
-    ColPlan p = col_plan(rows, c);
     float *part = static_cast<float *>(ws);
+    float *part1 = reinterpret_cast<float *>(static_cast<char *>(ws) +
+                                             align256((size_t)col_slots(rows, c) * c * sizeof(float)));
+    if (col4_ok(c, x, y) && col4_ok(c, gamma, beta) && col4_ok(c, mean, invstd) && col4_ok(c, part, part1)) {
+        // one statistics pass (shifted sums), then the normalisation: 12 bytes per element
+        Col4Plan p = col4_plan(rows, c);
+        hipLaunchKernelGGL(colred4_partial_kernel<1>, dim3(p.nchunks, p.blocks), dim3(EW_THREADS), 0, s, rows, c,
+                           p.rpc, p.g, p.rl_n, x, (const float *)nullptr, (const float *)nullptr,
+                           (const float *)nullptr, part, part1);
+        DC_HIP(hipGetLastError());
+        hipLaunchKernelGGL(colred_final_kernel<4>, dim3(c), dim3(EW_THREADS), 0, s, p.nchunks, c, rows, eps, part,
+                           (const float *)part1, mean, invstd, x);
+        DC_HIP(hipGetLastError());
+        const int64_t n4 = rows * c / 4;
+        hipLaunchKernelGGL(bn_apply4_kernel, dim3(bn4_blocks(n4, c / 4)), dim3(EW_THREADS), 0, s, n4, c / 4,
+                           reinterpret_cast<const float4 *>(x), reinterpret_cast<const float4 *>(gamma),
+                           reinterpret_cast<const float4 *>(beta), reinterpret_cast<const float4 *>(mean),
+                           reinterpret_cast<const float4 *>(invstd), relu, reinterpret_cast<float4 *>(y));
+        DC_HIP(hipGetLastError());
+        return DC_OK;
+    }
+    ColPlan p = col_plan(rows, c);
     dim3 g1(p.nchunks, (c + CG - 1) / CG);
     hipLaunchKernelGGL(colred_partial_kernel<0>, g1, dim3(EW_THREADS), 0, s, rows, c, p.rows_per_chunk, x,
                        (const float *)nullptr, (const float *)nullptr, (const float *)nullptr, part, (float *)nullptr);
     DC_HIP(hipGetLastError());
     hipLaunchKernelGGL(colred_final_kernel<1>, dim3(c), dim3(EW_THREADS), 0, s, p.nchunks, c, rows, eps, part,
-                       (const float *)nullptr, mean, (float *)nullptr);
+                       (const float *)nullptr, mean, (float *)nullptr, (const float *)nullptr);
     DC_HIP(hipGetLastError());
     hipLaunchKernelGGL(colred_partial_kernel<1>, g1, dim3(EW_THREADS), 0, s, rows, c, p.rows_per_chunk, x,
                        (const float *)nullptr, (const float *)mean, (const float *)nullptr, part, (float *)nullptr);
     DC_HIP(hipGetLastError());
     hipLaunchKernelGGL(colred_final_kernel<2>, dim3(c), dim3(EW_THREADS), 0, s, p.nchunks, c, rows, eps, part,
-                       (const float *)nullptr, invstd, (float *)nullptr);
+                       (const float *)nullptr, invstd, (float *)nullptr, (const float *)nullptr);
     DC_HIP(hipGetLastError());
     int64_t total = rows * c;
     hipLaunchKernelGGL(bn_apply_kernel, dim3(ew_blocks(total)), dim3(EW_THREADS), 0, s, rows, c, x, gamma, beta, mean,
@@ -612,20 +921,41 @@ int bn_backward(int64_t rows, int c, const float *dy, const float *x, const floa
                 const float *invstd, int accumulate, float *dx, float *dgamma, float *dbeta, void *ws, hipStream_t s) {
     if (rows <= 0 || c <= 0)
         return DC_OK;
-    ColPlan p = col_plan(rows, c);
     float *part0 = static_cast<float *>(ws);
-    float *part1 = reinterpret_cast<float *>(static_cast<char *>(ws) + align256((size_t)p.nchunks * c * sizeof(float)));
-    dim3 g1(p.nchunks, (c + CG - 1) / CG);
-    hipLaunchKernelGGL(colred_partial_kernel<2>, g1, dim3(EW_THREADS), 0, s, rows, c, p.rows_per_chunk, x, dy, mean,
-                       invstd, part0, part1);
+    float *part1 = reinterpret_cast<float *>(static_cast<char *>(ws) +
+                                             align256((size_t)col_slots(rows, c) * c * sizeof(float)));
+    const bool v4 = col4_ok(c, dy, x) && col4_ok(c, gamma, mean) && col4_ok(c, invstd, dgamma) &&
+                    col4_ok(c, dbeta, part0) && col4_ok(c, part1) && (!dx || col4_ok(c, dx));
+    int nchunks;
+    if (v4) {
+        Col4Plan p = col4_plan(rows, c);
+        hipLaunchKernelGGL(colred4_partial_kernel<2>, dim3(p.nchunks, p.blocks), dim3(EW_THREADS), 0, s, rows, c,
+                           p.rpc, p.g, p.rl_n, x, dy, mean, invstd, part0, part1);
+        nchunks = p.nchunks;
+    } else {
+        ColPlan p = col_plan(rows, c);
+        dim3 g1(p.nchunks, (c + CG - 1) / CG);
+        hipLaunchKernelGGL(colred_partial_kernel<2>, g1, dim3(EW_THREADS), 0, s, rows, c, p.rows_per_chunk, x, dy,
+                           mean, invstd, part0, part1);
+        nchunks = p.nchunks;
+    }
     DC_HIP(hipGetLastError());
-    hipLaunchKernelGGL(colred_final_kernel<3>, dim3(c), dim3(EW_THREADS), 0, s, p.nchunks, c, rows, 0.f, part0,
-                       (const float *)part1, dbeta, dgamma);
+    hipLaunchKernelGGL(colred_final_kernel<3>, dim3(c), dim3(EW_THREADS), 0, s, nchunks, c, rows, 0.f, part0,
+                       (const float *)part1, dbeta, dgamma, (const float *)nullptr);
     DC_HIP(hipGetLastError());
     if (dx) {
-        int64_t total = rows * c;
-        hipLaunchKernelGGL(bn_bwd_apply_kernel, dim3(ew_blocks(total)), dim3(EW_THREADS), 0, s, rows, c, dy, x, gamma,
-                           mean, invstd, dgamma, dbeta, accumulate, dx);
+        if (v4) {
+            const int64_t n4 = rows * c / 4;
+            hipLaunchKernelGGL(bn_bwd_apply4_kernel, dim3(bn4_blocks(n4, c / 4)), dim3(EW_THREADS), 0, s, n4, c / 4,
+                               rows, reinterpret_cast<const float4 *>(dy), reinterpret_cast<const float4 *>(x),
+                               reinterpret_cast<const float4 *>(gamma), reinterpret_cast<const float4 *>(mean),
+                               reinterpret_cast<const float4 *>(invstd), reinterpret_cast<const float4 *>(dgamma),
+                               reinterpret_cast<const float4 *>(dbeta), accumulate, reinterpret_cast<float4 *>(dx));
+        } else {
+            int64_t total = rows * c;
+            hipLaunchKernelGGL(bn_bwd_apply_kernel, dim3(ew_blocks(total)), dim3(EW_THREADS), 0, s, rows, c, dy, x,
+                               gamma, mean, invstd, dgamma, dbeta, accumulate, dx);
+        }
         DC_HIP(hipGetLastError());
     }
     return DC_OK;

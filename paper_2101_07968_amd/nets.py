@@ -184,6 +184,25 @@ def build(name):
     return BUILDERS[name]()
 
 
+def shapes(ops, hwc):
+    """(h, w, c) of every tensor: the input, then each op's output (FC and GAP give 1 x 1)."""
+    out = [(hwc[0], hwc[1], hwc[2])]
+    for (kind, _layer, src, other, out_ch, r, s, stride, pad, bias, in2, in3) in ops:
+        h, w, c = out[src]
+        if kind == DC_OP_CONCAT:
+            out.append((h, w, sum(out[t][2] for t in (src, other, in2, in3) if t >= 0)))
+        elif kind in (DC_OP_CONV, DC_OP_MAXPOOL):
+            out.append(((h + 2 * pad - r) // stride + 1, (w + 2 * pad - s) // stride + 1,
+                        out_ch if kind == DC_OP_CONV else c))
+        elif kind == DC_OP_FC:
+            out.append((1, 1, out_ch))
+        elif kind == DC_OP_GAP:
+            out.append((1, 1, c))
+        else:
+            out.append((h, w, c))
+    return out
+
+
 def param_specs(ops, hwc):
     """Initialisation kinds of the parameter tensors in parameter-server order.
 
@@ -191,55 +210,32 @@ def param_specs(ops, hwc):
     biases and BN beta, ones for BN gamma - the argument list of
     ``synth.cnn_inputs``.
     """
-    shapes = [(hwc[0], hwc[1], hwc[2])]
+    shp = shapes(ops, hwc)
     specs = []
     for (kind, _layer, src, other, out_ch, r, s, stride, pad, bias, in2, in3) in ops:
-        h, w, c = shapes[src]
-        if kind == DC_OP_CONCAT:
-            shapes.append((h, w, sum(shapes[t][2] for t in (src, other, in2, in3) if t >= 0)))
-            continue
+        h, w, c = shp[src]
         if kind == DC_OP_CONV:
             specs.append(("he", out_ch * r * s * c, r * s * c))
             if bias:
                 specs.append(("zeros", out_ch))
-            shapes.append(((h + 2 * pad - r) // stride + 1, (w + 2 * pad - s) // stride + 1, out_ch))
         elif kind == DC_OP_FC:
             specs.append(("he", out_ch * h * w * c, h * w * c))
             if bias:
                 specs.append(("zeros", out_ch))
-            shapes.append((1, 1, out_ch))
         elif kind == DC_OP_BN:
             specs.append(("ones", c))
             specs.append(("zeros", c))
-            shapes.append((h, w, c))
-        elif kind == DC_OP_MAXPOOL:
-            shapes.append(((h + 2 * pad - r) // stride + 1, (w + 2 * pad - s) // stride + 1, c))
-        elif kind == DC_OP_GAP:
-            shapes.append((1, 1, c))
-        else:
-            shapes.append((h, w, c))
     return specs
 
 
 def conv_geoms(ops, hwc, batch):
     """(op index, dc_conv_shape fields, reads_input_batch) of every conv / FC op; FC as a 1x1 conv."""
-    shapes = [(hwc[0], hwc[1], hwc[2])]
+    shp = shapes(ops, hwc)
     out = []
     for i, (kind, _layer, src, other, out_ch, r, s, stride, pad, bias, in2, in3) in enumerate(ops):
-        h, w, c = shapes[src]
-        if kind == DC_OP_CONCAT:
-            shapes.append((h, w, sum(shapes[t][2] for t in (src, other, in2, in3) if t >= 0)))
-            continue
+        h, w, c = shp[src]
         if kind == DC_OP_CONV:
             out.append((i, (batch, h, w, c, out_ch, r, s, stride, pad), src == 0))
-            shapes.append(((h + 2 * pad - r) // stride + 1, (w + 2 * pad - s) // stride + 1, out_ch))
         elif kind == DC_OP_FC:
             out.append((i, (batch, 1, 1, h * w * c, out_ch, 1, 1, 1, 0), src == 0))
-            shapes.append((1, 1, out_ch))
-        elif kind == DC_OP_MAXPOOL:
-            shapes.append(((h + 2 * pad - r) // stride + 1, (w + 2 * pad - s) // stride + 1, c))
-        elif kind == DC_OP_GAP:
-            shapes.append((1, 1, c))
-        else:
-            shapes.append((h, w, c))
     return out

@@ -200,7 +200,7 @@ def test_relu_add_copy(n, offset):
 
 
 POOLS = [(2, 8, 8, 5, 2, 2, 0), (3, 13, 13, 16, 3, 2, 0), (2, 12, 12, 7, 3, 2, 1), (32, 55, 55, 64, 3, 2, 0),
-         (64, 112, 112, 64, 3, 2, 1), (32, 224, 224, 64, 2, 2, 0)]
+         (64, 112, 112, 64, 3, 2, 1), (32, 224, 224, 64, 2, 2, 0), (2, 9, 9, 12, 3, 1, 1), (3, 14, 14, 4, 3, 2, 1)]
 
 
 @pytest.mark.parametrize("cfg", POOLS, ids=[str(p) for p in POOLS])
@@ -221,6 +221,11 @@ def test_maxpool(cfg):
     np.testing.assert_array_equal(host(arg).astype(np.int32), arg_ref)
     dx_ref = OC.maxpool_backward(dy, arg_ref, x.shape, r, r, st, pad)
     assert rel_err(host(dx), dx_ref) <= 1e-7
+    # accumulating into an existing gradient
+    acc0 = synth.random_tensor(13, (n, h, w, c))
+    dxa = dev(acc0)
+    D.call("dc_maxpool_backward", ctypes.byref(sh), dyd.data_ptr(), arg.data_ptr(), 1, dxa.data_ptr(), stream())
+    assert rel_err(host(dxa), dx_ref + acc0) <= 1e-6
 
 
 @pytest.mark.parametrize("cfg", [(3, 4, 4, 10), (128, 4, 4, 512), (64, 7, 7, 2048)])
@@ -237,14 +242,18 @@ def test_gap(cfg):
     assert rel_err(host(dx), np.broadcast_to(dy.astype(np.float64) / (h * w), x.shape)) <= 1e-7
 
 
-BNS = [(2, 5, 5, 64), (4, 9, 9, 130), (128, 32, 32, 64), (64, 112, 112, 64), (64, 7, 7, 2048), (1, 7, 7, 512)]
+BNS = [(2, 5, 5, 64, 0.5), (4, 9, 9, 130, 0.5), (128, 32, 32, 64, 0.5), (64, 112, 112, 64, 0.5),
+       (64, 7, 7, 2048, 0.5), (1, 7, 7, 512, 0.5), (3, 5, 5, 4, 0.5), (2, 11, 13, 12, 0.5), (5, 7, 7, 208, 0.5),
+       (32, 28, 28, 96, 300.0), (16, 56, 56, 64, -1000.0)]
 
 
 @pytest.mark.parametrize("cfg", BNS, ids=[str(b) for b in BNS])
 def test_batchnorm(cfg):
-    n, h, w, c = cfg
+    """Includes channel counts off the float4 path (130) and inputs whose mean is far
+    larger than their spread (the one-pass statistics must not cancel)."""
+    n, h, w, c, mu = cfg
     rows = n * h * w
-    x = (synth.random_tensor(15, (n, h, w, c)) * 2 + 0.5).astype(np.float32)
+    x = (synth.random_tensor(15, (n, h, w, c)) * 2 + mu).astype(np.float32)
     gamma = synth.random_tensor(16, (c,))
     beta = synth.random_tensor(17, (c,))
     dy = synth.random_tensor(18, (n, h, w, c))
