@@ -38,7 +38,8 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
-    ap.add_argument("--workload", default="vgg16", choices=["tiny", "alexnet", "resnet18", "vgg16", "resnet50", "googlenet"])
+    ap.add_argument("--workload", default="vgg16", choices=["tiny", "alexnet", "resnet18", "vgg16", "resnet50", "googlenet", "vgg19",
+                                                          "resnet152"])
     ap.add_argument("--batch", type=int, default=0, help="0 = the workload's own batch")
     ap.add_argument("--link-gbps", default="100", help="emulated link in Gb/s, or 'pcie' for unpaced copies")
     ap.add_argument("--dt-emul-ms", type=float, default=0.0)

@@ -1,6 +1,6 @@
 """Network definitions for the oracle (test infrastructure only).
 
-Five synthetic workloads, written independently of the product library's own
+The synthetic workloads, written independently of the product library's own
 definitions.  A network is a list of operations in forward order; tensor 0 is
 the input batch and tensor i+1 is the output of operation i.
 
@@ -82,11 +82,9 @@ def alexnet():
     return {"name": "alexnet", "ops": b.ops, "hwc": (224, 224, 3), "classes": 1000}
 
 
-def vgg16():
-    """VGG-16: 13 conv3x3 pad 1 with ReLU, five 2x2 max-pools, FC 25088->4096->4096->1000."""
+def _vgg(name, cfg):
     b = _Builder()
     t = 0
-    cfg = [64, 64, "M", 128, 128, "M", 256, 256, 256, "M", 512, 512, 512, "M", 512, 512, 512, "M"]
     for v in cfg:
         if v == "M":
             t = b.add("maxpool", t, r=2, s=2, stride=2, pad=0)
@@ -99,7 +97,18 @@ def vgg16():
         t = b.fc(t, out)
         if relu:
             t = b.add("relu", t)
-    return {"name": "vgg16", "ops": b.ops, "hwc": (224, 224, 3), "classes": 1000}
+    return {"name": name, "ops": b.ops, "hwc": (224, 224, 3), "classes": 1000}
+
+
+def vgg16():
+    """VGG-16 (configuration D): 13 conv3x3 pad 1 with ReLU, five 2x2 max-pools, FC 25088->4096->4096->1000."""
+    return _vgg("vgg16", [64, 64, "M", 128, 128, "M", 256, 256, 256, "M", 512, 512, 512, "M", 512, 512, 512, "M"])
+
+
+def vgg19():
+    """VGG-19 (configuration E): 16 conv3x3, otherwise as VGG-16."""
+    return _vgg("vgg19", [64, 64, "M", 128, 128, "M", 256, 256, 256, 256, "M", 512, 512, 512, 512, "M",
+                          512, 512, 512, 512, "M"])
 
 
 def resnet18_small():
@@ -134,8 +143,7 @@ def resnet18_small():
     return {"name": "resnet18", "ops": b.ops, "hwc": (32, 32, 3), "classes": 10}
 
 
-def resnet50():
-    """ResNet-50 (stride on the 3x3 conv of a bottleneck, projection in each stage's first block)."""
+def _bottleneck_resnet(name, stages):
     b = _Builder()
     b.new_layer()
     t = b.conv(0, 64, 7, stride=2, pad=3, bias=False)
@@ -143,7 +151,7 @@ def resnet50():
     t = b.add("relu", t)
     t = b.add("maxpool", t, r=3, s=3, stride=2, pad=1)
     cin = 64
-    for width, blocks, first_stride in ((64, 3, 1), (128, 4, 2), (256, 6, 2), (512, 3, 2)):
+    for width, blocks, first_stride in zip((64, 128, 256, 512), stages, (1, 2, 2, 2)):
         cout = 4 * width
         for blk in range(blocks):
             st = first_stride if blk == 0 else 1
@@ -169,7 +177,17 @@ def resnet50():
     t = b.add("gap", t)
     b.new_layer()
     b.fc(t, 1000)
-    return {"name": "resnet50", "ops": b.ops, "hwc": (224, 224, 3), "classes": 1000}
+    return {"name": name, "ops": b.ops, "hwc": (224, 224, 3), "classes": 1000}
+
+
+def resnet50():
+    """ResNet-50 (stride on the 3x3 conv of a bottleneck, projection in each stage's first block)."""
+    return _bottleneck_resnet("resnet50", (3, 4, 6, 3))
+
+
+def resnet152():
+    """ResNet-152: bottleneck stages of 3, 8, 36 and 3 blocks, otherwise as ResNet-50."""
+    return _bottleneck_resnet("resnet152", (3, 8, 36, 3))
 
 
 def googlenet():
@@ -216,7 +234,7 @@ def googlenet():
 
 
 NETS = {"tiny": tiny, "alexnet": alexnet, "resnet18": resnet18_small, "vgg16": vgg16, "resnet50": resnet50,
-        "googlenet": googlenet}
+        "googlenet": googlenet, "vgg19": vgg19, "resnet152": resnet152}
 
 
 def get(name):

@@ -1,4 +1,4 @@
-"""The five synthetic workloads as dc_op_desc lists for dc_model_create.
+"""The synthetic workloads as dc_op_desc lists for dc_model_create.
 
 Each builder returns ``(ops, hwc, classes)``: ``ops`` is a list of 12-tuples
 ``(kind, layer, in0, in1, out_ch, r, s, stride, pad, bias, in2, in3)`` in forward order
@@ -14,6 +14,8 @@ Workloads (inputs NHWC; batch and link are chosen by the caller):
   vgg16     13 conv3x3 + 3 FC, 224x224                                                        (L=16)
   resnet50  bottleneck [3,4,6,3], stride on the 3x3 conv, FC 2048->1000                        (L=50)
   googlenet Inception v1 (5x5 third branch, no LRN / dropout / auxiliary heads), FC 1024->1000  (L=22)
+  vgg19     16 conv3x3 + 3 FC, 224x224                                                        (L=19)
+  resnet152 bottleneck [3,8,36,3], as resnet50                                                (L=152)
 """
 from __future__ import annotations
 
@@ -79,10 +81,10 @@ def alexnet():
     return n.ops, (224, 224, 3), 1000
 
 
-def vgg16():
+def _vgg(reps_per_stage):
     n = NetBuilder()
     t = 0
-    for width, reps in ((64, 2), (128, 2), (256, 3), (512, 3), (512, 3)):
+    for width, reps in zip((64, 128, 256, 512, 512), reps_per_stage):
         for _ in range(reps):
             t = n.relu(n.conv(t, width, 3, pad=1))
         t = n.maxpool(t, 2, 2)
@@ -90,6 +92,14 @@ def vgg16():
     t = n.relu(n.fc(t, 4096))
     n.fc(t, 1000)
     return n.ops, (224, 224, 3), 1000
+
+
+def vgg16():
+    return _vgg((2, 2, 3, 3, 3))
+
+
+def vgg19():
+    return _vgg((2, 2, 4, 4, 4))
 
 
 def _basic_block(n, x, cin, cout, stride):
@@ -125,16 +135,24 @@ def _bottleneck(n, x, width, stride, project):
     return n.relu(n.add(u, short))
 
 
-def resnet50():
+def _resnet_bottleneck(blocks_per_stage):
     n = NetBuilder()
     t = n.relu(n.bn(n.conv(0, 64, 7, stride=2, pad=3, bias=False)))
     t = n.maxpool(t, 3, 2, pad=1)
-    for width, blocks, stride in ((64, 3, 1), (128, 4, 2), (256, 6, 2), (512, 3, 2)):
+    for width, blocks, stride in zip((64, 128, 256, 512), blocks_per_stage, (1, 2, 2, 2)):
         for i in range(blocks):
             t = _bottleneck(n, t, width, stride if i == 0 else 1, i == 0)
     t = n.gap(t)
     n.fc(t, 1000)
     return n.ops, (224, 224, 3), 1000
+
+
+def resnet50():
+    return _resnet_bottleneck((3, 4, 6, 3))
+
+
+def resnet152():
+    return _resnet_bottleneck((3, 8, 36, 3))
 
 
 def _inception(n, x, c1, r3, c3, r5, c5, pool_proj):
@@ -164,7 +182,8 @@ def googlenet():
     return n.ops, (224, 224, 3), 1000
 
 
-BUILDERS = {"tiny": tiny, "alexnet": alexnet, "resnet18": resnet18, "vgg16": vgg16, "resnet50": resnet50, "googlenet": googlenet}
+BUILDERS = {"tiny": tiny, "alexnet": alexnet, "resnet18": resnet18, "vgg16": vgg16, "resnet50": resnet50,
+            "googlenet": googlenet, "vgg19": vgg19, "resnet152": resnet152}
 
 # The workloads' batch size, emulated link rate (bytes/s; 1 Gb/s = 1.25e8 B/s),
 # input seed and SGD learning rate (1e-3 for the two networks without
@@ -177,6 +196,8 @@ WORKLOADS = {
     "vgg16": {"batch": 32, "link": 10e9 / 8, "seed": 3, "lr": 1e-3},
     "resnet50": {"batch": 64, "link": 10e9 / 8, "seed": 4, "lr": 1e-2},
     "googlenet": {"batch": 32, "link": 10e9 / 8, "seed": 5, "lr": 1e-2},
+    "vgg19": {"batch": 32, "link": 10e9 / 8, "seed": 6, "lr": 1e-3},
+    "resnet152": {"batch": 32, "link": 10e9 / 8, "seed": 7, "lr": 1e-2},
 }
 
 

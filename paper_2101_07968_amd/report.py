@@ -331,6 +331,8 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--only", default="tiny,alexnet,resnet18,vgg16,resnet50")
     ap.add_argument("--vgg-sweep", action="store_true", help="VGG-16 at 0.1, 1, 10, 100 Gb/s and unpaced")
+    ap.add_argument("--rate-sweep", default="", help="workload:g1,g2,... at those link rates (Gb/s), e.g. "
+                                                      "resnet152:1,5,10,25")
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--adapt", default="", help="workload for the link-change scenario, e.g. resnet50")
     ap.add_argument("--adapt-rates", default="100,10,100", help="Gb/s of the successive phases")
@@ -350,6 +352,9 @@ def main():
     if a.vgg_sweep:
         cases = [c for c in cases if c[0] != "vgg16"]
         cases += [("vgg16", g * 1e9 / 8, True, 0) for g in (0.1, 1, 10, 100)] + [("vgg16", 0, False, 0)]
+    if a.rate_sweep:
+        name, gs = a.rate_sweep.split(":")
+        cases += [(name, float(g) * 1e9 / 8, True, 0) for g in gs.split(",")]
     if a.dt_sweep:
         cases = [("vgg16", rate, paced, int(dt * 1e6)) for rate, paced in ((100e9 / 8, True), (0, False))
                  for dt in (0, 1, 10)]

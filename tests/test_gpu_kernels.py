@@ -102,10 +102,10 @@ def test_conv_small(shape, variant):
 
 
 def _full_size_geoms():
-    """Every distinct conv / FC geometry of the five workloads at their own batch."""
+    """Every distinct conv / FC geometry of the workloads at their own batch."""
     seen, out = set(), []
     for name, batch in (("tiny", 4), ("alexnet", 32), ("resnet18", 128), ("vgg16", 32), ("resnet50", 64),
-                        ("googlenet", 32)):
+                        ("googlenet", 32), ("vgg19", 32), ("resnet152", 32)):
         net = OC.Net(ON.get(name), batch)
         for i, op in enumerate(net.ops):
             if op["op"] not in ("conv", "fc"):

@@ -52,7 +52,8 @@ def plans_for(L, seed=0):
     }
 
 
-PARITY = [("tiny", 4), ("alexnet", 2), ("resnet18", 8), ("resnet50", 2), ("vgg16", 1), ("googlenet", 2)]
+PARITY = [("tiny", 4), ("alexnet", 2), ("resnet18", 8), ("resnet50", 2), ("vgg16", 1), ("googlenet", 2),
+          ("vgg19", 1), ("resnet152", 2)]
 
 
 def fp32_spread(spec, onet, x, y, params, g_ref):
@@ -143,7 +144,7 @@ def test_results_do_not_depend_on_segmentation(name, batch):
 
 
 FULL = [("tiny", 4, 0), ("alexnet", 32, 1), ("resnet18", 128, 2), ("vgg16", 32, 3), ("resnet50", 64, 4),
-        ("googlenet", 32, 5)]
+        ("googlenet", 32, 5), ("vgg19", 32, 6), ("resnet152", 32, 7)]
 
 
 @pytest.mark.parametrize("name,batch,seed", FULL, ids=[f"{n}-b{b}" for n, b, _ in FULL])

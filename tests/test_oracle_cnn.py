@@ -234,12 +234,14 @@ def test_sgd_closed_form():
 
 
 @pytest.mark.parametrize("name,count", [("tiny", 67642), ("alexnet", 61100840), ("resnet18", 11173962),
-                                        ("vgg16", 138357544), ("resnet50", 25557032), ("googlenet", 6998552)])
+                                        ("vgg16", 138357544), ("resnet50", 25557032), ("googlenet", 6998552),
+                                        ("vgg19", 143667240), ("resnet152", 60192808)])
 def test_parameter_counts(name, count):
     net = cnn.Net(nets.get(name), 1)
     assert net.n_params == count
     assert sum(c for _, c in net.layer_ranges.values()) == count
-    assert {"tiny": 4, "alexnet": 8, "resnet18": 18, "vgg16": 16, "resnet50": 50, "googlenet": 22}[name] == net.L
+    assert {"tiny": 4, "alexnet": 8, "resnet18": 18, "vgg16": 16, "resnet50": 50, "googlenet": 22, "vgg19": 19,
+            "resnet152": 152}[name] == net.L
 
 
 def _torch_loss(spec, net, x, y, p):
