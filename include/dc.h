@@ -184,7 +184,9 @@ typedef struct dc_profile_t {
  * event intervals on `stream`; dt and the host-interface rate come from a
  * least-squares fit t = a + bytes / rate over probe copies; pt = gt =
  * bytes / rate at the emulated rate when paced, the fitted one otherwise;
- * dt = a + dt_emul_ns.  Pulls all parameters to the device first.
+ * dt = a + h + dt_emul_ns, where h is the measured latency of the
+ * cross-stream handoff every segment adds (compute waiting for a pull, a
+ * push waiting for the backward).  Pulls all parameters to the device first.
  * Errors: DC_EINVAL (L or batch mismatch, reps < 1), DC_ESTATE, DC_EHIP.
  */
 int dc_profile(dc_model *m, const dc_batch *b, const dc_link *link, int reps, void *stream,

@@ -397,6 +397,35 @@ int probe_link(dc_model *m, const dc_link *link, bool h2d, const std::vector<siz
     return DC_OK;
 }
 
+// Handoff between streams: at a segment boundary one stream waits for an
+// event of another (the forward waits for a pull, a push for the backward).
+// The time from the awaited event to the waiting stream's next event is a
+// fixed cost of every segment, which the cost model counts in Delta t with
+// the transfer's own overhead.  Mean over reps of both directions, in ns.
+int probe_handoff(dc_model *m, hipStream_t cs, int reps, double *ns) {
+    double sum = 0;
+    int n = 0;
+    hipEvent_t e1 = m->ev_push_start[0], e2 = m->ev_push_done[0];
+    for (int r = 0; r <= reps; ++r) { // r = 0 warms up
+        for (int dir = 0; dir < 2; ++dir) {
+            hipStream_t a = dir == 0 ? m->pull_s : cs, b = dir == 0 ? cs : m->push_s;
+            DC_TRY(pace_mark(m->slots() + 2 * m->L, a));
+            DC_HIP(hipEventRecord(e1, a));
+            DC_HIP(hipStreamWaitEvent(b, e1, 0));
+            DC_HIP(hipEventRecord(e2, b));
+            DC_HIP(hipEventSynchronize(e2));
+            if (r == 0)
+                continue;
+            int64_t d;
+            DC_TRY(elapsed_ns(e1, e2, &d));
+            sum += (double)std::max<int64_t>(d, 0);
+            ++n;
+        }
+    }
+    *ns = n ? sum / n : 0.0;
+    return DC_OK;
+}
+
 } // namespace
 
 extern "C" int dc_profile(dc_model *m, const dc_batch *b, const dc_link *link, int reps, void *stream,
@@ -479,6 +508,8 @@ extern "C" int dc_profile(dc_model *m, const dc_batch *b, const dc_link *link, i
         out->pt_ns[l - 1] = (int64_t)llround(bytes * b_h2d);
         out->gt_ns[l - 1] = (int64_t)llround(bytes * b_d2h);
     }
-    out->dt_ns = std::max<int64_t>(0, (int64_t)llround(0.5 * (a_h2d + a_d2h)));
+    double handoff = 0;
+    DC_TRY(probe_handoff(m, cs, 5, &handoff));
+    out->dt_ns = std::max<int64_t>(0, (int64_t)llround(0.5 * (a_h2d + a_d2h) + handoff));
     return DC_OK;
 }
