@@ -48,6 +48,7 @@ struct GemmPlan {
     int splits;           // split-K factor (1 = no split)
     int kt_per_split;     // K stages (of depth kt) per split
     bool av, bv;          // float4 operand loads possible
+    bool tu;              // lean address mode: FWD C % 16 == 0; DGRAD K % 16 == 0, C % 4 == 0; WGRAD K, C % 4 == 0, Q >= 16
     int cpad;             // FWD / WGRAD with C % 4 != 0: padded channel count, else 0
     size_t pad_x_off;     // workspace offsets of the padded x and of the padded w (FWD) or dw (WGRAD)
     size_t pad_w_off;

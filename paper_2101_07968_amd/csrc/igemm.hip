@@ -75,6 +75,7 @@ struct Args {
     float *partial;         // split-K scratch
     int relu, accumulate;
     FDiv fC, fS, fK, fQ, fPQ;
+    unsigned a_bytes, b_bytes; // sizes of A and B (lean mode: each below 2^31)
 };
 
 // Per-phase geometry of dgrad (stride residues rh, rw).
@@ -105,6 +106,17 @@ __device__ __forceinline__ Phase make_phase(const Args &a, int z) {
 __device__ __forceinline__ float4 ld4(const float *p) { return *reinterpret_cast<const float4 *>(p); }
 __device__ __forceinline__ void st4(float *p, float4 v) { *reinterpret_cast<float4 *>(p) = v; }
 
+// Raw buffer loads for the lean address mode: a 32-bit byte offset into a
+// tensor described by base and size; an offset at or past the size reads as
+// zeros, which is how the kernel fetches padding and tails without branches.
+constexpr unsigned OOB = 0x80000000u;
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t tensor_rsrc(const float *p, unsigned bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<float *>(p), (short)0, (int)bytes, 0x00020000);
+}
+__device__ __forceinline__ float4 bld4(__amdgpu_buffer_rsrc_t r, unsigned elem_off, bool ok) {
+    return __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(r, ok ? elem_off * 4u : OOB, 0, 0));
+}
+
 // Address of output row m of a pass in its destination tensor (row-major
 // [rows][Ng] for FWD / WGRAD, the NHWC pixel of the phase for DGRAD).
 __device__ __forceinline__ size_t out_row(const Args &a, int pass, const Phase &ph, int z, int m) {
@@ -133,8 +145,19 @@ __device__ __forceinline__ float epilogue(const Args &a, int pass, float v, int 
     return v;
 }
 
-template <int PASS, int MT, int NT, int KT, bool AV, bool BV>
+// TU, the lean address mode (the host checks that every tensor has fewer
+// than 2^31 elements, so element offsets are 32-bit):
+//  * forward with C % KT == 0, dgrad with K % KT == 0 and C % 4 == 0: every K
+//    stage lies inside one filter tap, so the tap and first channel of a
+//    stage are workgroup-uniform scalars and every stage is full; a
+//    fragment's offset is its row's base offset plus a per-stage delta;
+//  * wgrad with K % 4 == 0, C % 4 == 0 and Q >= KT: every B fragment's pixel
+//    advances by KT per stage (at most one row wrap), so its (q, p), input
+//    origin and offset are carried from stage to stage with uniform
+//    increments instead of being decoded.
+template <int PASS, int MT, int NT, int KT, bool AV, bool BV, bool TU>
 __global__ __launch_bounds__(NTHR) void igemm_kernel(Args a) {
+    static_assert(!TU || (AV && BV), "the lean address mode needs float4 operands");
     constexpr bool A_KC = (PASS != PASS_WGRAD); // A tile stored [row][k]
     constexpr bool B_KC = (PASS == PASS_FWD);   // B tile stored [col][k]
     constexpr int A_LD = A_KC ? (KT + PADK) : (MT + PADR);
@@ -228,6 +251,19 @@ __global__ __launch_bounds__(NTHR) void igemm_kernel(Args a) {
             a_n[f] = a_h[f] = a_w[f] = 0;
         }
     }
+    // TU: element offset of each A fragment's (possibly padded-out) window
+    // origin, and of each B fragment's first k.
+    int a_base[FA], b_base[FB];
+    if (TU && PASS == PASS_FWD) {
+#pragma unroll
+        for (int f = 0; f < FA; ++f)
+            a_base[f] = ((a_n[f] * a.H + a_h[f]) * a.W + a_w[f]) * a.C + 4 * a_kc;
+    }
+    if (TU && PASS == PASS_DGRAD) {
+#pragma unroll
+        for (int f = 0; f < FA; ++f)
+            a_base[f] = ((a_n[f] * a.P + a_h[f]) * a.Q + a_w[f]) * a.K + 4 * a_kc;
+    }
     // B fragments: k-contiguous -> (row = idx / (KT/4), kc); n-contiguous ->
     // (krow = idx / (NT/4), nc = idx % (NT/4)).
     int b_row[FB];
@@ -247,6 +283,16 @@ __global__ __launch_bounds__(NTHR) void igemm_kernel(Args a) {
             b_kc = idx % (NT / 4);
         }
     }
+    if (TU && PASS == PASS_FWD) {
+#pragma unroll
+        for (int f = 0; f < FB; ++f)
+            b_base[f] = (tn * NT + b_row[f]) * a.Kg + 4 * b_kc;
+    }
+    if (TU && PASS == PASS_DGRAD) {
+#pragma unroll
+        for (int f = 0; f < FB; ++f)
+            b_base[f] = b_row[f] * (a.R * a.S * a.C) + tn * NT + 4 * b_kc;
+    }
     if (PASS == PASS_WGRAD) {
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
@@ -260,12 +306,96 @@ __global__ __launch_bounds__(NTHR) void igemm_kernel(Args a) {
         }
     }
 
+    // WGRAD TU: A fragment offsets (stage 0) and each B fragment's pixel
+    // state (q, p, window origin hh/ww, element offset) for its next stage.
+    int wa_off[FA];
+    int bq[FB], bp[FB], bhh[FB], bww[FB], boff[FB];
+    if (PASS == PASS_WGRAD && TU) {
+#pragma unroll
+        for (int f = 0; f < FA; ++f)
+            wa_off[f] = a_row[f] * a.K + tm * MT + 4 * a_kc;
+    }
+    auto wpix_init = [&](int kt) {
+#pragma unroll
+        for (int f = 0; f < FB; ++f) {
+            const int mp = min(kt * KT + b_row[f], max(a.Kg - 1, 0));
+            const int n = a.fPQ.div(mp);
+            const int rem = mp - n * a.P * a.Q;
+            const int pp = a.fQ.div(rem);
+            bq[f] = rem - pp * a.Q;
+            bp[f] = pp;
+            bhh[f] = pp * a.st - a.pad + b_r[0];
+            bww[f] = bq[f] * a.st - a.pad + b_s[0];
+            boff[f] = ((n * a.H + bhh[f]) * a.W + bww[f]) * a.C + b_c[0];
+        }
+    };
+    auto wpix_next = [&]() {
+        const int row_step = (a.st * a.W - a.Q * a.st) * a.C, img_step = (a.H - a.P * a.st) * a.W * a.C;
+#pragma unroll
+        for (int f = 0; f < FB; ++f) {
+            bq[f] += KT;
+            bww[f] += KT * a.st;
+            boff[f] += KT * a.st * a.C;
+            if (bq[f] >= a.Q) { // Q >= KT: at most one row wrap per stage
+                bq[f] -= a.Q;
+                bww[f] -= a.Q * a.st;
+                ++bp[f];
+                bhh[f] += a.st;
+                boff[f] += row_step;
+                if (bp[f] >= a.P) {
+                    bp[f] -= a.P;
+                    bhh[f] -= a.P * a.st;
+                    boff[f] += img_step;
+                }
+            }
+        }
+    };
+
     float4 ra[FA], rb[FB];
+    const __amdgpu_buffer_rsrc_t rs_a = tensor_rsrc(a.A, a.a_bytes), rs_b = tensor_rsrc(a.B, a.b_bytes);
+
+    // TU stage cursor, uniform over the workgroup: first channel c0 of the
+    // next stage to load and its tap, (r, s) for the forward pass or (tr, ts)
+    // for dgrad.  Set once by division, then advanced one stage at a time.
+    int cur_c0 = 0, cur_t1 = 0, cur_t2 = 0;
+    auto cursor_init = [&](int kt) {
+        const int kbase = kt * KT;
+        if (PASS == PASS_FWD) {
+            const int tap = a.fC.div(kbase);
+            cur_c0 = kbase - tap * a.C;
+            cur_t1 = a.fS.div(tap);
+            cur_t2 = tap - cur_t1 * a.S;
+        } else {
+            const int tt = a.fK.div(kbase);
+            cur_c0 = kbase - tt * a.K;
+            cur_t1 = ph.St ? tt / ph.St : 0;
+            cur_t2 = tt - cur_t1 * ph.St;
+        }
+    };
+    auto cursor_next = [&]() {
+        cur_c0 += KT;
+        if (cur_c0 == (PASS == PASS_FWD ? a.C : a.K)) {
+            cur_c0 = 0;
+            if (++cur_t2 == (PASS == PASS_FWD ? a.S : ph.St)) {
+                cur_t2 = 0;
+                ++cur_t1;
+            }
+        }
+    };
 
     // ------------------------------------------------ global -> registers
     auto load_a = [&](int kt) {
         const int kbase = kt * KT;
-        if (PASS == PASS_FWD) {
+        if (PASS == PASS_FWD && TU) {
+            const int r = cur_t1, s = cur_t2;
+            const int delta = (r * a.W + s) * a.C + cur_c0;
+#pragma unroll
+            for (int f = 0; f < FA; ++f) {
+                const int h = a_h[f] + r, w = a_w[f] + s;
+                const bool ok = a_ok[f] && (unsigned)h < (unsigned)a.H && (unsigned)w < (unsigned)a.W;
+                ra[f] = bld4(rs_a, (unsigned)(a_base[f] + delta), ok);
+            }
+        } else if (PASS == PASS_FWD) {
             if (AV) {
                 int kk = kbase + 4 * a_kc;
                 bool kok = kk < Kg;
@@ -303,6 +433,15 @@ __global__ __launch_bounds__(NTHR) void igemm_kernel(Args a) {
                 for (int f = 0; f < FA; ++f)
                     ra[f] = make_float4(v[0][f], v[1][f], v[2][f], v[3][f]);
             }
+        } else if (PASS == PASS_DGRAD && TU) {
+            const int tr = cur_t1, ts = cur_t2;
+            const int delta = cur_c0 - (tr * a.Q + ts) * a.K;
+#pragma unroll
+            for (int f = 0; f < FA; ++f) {
+                const int p = a_h[f] - tr, q = a_w[f] - ts;
+                const bool ok = a_ok[f] && (unsigned)p < (unsigned)a.P && (unsigned)q < (unsigned)a.Q;
+                ra[f] = bld4(rs_a, (unsigned)(a_base[f] + delta), ok);
+            }
         } else if (PASS == PASS_DGRAD) {
             // kk = (tr, ts, k) with k fastest
             float v[4][FA];
@@ -333,6 +472,13 @@ __global__ __launch_bounds__(NTHR) void igemm_kernel(Args a) {
                 for (int f = 0; f < FA; ++f)
                     ra[f] = make_float4(v[0][f], v[1][f], v[2][f], v[3][f]);
             }
+        } else if (PASS == PASS_WGRAD && TU) {
+            const bool kok = tm * MT + 4 * a_kc < a.M;
+#pragma unroll
+            for (int f = 0; f < FA; ++f) {
+                const bool ok = kok && kbase + a_row[f] < Kg;
+                ra[f] = bld4(rs_a, (unsigned)(wa_off[f] + kbase * a.K), ok);
+            }
         } else { // WGRAD: A = dY^T, rows are output channels (contiguous), k = pixel
 #pragma unroll
             for (int f = 0; f < FA; ++f) {
@@ -355,7 +501,13 @@ __global__ __launch_bounds__(NTHR) void igemm_kernel(Args a) {
 
     auto load_b = [&](int kt) {
         const int kbase = kt * KT;
-        if (PASS == PASS_FWD) { // B = W[k][kk], k-contiguous
+        if (PASS == PASS_FWD && TU) {
+#pragma unroll
+            for (int f = 0; f < FB; ++f) {
+                const bool jok = tn * NT + b_row[f] < a.Ng;
+                rb[f] = bld4(rs_b, (unsigned)(b_base[f] + kbase), jok);
+            }
+        } else if (PASS == PASS_FWD) { // B = W[k][kk], k-contiguous
 #pragma unroll
             for (int f = 0; f < FB; ++f) {
                 int j = tn * NT + b_row[f];
@@ -372,6 +524,13 @@ __global__ __launch_bounds__(NTHR) void igemm_kernel(Args a) {
                     rb[f] = make_float4(v0, v1, v2, v3);
                 }
             }
+        } else if (PASS == PASS_DGRAD && TU) {
+            const int r = ph.r0 + a.st * cur_t1, s = ph.s0 + a.st * cur_t2;
+            const int delta = cur_c0 * (a.R * a.S * a.C) + (r * a.S + s) * a.C;
+            const bool cok = tn * NT + 4 * b_kc < a.C;
+#pragma unroll
+            for (int f = 0; f < FB; ++f)
+                rb[f] = bld4(rs_b, (unsigned)(b_base[f] + delta), cok);
         } else if (PASS == PASS_DGRAD) { // B[kk][c] = W[k][r][s][c], c contiguous
 #pragma unroll
             for (int f = 0; f < FB; ++f) {
@@ -394,6 +553,13 @@ __global__ __launch_bounds__(NTHR) void igemm_kernel(Args a) {
                     float v3 = (kok && c + 3 < a.C) ? src[3] : 0.f;
                     rb[f] = make_float4(v0, v1, v2, v3);
                 }
+            }
+        } else if (PASS == PASS_WGRAD && TU) {
+#pragma unroll
+            for (int f = 0; f < FB; ++f) {
+                const bool ok = b_cok[0] && kbase + b_row[f] < Kg && (unsigned)bhh[f] < (unsigned)a.H &&
+                                (unsigned)bww[f] < (unsigned)a.W;
+                rb[f] = bld4(rs_b, (unsigned)boff[f], ok);
             }
         } else { // WGRAD: B[pixel][kk] = X~, c contiguous within a tap
 #pragma unroll
@@ -505,8 +671,16 @@ __global__ __launch_bounds__(NTHR) void igemm_kernel(Args a) {
     // ------------------------------------------------ pipeline
     int buf = 0;
     if (nkt > 0) {
+        if (TU && PASS != PASS_WGRAD)
+            cursor_init(kt0);
+        if (TU && PASS == PASS_WGRAD)
+            wpix_init(kt0);
         load_a(kt0);
         load_b(kt0);
+        if (TU && PASS != PASS_WGRAD)
+            cursor_next();
+        if (TU && PASS == PASS_WGRAD)
+            wpix_next();
         store(0);
     }
     __syncthreads();
@@ -515,6 +689,10 @@ __global__ __launch_bounds__(NTHR) void igemm_kernel(Args a) {
         if (more) {
             load_a(kt0 + it + 1);
             load_b(kt0 + it + 1);
+            if (TU && PASS != PASS_WGRAD)
+                cursor_next();
+            if (TU && PASS == PASS_WGRAD)
+                wpix_next();
         }
         compute(buf);
         if (more)
@@ -669,13 +847,17 @@ int unpad_channels(const float *in, float *out, int64_t rows, int c, int cp, hip
     return DC_OK;
 }
 
-template <int PASS, int MT, int NT, int KT, bool AV, bool BV>
+template <int PASS, int MT, int NT, int KT, bool AV, bool BV, bool TU = false>
 void launch_t(const Args &a, int grid_x, hipStream_t s) {
-    hipLaunchKernelGGL((igemm_kernel<PASS, MT, NT, KT, AV, BV>), dim3(grid_x), dim3(NTHR), 0, s, a);
+    hipLaunchKernelGGL((igemm_kernel<PASS, MT, NT, KT, AV, BV, TU>), dim3(grid_x), dim3(NTHR), 0, s, a);
 }
 
 template <int PASS, int MT, int NT, int KT>
-void launch_v(const Args &a, bool av, bool bv, int grid_x, hipStream_t s) {
+void launch_v(const Args &a, bool av, bool bv, bool tu, int grid_x, hipStream_t s) {
+    if (tu) {
+        launch_t<PASS, MT, NT, KT, true, true, true>(a, grid_x, s);
+        return;
+    }
     if (av && bv)
         launch_t<PASS, MT, NT, KT, true, true>(a, grid_x, s);
     else if (av)
@@ -689,13 +871,13 @@ void launch_v(const Args &a, bool av, bool bv, int grid_x, hipStream_t s) {
 template <int PASS, int KT>
 void launch_k(const Args &a, const GemmPlan &pl, int grid_x, hipStream_t s) {
     if (pl.mt == 128 && pl.nt == 128)
-        launch_v<PASS, 128, 128, KT>(a, pl.av, pl.bv, grid_x, s);
+        launch_v<PASS, 128, 128, KT>(a, pl.av, pl.bv, pl.tu, grid_x, s);
     else if (pl.mt == 128 && pl.nt == 64)
-        launch_v<PASS, 128, 64, KT>(a, pl.av, pl.bv, grid_x, s);
+        launch_v<PASS, 128, 64, KT>(a, pl.av, pl.bv, pl.tu, grid_x, s);
     else if (pl.mt == 64 && pl.nt == 128)
-        launch_v<PASS, 64, 128, KT>(a, pl.av, pl.bv, grid_x, s);
+        launch_v<PASS, 64, 128, KT>(a, pl.av, pl.bv, pl.tu, grid_x, s);
     else
-        launch_v<PASS, 64, 64, KT>(a, pl.av, pl.bv, grid_x, s);
+        launch_v<PASS, 64, 64, KT>(a, pl.av, pl.bv, pl.tu, grid_x, s);
 }
 
 template <int PASS>
@@ -712,6 +894,11 @@ Args make_args(const ConvGeom &g, const GemmPlan &pl) {
     a.splits = pl.splits; a.kt_per_split = pl.kt_per_split; a.phases = pl.phases;
     a.fC = make_fdiv(g.C); a.fS = make_fdiv(g.S); a.fK = make_fdiv(g.K);
     a.fQ = make_fdiv(g.Q); a.fPQ = make_fdiv(g.P * g.Q);
+    const int64_t x_el = (int64_t)g.N * g.H * g.W * g.C, y_el = (int64_t)g.N * g.P * g.Q * g.K,
+                  w_el = (int64_t)g.K * g.R * g.S * g.C;
+    const int64_t a_el = pl.pass == PASS_FWD ? x_el : y_el, b_el = pl.pass == PASS_WGRAD ? x_el : w_el;
+    a.a_bytes = (unsigned)std::min<int64_t>(4 * a_el, OOB);
+    a.b_bytes = (unsigned)std::min<int64_t>(4 * b_el, OOB);
     return a;
 }
 
@@ -783,6 +970,7 @@ static GemmPlan plan_core(const ConvGeom &g, int pass) {
         pl.M = g.N * g.P * g.Q; pl.Ng = g.K; pl.Kg = g.R * g.S * g.C;
         pl.av = g.C % 4 == 0;
         pl.bv = (g.R * g.S * g.C) % 4 == 0;
+        pl.tu = g.C % 16 == 0;
     } else if (pass == PASS_DGRAD) {
         pl.phases = g.st * g.st;
         int hh = (g.H + g.st - 1) / g.st, wh = (g.W + g.st - 1) / g.st;
@@ -790,11 +978,19 @@ static GemmPlan plan_core(const ConvGeom &g, int pass) {
         pl.M = g.N * hh * wh; pl.Ng = g.C; pl.Kg = rt * stt * g.K;
         pl.av = g.K % 4 == 0;
         pl.bv = g.C % 4 == 0;
+        pl.tu = g.K % 16 == 0 && g.C % 4 == 0;
     } else {
         pl.M = g.K; pl.Ng = g.R * g.S * g.C; pl.Kg = g.N * g.P * g.Q;
         pl.av = g.K % 4 == 0;
         pl.bv = g.C % 4 == 0;
+        pl.tu = pl.av && pl.bv && g.Q >= 16;
     }
+    // The lean mode reads each operand through a 32-bit byte offset and needs
+    // offsets at or past 2^31 to read as zeros: every operand below 2 GB.
+    const int64_t x_el = (int64_t)g.N * g.H * g.W * g.C, y_el = (int64_t)g.N * g.P * g.Q * g.K,
+                  w_el = (int64_t)g.K * g.R * g.S * g.C;
+    if (4 * std::max({x_el, y_el, w_el}) >= (int64_t)OOB)
+        pl.tu = false;
     // Pick the tile and split-K factor with the least estimated time.  A CU
     // holds at most occ[c] workgroups of a tile at once (registers and LDS)
     // and, holding k of them, keeps its matrix cores busy a fraction util(k)

@@ -15,85 +15,6 @@
 
 namespace dc {
 
-// ---------------------------------------------------------------- host pool
-
-HostPool::HostPool(int threads) {
-    for (int i = 1; i < threads; ++i)
-        workers_.emplace_back([this, i] { loop(i); });
-}
-
-HostPool::~HostPool() {
-    {
-        std::lock_guard<std::mutex> g(mu_);
-        stop_ = true;
-    }
-    cv_.notify_all();
-    for (auto &t : workers_)
-        t.join();
-}
-
-void HostPool::loop(int) {
-    long seen = 0;
-    for (;;) {
-        const std::function<void(int, int)> *job;
-        int n;
-        {
-            std::unique_lock<std::mutex> lk(mu_);
-            cv_.wait(lk, [&] { return stop_ || gen_ != seen; });
-            if (stop_)
-                return;
-            seen = gen_;
-            job = job_;
-            n = job_n_;
-            ++active_;
-        }
-        for (;;) {
-            int i;
-            {
-                std::lock_guard<std::mutex> g(mu_);
-                i = next_ < n ? next_++ : -1;
-            }
-            if (i < 0)
-                break;
-            (*job)(i, n);
-        }
-        {
-            std::lock_guard<std::mutex> g(mu_);
-            --active_;
-        }
-        done_cv_.notify_all();
-    }
-}
-
-void HostPool::run(int n, const std::function<void(int, int)> &fn) {
-    if (workers_.empty() || n <= 1) {
-        for (int i = 0; i < n; ++i)
-            fn(i, n);
-        return;
-    }
-    {
-        std::lock_guard<std::mutex> g(mu_);
-        job_ = &fn;
-        job_n_ = n;
-        next_ = 0;
-        ++gen_;
-    }
-    cv_.notify_all();
-    for (;;) {
-        int i;
-        {
-            std::lock_guard<std::mutex> g(mu_);
-            i = next_ < n ? next_++ : -1;
-        }
-        if (i < 0)
-            break;
-        fn(i, n);
-    }
-    std::unique_lock<std::mutex> lk(mu_);
-    done_cv_.wait(lk, [&] { return active_ == 0 && next_ >= n; });
-    job_ = nullptr;
-}
-
 namespace {
 
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }

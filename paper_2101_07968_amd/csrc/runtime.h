@@ -2,6 +2,7 @@
 #pragma once
 
 #include "dc_internal.h"
+#include "host_pool.h"
 
 #include <condition_variable>
 #include <functional>
@@ -33,28 +34,6 @@ struct OpInfo {
     int ch_off[4] = {0, 0, 0, 0};    // CONCAT: channel offset of each input in the output
     bool grad_in[4] = {false, false, false, false};
     int acc_in[4] = {0, 0, 0, 0};    // backward adds into the input gradient
-};
-
-// Small persistent pool for the server-side SGD update.
-class HostPool {
-  public:
-    explicit HostPool(int threads);
-    ~HostPool();
-    // Run fn(i, n) for i in [0, n) over the pool and the calling thread.
-    void run(int n, const std::function<void(int, int)> &fn);
-    int size() const { return (int)workers_.size() + 1; }
-
-  private:
-    void loop(int id);
-    std::vector<std::thread> workers_;
-    std::mutex mu_;
-    std::condition_variable cv_, done_cv_;
-    const std::function<void(int, int)> *job_ = nullptr;
-    int job_n_ = 0;
-    int next_ = 0;
-    int active_ = 0;
-    long gen_ = 0;
-    bool stop_ = false;
 };
 
 } // namespace dc

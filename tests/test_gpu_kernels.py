@@ -71,6 +71,12 @@ SMALL = [
     (2, 5, 5, 6, 5, 5, 1, 2),
     (2, 6, 6, 4, 4, 3, 3, 1),
     (5, 17, 17, 40, 136, 3, 1, 1),
+    # lean address modes: wgrad pixel carry with row and image wraps and a
+    # ragged last stage (Q >= 16), strided; dgrad / forward tap-uniform stages
+    (3, 17, 19, 8, 12, 3, 1, 1),
+    (2, 35, 33, 4, 8, 3, 2, 1),
+    (2, 9, 10, 32, 48, 3, 2, 1),
+    (3, 20, 18, 16, 32, 5, 1, 2),
 ]
 
 
