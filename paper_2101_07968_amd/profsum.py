@@ -13,6 +13,15 @@ to one iteration's worth, for comparison with the bench's conv_ms_per_step.
 traffic: FETCH_SIZE / WRITE_SIZE (KiB per dispatch) of the igemm dispatches of a
 `bench.py --kernels-only` run, scaled by what the same counters read for the
 256 MiB calibration copy, against the algorithmic bytes of those launches.
+
+mfma: SQ_INSTS_VALU_MFMA_MOPS_F32 (units of 512 flops), SQ_VALU_MFMA_BUSY_CYCLES
+and GRBM_GUI_ACTIVE of the same igemm dispatches, with their durations from a
+kernel-trace run: MFMA flops issued against algorithmic flops, and the fraction
+of SIMD cycles the matrix cores were busy.
+
+hbm: FETCH_SIZE / WRITE_SIZE of every dispatch of a run that includes a
+calibration copy (the non-GEMM report does), over durations from a
+kernel-trace run of the same command, per bandwidth-bound kernel.
 """
 from __future__ import annotations
 
@@ -112,6 +121,95 @@ def cmd_traffic(a):
     print(f"igemm_source_sha256={sha}")
 
 
+def _trace_durations(path, keep):
+    """Durations (ns) of the dispatches whose kernel name passes keep(), in dispatch order."""
+    rows = [r for r in csv.DictReader(open(path)) if keep(r["Kernel_Name"])]
+    rows.sort(key=lambda r: int(r["Start_Timestamp"]))
+    return [(r["Kernel_Name"], int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) for r in rows]
+
+
+def _counters(path, names):
+    """{dispatch id: (kernel name, {counter: value})} for the named counters."""
+    out = {}
+    for r in csv.DictReader(open(path)):
+        if r["Counter_Name"] not in names:
+            continue
+        d = out.setdefault(int(r["Dispatch_Id"]), (r["Kernel_Name"], {}))
+        d[1][r["Counter_Name"]] = d[1].get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+    return dict(sorted(out.items()))
+
+
+def cmd_mfma(a):
+    """MFMA work and busy fraction of the implicit-GEMM dispatches of a `bench.py --kernels-only` run."""
+    from . import nets as PN
+    cnt = _counters(a.counters, {"SQ_INSTS_VALU_MFMA_MOPS_F32", "SQ_VALU_MFMA_BUSY_CYCLES", "GRBM_GUI_ACTIVE"})
+    gem = [(k, v) for k, v in cnt.values() if "igemm_kernel" in k]
+    dur = [d for _, d in _trace_durations(a.trace, lambda n: "igemm_kernel" in n)]
+    if len(dur) != len(gem):
+        raise SystemExit(f"{len(gem)} counted igemm dispatches but {len(dur)} in the trace")
+    mops = sum(v.get("SQ_INSTS_VALU_MFMA_MOPS_F32", 0) for _, v in gem)
+    busy = sum(v.get("SQ_VALU_MFMA_BUSY_CYCLES", 0) for _, v in gem)
+    active = sum(v.get("GRBM_GUI_ACTIVE", 0) for _, v in gem)
+    ops, hwc, _ = PN.build(a.workload)
+    algo = 0.0
+    for _i, g, first in PN.conv_geoms(ops, hwc, a.batch):
+        n, h, w, c, k, r, s_, st, pad = g
+        P, Q = (h + 2 * pad - r) // st + 1, (w + 2 * pad - s_) // st + 1
+        algo += 2.0 * n * P * Q * k * r * s_ * c * (2 if first else 3)
+    launches = len(gem) / (len(PN.conv_geoms(ops, hwc, a.batch)) * 3 - sum(1 for *_, f in
+                                                                          PN.conv_geoms(ops, hwc, a.batch) if f))
+    flops = mops * 512.0
+    simds = a.cus * 4
+    print(f"# fp32 MFMA counters of the implicit-GEMM kernel, {a.workload} batch {a.batch}")
+    print(f"# commands: {a.cmd}")
+    print(f"# igemm dispatches: {len(gem)} ({launches:g} launches of each conv/FC pass)")
+    print(f"mfma_flops_per_iteration={flops / launches:.4e}")
+    print(f"algorithmic_flops_per_iteration={algo:.4e}")
+    print(f"mfma_over_algorithmic={flops / launches / algo:.3f}")
+    print(f"kernel_time_per_iteration_ms={sum(dur) / launches / 1e6:.3f}")
+    print(f"mfma_tflops_issued={flops / sum(dur) / 1e3:.1f}")
+    print(f"algorithmic_tflops={algo * launches / sum(dur) / 1e3:.1f}")
+    # GRBM_GUI_ACTIVE arrives summed over the XCDs; per XCD it counts the
+    # cycles the GPU was busy, which all of its SIMDs share
+    print(f"gpu_active_cycles_per_xcd={active / a.xcds:.4e} (over {sum(dur) / 1e6:.2f} ms: "
+          f"{active / a.xcds / sum(dur):.2f} GHz)")
+    print(f"mfma_busy_percent={100.0 * busy / (active / a.xcds * simds):.1f}")
+    print(f"igemm_source_sha256={hashlib.sha256(open(os.path.join(HERE, 'csrc', 'igemm.hip'), 'rb').read()).hexdigest()}")
+
+
+def cmd_hbm(a):
+    """HBM GB/s of the bandwidth-bound kernels: calibrated FETCH_SIZE + WRITE_SIZE per dispatch over the
+    dispatch's duration from a kernel-trace run of the same command."""
+    fetch = _counters(a.fetch, {"FETCH_SIZE"})
+    write = _counters(a.write, {"WRITE_SIZE"})
+    cal = [v["FETCH_SIZE"] for k, v in fetch.values() if "copy_grad_kernel" in k]
+    calw = [v["WRITE_SIZE"] for k, v in write.values() if "copy_grad_kernel" in k]
+    known_kib = a.cal_bytes / 1024.0
+    sf, sw = known_kib / max(cal), known_kib / max(calw)
+    names = [k for k, _ in fetch.values()]
+    dur = _trace_durations(a.trace, lambda n: True)
+    if [short(k) for k, _ in dur] != [short(k) for k in names] or len(write) != len(fetch):
+        raise SystemExit("the counter and trace runs dispatched different kernel sequences")
+    agg = {}
+    for (k, fv), (_, wv), (_, d) in zip(fetch.values(), write.values(), dur):
+        key = short(k)
+        if not any(t in key for t in ("relu", "maxpool", "bn_", "colred", "add_kernel", "copy_grad", "gap_",
+                                      "concat")):
+            continue
+        t = agg.setdefault(key, [0, 0.0, 0])
+        t[0] += fv["FETCH_SIZE"] * sf * 1024 + wv["WRITE_SIZE"] * sw * 1024
+        t[1] += d
+        t[2] += 1
+    print(f"# HBM traffic of the bandwidth-bound kernels ({a.what_ran})")
+    print(f"# commands: {a.cmd}")
+    print(f"# calibration: {a.cal_bytes} B copy read as FETCH_SIZE {max(cal):.1f} KiB, WRITE_SIZE {max(calw):.1f} KiB")
+    print("")
+    print("| kernel | dispatches | HBM bytes (counters) | time (ms) | GB/s | % of 8 TB/s |")
+    print("|---|---|---|---|---|---|")
+    for key, (b, d, n) in sorted(agg.items(), key=lambda kv: -kv[1][1]):
+        print(f"| `{key}` | {n} | {b / 1e9:.3f} GB | {d / 1e6:.3f} | {b / d:.0f} | {100 * b / d / 8000:.1f}% |")
+
+
 def main():
     ap = argparse.ArgumentParser()
     sub = ap.add_subparsers(dest="what", required=True)
@@ -129,8 +227,23 @@ def main():
     t.add_argument("--batch", type=int, default=32)
     t.add_argument("--cal-bytes", type=int, default=256 << 20)
     t.add_argument("--cmd", default="")
+    m = sub.add_parser("mfma")
+    m.add_argument("counters")
+    m.add_argument("trace")
+    m.add_argument("--workload", default="vgg16")
+    m.add_argument("--batch", type=int, default=32)
+    m.add_argument("--cus", type=int, default=256)
+    m.add_argument("--xcds", type=int, default=8)
+    m.add_argument("--cmd", default="")
+    h = sub.add_parser("hbm")
+    h.add_argument("fetch")
+    h.add_argument("write")
+    h.add_argument("trace")
+    h.add_argument("--cal-bytes", type=int, default=256 << 20)
+    h.add_argument("--what-ran", default="")
+    h.add_argument("--cmd", default="")
     a = ap.parse_args()
-    cmd_stats(a) if a.what == "stats" else cmd_traffic(a)
+    {"stats": cmd_stats, "traffic": cmd_traffic, "mfma": cmd_mfma, "hbm": cmd_hbm}[a.what](a)
 
 
 if __name__ == "__main__":

@@ -380,6 +380,12 @@ def main():
             "\n".join(x for r in rows for x in split_rows(r)) + "\n\nfitted link rate (Gb/s): " + \
             ", ".join(f"{r['workload']} {r['link']}: {r['link_fit_gbps']:g}" for r in rows)
     if a.non_gemm:
+        # a 256 MiB copy of known size first: the scale for HBM byte counters
+        src = torch.ones(64 << 20, device="cuda")
+        dst = torch.empty_like(src)
+        D.call("dc_copy_grad", src.data_ptr(), 0, dst.data_ptr(), src.numel(), torch.cuda.current_stream().cuda_stream)
+        torch.cuda.synchronize()
+        del src, dst
         text = "\n\n".join(non_gemm(D, PN, torch, w) for w in a.non_gemm.split(","))
     if a.planner_scaling:
         text = planner_scaling(D, synth, [4, 8, 16, 18, 50, 100, 160, 200, 300])
