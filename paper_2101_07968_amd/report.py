@@ -57,6 +57,21 @@ def breakdown(tl):
     return out
 
 
+def link_rates(tl, layer_bytes, dt_ns):
+    """Achieved pull and push rates (bytes/s) of one step: each segment's bytes over its
+    duration less the per-transfer overhead dt, summed over the segments (a segment
+    appears on the timeline row of every layer it carries)."""
+    out = []
+    for c0 in (0, 6):
+        segs = {}
+        for l in range(tl.shape[0]):
+            key = (int(tl[l, c0]), int(tl[l, c0 + 1]))
+            segs[key] = segs.get(key, 0) + layer_bytes[l]
+        t = sum(max(e - s - dt_ns, 1) for s, e in segs)
+        out.append(sum(segs.values()) / t * 1e9)
+    return out
+
+
 def run_case(D, PN, synth, torch, name, rate_bps, paced, steps, lbl_limit_s=6.0, dt_emul_ns=0):
     wl = PN.WORKLOADS[name]
     ops, hwc, classes = PN.build(name)
@@ -105,6 +120,9 @@ def run_case(D, PN, synth, torch, name, rate_bps, paced, steps, lbl_limit_s=6.0,
                     "model_err": round(abs(t_iter - t_model_s * 1e3) / (t_model_s * 1e3), 4),
                     "n_pull": st["n_pull"], "n_push": st["n_push"], "steps": n,
                     "split": breakdown(model.timeline())}
+        if key == "dp":
+            pr, gr = link_rates(model.timeline(), model.layer_bytes(), prof.dt)
+            res["link_achieved_gbps"] = [round(pr * 8 / 1e9, 3), round(gr * 8 / 1e9, 3)]
     model.close()
     del xd, yd
     torch.cuda.empty_cache()
@@ -377,8 +395,10 @@ def main():
     text = ""
     if rows:
         text = HEADER + "\n" + "\n".join(row(r) for r in rows) + "\n\n" + SPLIT_HEADER + "\n" + \
-            "\n".join(x for r in rows for x in split_rows(r)) + "\n\nfitted link rate (Gb/s): " + \
-            ", ".join(f"{r['workload']} {r['link']}: {r['link_fit_gbps']:g}" for r in rows)
+            "\n".join(x for r in rows for x in split_rows(r)) + "\n\nlink rate (Gb/s), fitted by dc_profile / " + \
+            "achieved by the DP step's pulls / pushes: " + \
+            ", ".join(f"{r['workload']} {r['link']}: {r['link_fit_gbps']:g} / {r['link_achieved_gbps'][0]:g} / "
+                      f"{r['link_achieved_gbps'][1]:g}" for r in rows)
     if a.non_gemm:
         # a 256 MiB copy of known size first: the scale for HBM byte counters
         src = torch.ones(64 << 20, device="cuda")

@@ -77,6 +77,9 @@ SMALL = [
     (2, 35, 33, 4, 8, 3, 2, 1),
     (2, 9, 10, 32, 48, 3, 2, 1),
     (3, 20, 18, 16, 32, 5, 1, 2),
+    # a single output pixel; a stride larger than the filter (dgrad phases with no tap)
+    (2, 3, 3, 8, 16, 3, 1, 0),
+    (2, 9, 9, 4, 8, 1, 3, 0),
 ]
 
 

@@ -53,7 +53,7 @@ def plans_for(L, seed=0):
 
 
 PARITY = [("tiny", 4), ("alexnet", 2), ("resnet18", 8), ("resnet50", 2), ("vgg16", 1), ("googlenet", 2),
-          ("vgg19", 1), ("resnet152", 2)]
+          ("vgg19", 1), ("resnet152", 2), ("tiny", 1), ("resnet18", 1)]
 
 
 def fp32_spread(spec, onet, x, y, params, g_ref):
@@ -288,3 +288,42 @@ def test_replanning_follows_the_link():
         plans[rate] = plan.decisions()
     # the fast link is worth splitting, the slow one barely
     assert sum(plans[1.25e10 / 8 * 8][0]) >= sum(plans[1.25e8][0])
+
+
+def test_degenerate_models():
+    """L = 1 (one FC layer: no segment decision to make) at batch 1, and a two-layer
+    conv net whose conv output is a single pixel, each against the oracle."""
+    cases = [
+        ({"name": "fc1", "ops": [{"op": "fc", "in": 0, "layer": 1, "out": 10, "bias": True}],
+          "hwc": (4, 4, 3), "classes": 10},
+         [(D.DC_OP_FC, 1, 0, -1, 10, 0, 0, 0, 0, 1, -1, -1)], 1),
+        ({"name": "pix1", "ops": [
+            {"op": "conv", "in": 0, "layer": 1, "k": 8, "r": 3, "s": 3, "stride": 1, "pad": 0, "bias": True},
+            {"op": "relu", "in": 1, "layer": 1},
+            {"op": "fc", "in": 2, "layer": 2, "out": 5, "bias": True}],
+          "hwc": (3, 3, 4), "classes": 5},
+         [(D.DC_OP_CONV, 1, 0, -1, 8, 3, 3, 1, 0, 1, -1, -1), (D.DC_OP_RELU, 1, 1, -1, 0, 0, 0, 0, 0, 0, -1, -1),
+          (D.DC_OP_FC, 2, 2, -1, 5, 0, 0, 0, 0, 1, -1, -1)], 3),
+    ]
+    for spec, ops, batch in cases:
+        print(f"degenerate {spec['name']} batch {batch}", flush=True)
+        hwc, classes = spec["hwc"], spec["classes"]
+        specs = PN.param_specs(ops, hwc)
+        onet = OC.Net(spec, batch)
+        assert specs == onet.param_specs
+        x, y, params = synth.cnn_inputs(21, batch, hwc, classes, specs)
+        model = D.Model(ops, batch, hwc, classes)
+        model.ps_write(params)
+        xd, yd = dev(x), dev(y)
+        prof = model.profile(xd, yd, D.link(1e9, 0, paced=True), reps=1)
+        plan = D.dc_plan(prof)
+        p_ref, _, _, _ = OP.forward_dp(prof.pt.tolist(), prof.fc.tolist(), prof.dt)
+        assert list(plan.decisions()[0]) == list(p_ref)
+        model.ps_write(params)
+        st = model.step(xd, yd, plan, UNPACED)
+        p_new, g = model.ps_read()
+        loss_ref, g_ref, p_ref = onet.step(x, y, params)
+        assert abs(st["loss"] - loss_ref) <= 1e-4 * abs(loss_ref)
+        assert rel_err(g, g_ref) <= 1e-3
+        assert rel_err(p_new, p_ref) <= 1e-3
+        model.close()

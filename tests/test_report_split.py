@@ -24,3 +24,14 @@ def test_breakdown_segments_repeat_per_layer():
     s = breakdown(tl)
     assert s["fwd"] == [4.0, 0.0, 10.0]
     assert s["bwd"] == [4.0, 0.0, 4.0]
+
+
+def test_link_rates_count_each_segment_once():
+    from paper_2101_07968_amd.report import link_rates
+    # two layers in one pull segment (0..10 us), one push segment per layer
+    tl = np.array([[0, 10_000, 0, 0, 0, 0, 30_000, 32_000],
+                   [0, 10_000, 0, 0, 0, 0, 20_000, 30_000]], dtype=np.int64)
+    pull, push = link_rates(tl, [1000, 3000], dt_ns=2_000)
+    assert pull == 4000 / 8_000 * 1e9
+    # 1000 B in 2 us - 2 us overhead -> clamped to 1 ns; 3000 B in 10 - 2 us
+    assert push == 4000 / (1 + 8_000) * 1e9
