@@ -106,6 +106,21 @@ __device__ __forceinline__ Phase make_phase(const Args &a, int z) {
 __device__ __forceinline__ float4 ld4(const float *p) { return *reinterpret_cast<const float4 *>(p); }
 __device__ __forceinline__ void st4(float *p, float4 v) { *reinterpret_cast<float4 *>(p) = v; }
 
+// Fragment idx (of NTHR * F) of a k-contiguous tile [row][KT + PADK] -> (row,
+// k quad).  A wave's 64 fragments cover 64 / (KT/4) rows; within each run of
+// 16 lanes the row changes fastest and the quad is fixed, so the 16 float4
+// LDS writes of a run land on disjoint banks (rows are KT + 4 floats apart);
+// the global addresses a wave loads are the same set as with the quad
+// fastest, so coalescing is unchanged.
+template <int KT>
+__device__ __forceinline__ void kc_map_t(int idx, int *row, int *kc) {
+    constexpr int Q4 = KT / 4;               // quads per row
+    constexpr int RW = 64 / Q4;              // rows per wave
+    const int lane = idx & 63;
+    *row = (idx >> 6) * RW + lane % RW;
+    *kc = lane / RW;
+}
+
 // Raw buffer loads for the lean address mode: a 32-bit byte offset into a
 // tensor described by base and size; an offset at or past the size reads as
 // zeros, which is how the kernel fetches padding and tails without branches.
@@ -156,7 +171,7 @@ __device__ __forceinline__ float epilogue(const Args &a, int pass, float v, int 
 //    origin and offset are carried from stage to stage with uniform
 //    increments instead of being decoded.
 template <int PASS, int MT, int NT, int KT, bool AV, bool BV, bool TU>
-__global__ __launch_bounds__(NTHR) void igemm_kernel(Args a) {
+__global__ __launch_bounds__(NTHR, TU ? 4 : 1) void igemm_kernel(Args a) {
     static_assert(!TU || (AV && BV), "the lean address mode needs float4 operands");
     constexpr bool A_KC = (PASS != PASS_WGRAD); // A tile stored [row][k]
     constexpr bool B_KC = (PASS == PASS_FWD);   // B tile stored [col][k]
@@ -210,7 +225,8 @@ __global__ __launch_bounds__(NTHR) void igemm_kernel(Args a) {
     const int nkt = max(kt1 - kt0, 0);
 
     // ------------------------------------------------ per-thread load state
-    // A fragments: k-contiguous -> (row = idx / (KT/4), kc = idx % (KT/4));
+    auto kc_map = [](int idx, int *row, int *kc) { kc_map_t<KT>(idx, row, kc); };
+    // A fragments: k-contiguous -> kc_map (row, k quad);
     // row-contiguous -> (krow = idx / (MT/4), mc = idx % (MT/4)).
     int a_row[FA];
     int a_kc = 0;
@@ -221,8 +237,7 @@ __global__ __launch_bounds__(NTHR) void igemm_kernel(Args a) {
     for (int f = 0; f < FA; ++f) {
         int idx = t + NTHR * f;
         if (A_KC) {
-            a_row[f] = idx / (KT / 4);
-            a_kc = idx % (KT / 4);
+            kc_map(idx, &a_row[f], &a_kc);
             int m = tm * MT + a_row[f];
             a_ok[f] = m < M;
             int mm = a_ok[f] ? m : 0;
@@ -264,7 +279,7 @@ __global__ __launch_bounds__(NTHR) void igemm_kernel(Args a) {
         for (int f = 0; f < FA; ++f)
             a_base[f] = ((a_n[f] * a.P + a_h[f]) * a.Q + a_w[f]) * a.K + 4 * a_kc;
     }
-    // B fragments: k-contiguous -> (row = idx / (KT/4), kc); n-contiguous ->
+    // B fragments: k-contiguous -> kc_map (row, k quad); n-contiguous ->
     // (krow = idx / (NT/4), nc = idx % (NT/4)).
     int b_row[FB];
     int b_kc = 0;
@@ -276,8 +291,7 @@ __global__ __launch_bounds__(NTHR) void igemm_kernel(Args a) {
     for (int f = 0; f < FB; ++f) {
         int idx = t + NTHR * f;
         if (B_KC) {
-            b_row[f] = idx / (KT / 4);
-            b_kc = idx % (KT / 4);
+            kc_map(idx, &b_row[f], &b_kc);
         } else {
             b_row[f] = idx / (NT / 4);
             b_kc = idx % (NT / 4);
@@ -1002,7 +1016,9 @@ static GemmPlan plan_core(const ConvGeom &g, int pass) {
     // for writing and re-reading its partial sums.
     static const int cand[4][2] = {{128, 128}, {128, 64}, {64, 128}, {64, 64}};
     static const double eff[4] = {1.0, 0.9, 0.85, 0.85};
-    static const int occ[4] = {3, 4, 4, 6};
+    // workgroups per CU of each tile (registers and 160 KB of LDS): the lean
+    // and wgrad 128 x 128 kernels fit four, the others three
+    const int occ[4] = {(pl.tu || pass == PASS_WGRAD) ? 4 : 3, 5, 5, 8};
     auto util = [](int k) { return std::min(0.95, 0.35 + 0.3 * k); };
     double best = 1e300;
     const int KT = 16;
