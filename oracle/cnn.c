@@ -24,10 +24,11 @@
 
 #define IDX4(a, b, c, d, B, C, D) ((((size_t)(a) * (B) + (b)) * (C) + (c)) * (D) + (d))
 
-/* Convolution (cross-correlation, zero padding):
- *   y[n,p,q,k] = b[k] + sum over r, s, c of x[n, p*st+r-pad, q*st+s-pad, c] * w[k,r,s,c]
+/* Convolution (cross-correlation, zero padding: pad rows above and below,
+ * pad_w columns left and right):
+ *   y[n,p,q,k] = b[k] + sum over r, s, c of x[n, p*st+r-pad, q*st+s-pad_w, c] * w[k,r,s,c]
  * Taps that fall into the padding contribute nothing.  b may be NULL. */
-void or_conv2d_forward(int N, int H, int W, int C, int K, int R, int S, int st, int pad,
+void or_conv2d_forward(int N, int H, int W, int C, int K, int R, int S, int st, int pad, int pad_w,
                        int P, int Q, const double *x, const double *w, const double *b,
                        double *y)
 {
@@ -51,7 +52,7 @@ void or_conv2d_forward(int N, int H, int W, int C, int K, int R, int S, int st, 
                     if (h < 0 || h >= H)
                         continue;
                     for (int s = 0; s < S; ++s) {
-                        int ww = q * st + s - pad;
+                        int ww = q * st + s - pad_w;
                         if (ww < 0 || ww >= W)
                             continue;
                         const double *xp = x + IDX4(n, h, ww, 0, H, W, C);
@@ -69,9 +70,9 @@ void or_conv2d_forward(int N, int H, int W, int C, int K, int R, int S, int st, 
 
 /* Gradient of the convolution with respect to its input:
  *   dx[n,h,w,c] = sum over r, s, k of dy[n,p,q,k] * w[k,r,s,c]
- * over the taps with h = p*st + r - pad and w = q*st + s - pad for an output
+ * over the taps with h = p*st + r - pad and w = q*st + s - pad_w for an output
  * position (p, q) inside the output. */
-void or_conv2d_backward_data(int N, int H, int W, int C, int K, int R, int S, int st, int pad,
+void or_conv2d_backward_data(int N, int H, int W, int C, int K, int R, int S, int st, int pad, int pad_w,
                              int P, int Q, const double *dy, const double *w, double *dx)
 {
 #pragma omp parallel for collapse(2) schedule(dynamic, 1)
@@ -87,7 +88,7 @@ void or_conv2d_backward_data(int N, int H, int W, int C, int K, int R, int S, in
                         continue;
                     int p = t / st;
                     for (int s = 0; s < S; ++s) {
-                        int u = ww + pad - s;
+                        int u = ww + pad_w - s;
                         if (u < 0 || u % st != 0 || u / st >= Q)
                             continue;
                         int q = u / st;
@@ -104,8 +105,8 @@ void or_conv2d_backward_data(int N, int H, int W, int C, int K, int R, int S, in
 }
 
 /* Gradient of the convolution with respect to its filter:
- *   dw[k,r,s,c] = sum over n, p, q of dy[n,p,q,k] * x[n, p*st+r-pad, q*st+s-pad, c] */
-void or_conv2d_backward_filter(int N, int H, int W, int C, int K, int R, int S, int st, int pad,
+ *   dw[k,r,s,c] = sum over n, p, q of dy[n,p,q,k] * x[n, p*st+r-pad, q*st+s-pad_w, c] */
+void or_conv2d_backward_filter(int N, int H, int W, int C, int K, int R, int S, int st, int pad, int pad_w,
                                int P, int Q, const double *x, const double *dy, double *dw)
 {
 #pragma omp parallel for collapse(2) schedule(dynamic, 1)
@@ -121,7 +122,7 @@ void or_conv2d_backward_filter(int N, int H, int W, int C, int K, int R, int S, 
                         if (h < 0 || h >= H)
                             continue;
                         for (int q = 0; q < Q; ++q) {
-                            int ww = q * st + s - pad;
+                            int ww = q * st + s - pad_w;
                             if (ww < 0 || ww >= W)
                                 continue;
                             const double g = dy[IDX4(n, p, q, k, P, Q, K)];
@@ -192,7 +193,7 @@ void or_maxpool_backward(int N, int H, int W, int C, int R, int S, int st, int p
  * (every float32 is exact in double); each sample is accumulated in double in
  * the order of its definition.  idx holds 4 indices per sample:
  *   forward (n, p, q, k); data gradient (n, h, w, c); filter gradient (k, r, s, c). */
-void or_conv2d_forward_samples(int N, int H, int W, int C, int K, int R, int S, int st, int pad,
+void or_conv2d_forward_samples(int N, int H, int W, int C, int K, int R, int S, int st, int pad, int pad_w,
                                int P, int Q, const float *x, const float *w, const float *b,
                                int ns, const int *idx, double *out)
 {
@@ -206,7 +207,7 @@ void or_conv2d_forward_samples(int N, int H, int W, int C, int K, int R, int S, 
             if (h < 0 || h >= H)
                 continue;
             for (int s = 0; s < S; ++s) {
-                int ww = q * st + s - pad;
+                int ww = q * st + s - pad_w;
                 if (ww < 0 || ww >= W)
                     continue;
                 for (int c = 0; c < C; ++c)
@@ -219,7 +220,7 @@ void or_conv2d_forward_samples(int N, int H, int W, int C, int K, int R, int S, 
     }
 }
 
-void or_conv2d_backward_data_samples(int N, int H, int W, int C, int K, int R, int S, int st, int pad,
+void or_conv2d_backward_data_samples(int N, int H, int W, int C, int K, int R, int S, int st, int pad, int pad_w,
                                      int P, int Q, const float *dy, const float *w,
                                      int ns, const int *idx, double *out)
 {
@@ -234,7 +235,7 @@ void or_conv2d_backward_data_samples(int N, int H, int W, int C, int K, int R, i
                 continue;
             int p = t / st;
             for (int s = 0; s < S; ++s) {
-                int u = ww + pad - s;
+                int u = ww + pad_w - s;
                 if (u < 0 || u % st != 0 || u / st >= Q)
                     continue;
                 int q = u / st;
@@ -246,7 +247,7 @@ void or_conv2d_backward_data_samples(int N, int H, int W, int C, int K, int R, i
     }
 }
 
-void or_conv2d_backward_filter_samples(int N, int H, int W, int C, int K, int R, int S, int st, int pad,
+void or_conv2d_backward_filter_samples(int N, int H, int W, int C, int K, int R, int S, int st, int pad, int pad_w,
                                        int P, int Q, const float *x, const float *dy,
                                        int ns, const int *idx, double *out)
 {
@@ -260,7 +261,7 @@ void or_conv2d_backward_filter_samples(int N, int H, int W, int C, int K, int R,
                 if (h < 0 || h >= H)
                     continue;
                 for (int q = 0; q < Q; ++q) {
-                    int ww = q * st + s - pad;
+                    int ww = q * st + s - pad_w;
                     if (ww < 0 || ww >= W)
                         continue;
                     acc += (double)dy[IDX4(n, p, q, k, P, Q, K)] * (double)x[IDX4(n, h, ww, c, H, W, C)];

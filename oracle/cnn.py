@@ -4,9 +4,10 @@ A plain CPU implementation of what one worker computes between pulling the
 parameters and pushing the gradients in the parameter-server iteration of
 Sec. III-A (pull, forward, backward, push), and of the server's update:
 
-* forward: convolution, FC, BatchNorm (training mode, batch statistics),
-  ReLU, max-pooling, global average pooling, residual add, channel
-  concatenation;
+* forward: convolution (its row and column padding may differ), FC,
+  BatchNorm (training mode, batch statistics), ReLU, max-pooling, average
+  pooling (padded taps excluded from the count), global average pooling,
+  residual add, channel concatenation;
 * loss: mean over the batch of the softmax cross-entropy;
 * backward by the chain rule, giving the gradient of every parameter;
 * the server's SGD update w <- w - lr * g.
@@ -45,15 +46,15 @@ def lib():
         dp = ctypes.POINTER(ctypes.c_double)
         ip = ctypes.POINTER(ctypes.c_int)
         i = ctypes.c_int
-        L.or_conv2d_forward.argtypes = [i] * 11 + [dp, dp, dp, dp]
-        L.or_conv2d_backward_data.argtypes = [i] * 11 + [dp, dp, dp]
-        L.or_conv2d_backward_filter.argtypes = [i] * 11 + [dp, dp, dp]
+        L.or_conv2d_forward.argtypes = [i] * 12 + [dp, dp, dp, dp]
+        L.or_conv2d_backward_data.argtypes = [i] * 12 + [dp, dp, dp]
+        L.or_conv2d_backward_filter.argtypes = [i] * 12 + [dp, dp, dp]
         L.or_maxpool_forward.argtypes = [i] * 10 + [dp, dp, ip]
         L.or_maxpool_backward.argtypes = [i] * 10 + [dp, ip, dp]
         fp = ctypes.POINTER(ctypes.c_float)
-        L.or_conv2d_forward_samples.argtypes = [i] * 11 + [fp, fp, fp, i, ip, dp]
-        L.or_conv2d_backward_data_samples.argtypes = [i] * 11 + [fp, fp, i, ip, dp]
-        L.or_conv2d_backward_filter_samples.argtypes = [i] * 11 + [fp, fp, i, ip, dp]
+        L.or_conv2d_forward_samples.argtypes = [i] * 12 + [fp, fp, fp, i, ip, dp]
+        L.or_conv2d_backward_data_samples.argtypes = [i] * 12 + [fp, fp, i, ip, dp]
+        L.or_conv2d_backward_filter_samples.argtypes = [i] * 12 + [fp, fp, i, ip, dp]
         for f in ("or_conv2d_forward", "or_conv2d_backward_data", "or_conv2d_backward_filter",
                   "or_maxpool_forward", "or_maxpool_backward", "or_conv2d_forward_samples",
                   "or_conv2d_backward_data_samples", "or_conv2d_backward_filter_samples"):
@@ -74,18 +75,26 @@ def conv_out(h, r, st, pad):
     return (h + 2 * pad - r) // st + 1
 
 
+def _pads(pad):
+    """Padding given as one int (rows and columns alike) or as (rows, columns)."""
+    if isinstance(pad, (tuple, list)):
+        return int(pad[0]), int(pad[1])
+    return int(pad), int(pad)
+
+
 # ---------------------------------------------------------------- primitives
 
 def conv2d_forward(x, w, b, st, pad):
-    """y[n,p,q,k] = b[k] + sum_{r,s,c} x[n,p*st+r-pad,q*st+s-pad,c] w[k,r,s,c]."""
+    """y[n,p,q,k] = b[k] + sum_{r,s,c} x[n,p*st+r-ph,q*st+s-pw,c] w[k,r,s,c], (ph, pw) = pad."""
     x, w = _f64(x), _f64(w)
     N, H, W, C = x.shape
     K, R, S, C2 = w.shape
     assert C == C2
-    P, Q = conv_out(H, R, st, pad), conv_out(W, S, st, pad)
+    ph, pw = _pads(pad)
+    P, Q = conv_out(H, R, st, ph), conv_out(W, S, st, pw)
     y = np.empty((N, P, Q, K))
     bb = _f64(b) if b is not None else None
-    lib().or_conv2d_forward(N, H, W, C, K, R, S, st, pad, P, Q, _dp(x), _dp(w), _dp(bb), _dp(y))
+    lib().or_conv2d_forward(N, H, W, C, K, R, S, st, ph, pw, P, Q, _dp(x), _dp(w), _dp(bb), _dp(y))
     return y
 
 
@@ -96,7 +105,8 @@ def conv2d_backward_data(dy, w, in_hw, st, pad):
     assert K == K2
     H, W = in_hw
     dx = np.empty((N, H, W, C))
-    lib().or_conv2d_backward_data(N, H, W, C, K, R, S, st, pad, P, Q, _dp(dy), _dp(w), _dp(dx))
+    ph, pw = _pads(pad)
+    lib().or_conv2d_backward_data(N, H, W, C, K, R, S, st, ph, pw, P, Q, _dp(dy), _dp(w), _dp(dx))
     return dx
 
 
@@ -106,7 +116,8 @@ def conv2d_backward_filter(x, dy, rs, st, pad):
     N2, P, Q, K = dy.shape
     R, S = rs
     dw = np.empty((K, R, S, C))
-    lib().or_conv2d_backward_filter(N, H, W, C, K, R, S, st, pad, P, Q, _dp(x), _dp(dy), _dp(dw))
+    ph, pw = _pads(pad)
+    lib().or_conv2d_backward_filter(N, H, W, C, K, R, S, st, ph, pw, P, Q, _dp(x), _dp(dy), _dp(dw))
     return dw
 
 
@@ -132,6 +143,44 @@ def maxpool_backward(dy, arg, in_shape, r, s, st, pad):
     return dx
 
 
+def _avg_counts(H, W, r, s, st, pad, P, Q):
+    """Number of in-image taps of each R x S window (padded taps do not count)."""
+    hs = np.arange(P)[:, None] * st + np.arange(r)[None, :] - pad
+    ws = np.arange(Q)[:, None] * st + np.arange(s)[None, :] - pad
+    rows = ((hs >= 0) & (hs < H)).sum(axis=1)
+    cols = ((ws >= 0) & (ws < W)).sum(axis=1)
+    return rows[:, None] * cols[None, :]
+
+
+def avgpool_forward(x, r, s, st, pad):
+    """y[n,p,q,c] = mean of x over the in-image taps of the window at (p*st-pad, q*st-pad)."""
+    x = _f64(x)
+    N, H, W, C = x.shape
+    P, Q = conv_out(H, r, st, pad), conv_out(W, s, st, pad)
+    y = np.zeros((N, P, Q, C))
+    for p in range(P):
+        for q in range(Q):
+            h0, w0 = p * st - pad, q * st - pad
+            win = x[:, max(h0, 0):min(h0 + r, H), max(w0, 0):min(w0 + s, W), :]
+            y[:, p, q, :] = win.sum(axis=(1, 2)) / (win.shape[1] * win.shape[2])
+    return y
+
+
+def avgpool_backward(dy, in_shape, r, s, st, pad):
+    """dx[n,h,w,c] = sum over the windows holding (h, w) of dy[n,p,q,c] / count(p, q)."""
+    dy = _f64(dy)
+    N, P, Q, C = dy.shape
+    _, H, W, _ = in_shape
+    cnt = _avg_counts(H, W, r, s, st, pad, P, Q)
+    dx = np.zeros((N, H, W, C))
+    for p in range(P):
+        for q in range(Q):
+            h0, w0 = p * st - pad, q * st - pad
+            dx[:, max(h0, 0):min(h0 + r, H), max(w0, 0):min(w0 + s, W), :] += \
+                (dy[:, p, q, :] / cnt[p, q])[:, None, None, :]
+    return dx
+
+
 def _fp(a):
     return a.ctypes.data_as(ctypes.POINTER(ctypes.c_float)) if a is not None else None
 
@@ -139,17 +188,19 @@ def _fp(a):
 def conv2d_samples(which, geom, a, b, idx, bias=None):
     """Selected outputs of a conv pass, each from its definition, on float32 inputs.
 
-    geom = (N, H, W, C, K, R, S, stride, pad); which = "fwd" (a = x, b = w,
+    geom = (N, H, W, C, K, R, S, stride, pad[, pad_w]) (pad_w defaults to pad);
+    which = "fwd" (a = x, b = w,
     idx rows (n, p, q, k)), "dgrad" (a = dy, b = w, rows (n, h, w, c)) or
     "wgrad" (a = x, b = dy, rows (k, r, s, c)).  Returns float64 values.
     """
-    N, H, W, C, K, R, S, st, pad = geom
-    P, Q = conv_out(H, R, st, pad), conv_out(W, S, st, pad)
+    N, H, W, C, K, R, S, st, pad = geom[:9]
+    pad_w = geom[9] if len(geom) > 9 else pad
+    P, Q = conv_out(H, R, st, pad), conv_out(W, S, st, pad_w)
     a = np.ascontiguousarray(a, dtype=np.float32)
     b = np.ascontiguousarray(b, dtype=np.float32)
     idx = np.ascontiguousarray(idx, dtype=np.int32).reshape(-1, 4)
     out = np.empty(len(idx))
-    args = (N, H, W, C, K, R, S, st, pad, P, Q)
+    args = (N, H, W, C, K, R, S, st, pad, pad_w, P, Q)
     ip = idx.ctypes.data_as(ctypes.POINTER(ctypes.c_int))
     if which == "fwd":
         bb = None if bias is None else np.ascontiguousarray(bias, dtype=np.float32)
@@ -239,7 +290,8 @@ class Net:
             start = off
             kind = op["op"]
             if kind == "conv":
-                P, Q = conv_out(h, op["r"], op["stride"], op["pad"]), conv_out(w, op["s"], op["stride"], op["pad"])
+                ph, pw = _op_pads(op)
+                P, Q = conv_out(h, op["r"], op["stride"], ph), conv_out(w, op["s"], op["stride"], pw)
                 take("w", (op["k"], op["r"], op["s"], c), "he", op["r"] * op["s"] * c)
                 if op["bias"]:
                     take("b", (op["k"],), "zeros")
@@ -264,7 +316,7 @@ class Net:
                     assert shapes[o][:3] == (n, h, w)
                     cs += shapes[o][3]
                 out = (n, h, w, cs)
-            elif kind == "maxpool":
+            elif kind in ("maxpool", "avgpool"):
                 out = (n, conv_out(h, op["r"], op["stride"], op["pad"]),
                        conv_out(w, op["s"], op["stride"], op["pad"]), c)
             elif kind == "gap":
@@ -298,7 +350,7 @@ class Net:
             kind = op["op"]
             if kind == "conv":
                 b = self._p(params, i, "b") if op["bias"] else None
-                y = conv2d_forward(a, self._p(params, i, "w"), b, op["stride"], op["pad"])
+                y = conv2d_forward(a, self._p(params, i, "w"), b, op["stride"], _op_pads(op))
             elif kind == "fc":
                 a2 = a.reshape(a.shape[0], -1)
                 y = a2 @ self._p(params, i, "w").T
@@ -313,6 +365,8 @@ class Net:
             elif kind == "maxpool":
                 y, arg = maxpool_forward(a, op["r"], op["s"], op["stride"], op["pad"])
                 cache[i] = arg
+            elif kind == "avgpool":
+                y = avgpool_forward(a, op["r"], op["s"], op["stride"], op["pad"])
             elif kind == "gap":
                 y = a.mean(axis=(1, 2), keepdims=True)
             elif kind == "add":
@@ -352,12 +406,12 @@ class Net:
             a = t[op["in"]]
             kind = op["op"]
             if kind == "conv":
-                put(i, "w", conv2d_backward_filter(a, dy, (op["r"], op["s"]), op["stride"], op["pad"]))
+                put(i, "w", conv2d_backward_filter(a, dy, (op["r"], op["s"]), op["stride"], _op_pads(op)))
                 if op["bias"]:
                     put(i, "b", dy.sum(axis=(0, 1, 2)))
                 if op["in"] != 0:  # the input batch needs no gradient
                     acc(op["in"], conv2d_backward_data(dy, self._p(params, i, "w"), a.shape[1:3],
-                                                       op["stride"], op["pad"]))
+                                                       op["stride"], _op_pads(op)))
             elif kind == "fc":
                 a2 = a.reshape(a.shape[0], -1)
                 dy2 = dy.reshape(dy.shape[0], -1)
@@ -376,6 +430,8 @@ class Net:
                 acc(op["in"], np.where(relu_mask(a), dy, 0.0))
             elif kind == "maxpool":
                 acc(op["in"], maxpool_backward(dy, cache[i], a.shape, op["r"], op["s"], op["stride"], op["pad"]))
+            elif kind == "avgpool":
+                acc(op["in"], avgpool_backward(dy, a.shape, op["r"], op["s"], op["stride"], op["pad"]))
             elif kind == "gap":
                 hw = a.shape[1] * a.shape[2]
                 acc(op["in"], np.broadcast_to(dy / hw, a.shape))
@@ -399,6 +455,11 @@ class Net:
         """One full iteration: (loss, gradient, updated parameters)."""
         loss, grads = self.loss_and_grads(x, y, params)
         return loss, grads, sgd(params, grads, lr)
+
+
+def _op_pads(op):
+    """(row, column) padding of a conv op; "pad_w" defaults to "pad"."""
+    return op["pad"], op.get("pad_w", op["pad"])
 
 
 def flops_per_image(net):

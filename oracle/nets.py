@@ -39,7 +39,10 @@ class _Builder:
         return len(self.ops)  # tensor id of the output
 
     def conv(self, inp, k, r, stride=1, pad=0, bias=True):
-        return self.add("conv", inp, k=k, r=r, s=r, stride=stride, pad=pad, bias=bias)
+        """r: filter size, or (rows, columns); pad: padding, or (rows, columns)."""
+        rr, ss = r if isinstance(r, tuple) else (r, r)
+        ph, pw = pad if isinstance(pad, tuple) else (pad, pad)
+        return self.add("conv", inp, k=k, r=rr, s=ss, stride=stride, pad=ph, pad_w=pw, bias=bias)
 
     def fc(self, inp, out, bias=True):
         return self.add("fc", inp, out=out, bias=bias)
@@ -233,8 +236,105 @@ def googlenet():
     return {"name": "googlenet", "ops": b.ops, "hwc": (224, 224, 3), "classes": 1000}
 
 
+def inception_v4():
+    """Inception-v4 (stem, 4 x Inception-A, Reduction-A, 7 x Inception-B,
+    Reduction-B, 3 x Inception-C, global average pooling, FC 1536 -> 1000) on
+    299 x 299 inputs.  Every convolution is bias-free and followed by BN and
+    ReLU; "V" convolutions and pools are unpadded, the others keep the size
+    (a 1 x 7 filter pads 3 columns, a 7 x 1 filter 3 rows).  The pooling
+    branch of modules A, B and C is a 3 x 3 / 1 average pool padded by one,
+    averaging the in-image taps only.  No dropout, no auxiliary head.
+
+    Planner layers follow depth: inside a module, the convolutions at the same
+    distance from the module input form one layer (in the order of the
+    branches in the concatenation), a pool that opens a branch joins the
+    layer before it, and the concatenation joins the module's last layer.
+    Operations are listed layer by layer.
+    """
+    b = _Builder()
+
+    def cbr(inp, k, r, stride=1, pad=0):
+        return b.add("relu", b.add("bn", b.conv(inp, k, r, stride=stride, pad=pad, bias=False)))
+
+    def module(t, branches, tail=None):
+        """branches: per branch a list of steps, each ("conv", k, r, stride, pad) or
+        ("avg",) or ("max",); a step may be ("split", [conv, conv]) to end the
+        branch in parallel convs."""
+        heads = [t] * len(branches)
+        outs = [None] * len(branches)
+        pos = [0] * len(branches)
+        while any(pos[i] < len(br) for i, br in enumerate(branches)):
+            # pools are parameter-less: they join the layer that is open
+            for i, br in enumerate(branches):
+                while pos[i] < len(br) and br[pos[i]][0] in ("avg", "max"):
+                    if br[pos[i]][0] == "avg":
+                        heads[i] = b.add("avgpool", heads[i], r=3, s=3, stride=1, pad=1)
+                    else:
+                        heads[i] = b.add("maxpool", heads[i], r=3, s=3, stride=2, pad=0)
+                    pos[i] += 1
+                    if pos[i] == len(br):
+                        outs[i] = [heads[i]]
+            if all(pos[i] == len(br) for i, br in enumerate(branches)):
+                break
+            b.new_layer()
+            for i, br in enumerate(branches):
+                if pos[i] >= len(br):
+                    continue
+                step = br[pos[i]]
+                if step[0] == "split":
+                    outs[i] = [cbr(heads[i], *c) for c in step[1]]
+                else:
+                    heads[i] = cbr(heads[i], *step[1:])
+                    if pos[i] + 1 == len(br):
+                        outs[i] = [heads[i]]
+                pos[i] += 1
+        parts = [o for out in outs for o in out]
+        return b.add("concat", parts[0], others=parts[1:])
+
+    b.new_layer()
+    t = cbr(0, 32, 3, stride=2)
+    b.new_layer()
+    t = cbr(t, 32, 3)
+    b.new_layer()
+    t = cbr(t, 64, 3, pad=1)
+    t = module(t, [[("max",)], [("conv", 96, 3, 2, 0)]])
+    t = module(t, [[("conv", 64, 1), ("conv", 96, 3)],
+                   [("conv", 64, 1), ("conv", 64, (7, 1), 1, (3, 0)), ("conv", 64, (1, 7), 1, (0, 3)),
+                    ("conv", 96, 3)]])
+    t = module(t, [[("conv", 192, 3, 2, 0)], [("max",)]])
+    for _ in range(4):
+        t = module(t, [[("avg",), ("conv", 96, 1)],
+                       [("conv", 96, 1)],
+                       [("conv", 64, 1), ("conv", 96, 3, 1, 1)],
+                       [("conv", 64, 1), ("conv", 96, 3, 1, 1), ("conv", 96, 3, 1, 1)]])
+    t = module(t, [[("max",)],
+                   [("conv", 384, 3, 2, 0)],
+                   [("conv", 192, 1), ("conv", 224, 3, 1, 1), ("conv", 256, 3, 2, 0)]])
+    for _ in range(7):
+        t = module(t, [[("avg",), ("conv", 128, 1)],
+                       [("conv", 384, 1)],
+                       [("conv", 192, 1), ("conv", 224, (1, 7), 1, (0, 3)), ("conv", 256, (7, 1), 1, (3, 0))],
+                       [("conv", 192, 1), ("conv", 192, (1, 7), 1, (0, 3)), ("conv", 224, (7, 1), 1, (3, 0)),
+                        ("conv", 224, (1, 7), 1, (0, 3)), ("conv", 256, (7, 1), 1, (3, 0))]])
+    t = module(t, [[("max",)],
+                   [("conv", 192, 1), ("conv", 192, 3, 2, 0)],
+                   [("conv", 256, 1), ("conv", 256, (1, 7), 1, (0, 3)), ("conv", 320, (7, 1), 1, (3, 0)),
+                    ("conv", 320, 3, 2, 0)]])
+    split = ("split", [(256, (1, 3), 1, (0, 1)), (256, (3, 1), 1, (1, 0))])
+    for _ in range(3):
+        t = module(t, [[("avg",), ("conv", 256, 1)],
+                       [("conv", 256, 1)],
+                       [("conv", 384, 1), split],
+                       [("conv", 384, 1), ("conv", 448, (1, 3), 1, (0, 1)), ("conv", 512, (3, 1), 1, (1, 0)),
+                        split]])
+    t = b.add("gap", t)
+    b.new_layer()
+    b.fc(t, 1000)
+    return {"name": "inception_v4", "ops": b.ops, "hwc": (299, 299, 3), "classes": 1000}
+
+
 NETS = {"tiny": tiny, "alexnet": alexnet, "resnet18": resnet18_small, "vgg16": vgg16, "resnet50": resnet50,
-        "googlenet": googlenet, "vgg19": vgg19, "resnet152": resnet152}
+        "googlenet": googlenet, "vgg19": vgg19, "resnet152": resnet152, "inception_v4": inception_v4}
 
 
 def get(name):

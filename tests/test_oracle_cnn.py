@@ -57,6 +57,74 @@ def test_conv_against_torch(shape):
     np.testing.assert_allclose(dw, wt.grad.numpy().transpose(0, 2, 3, 1), rtol=1e-11, atol=1e-11)
 
 
+@pytest.mark.parametrize("shape", [
+    # N, H, W, C, K, R, S, stride, pad rows, pad columns
+    (2, 9, 8, 3, 5, 1, 7, 1, 0, 3),
+    (2, 9, 8, 4, 3, 7, 1, 1, 3, 0),
+    (2, 11, 10, 3, 4, 1, 3, 2, 0, 1),
+    (1, 8, 9, 2, 3, 3, 1, 1, 1, 0),
+    (2, 7, 7, 3, 2, 3, 5, 2, 1, 2),
+    (1, 7, 9, 2, 3, 3, 3, 2, 0, 0),
+])
+def test_conv_asymmetric_against_torch(shape):
+    """Rectangular filters with separate row and column padding (the 1 x n / n x 1 convs)."""
+    N, H, W, C, K, R, S, st, ph, pw = shape
+    x = synth.random_tensor(21, (N, H, W, C)).astype(np.float64)
+    w = synth.random_tensor(22, (K, R, S, C)).astype(np.float64)
+    b = synth.random_tensor(23, (K,)).astype(np.float64)
+    y = cnn.conv2d_forward(x, w, b, st, (ph, pw))
+    xt = _nchw(x).requires_grad_(True)
+    wt = torch.from_numpy(np.ascontiguousarray(w.transpose(0, 3, 1, 2))).requires_grad_(True)
+    yt = torch.nn.functional.conv2d(xt, wt, torch.from_numpy(b), stride=st, padding=(ph, pw))
+    np.testing.assert_allclose(y, _nhwc(yt), rtol=1e-12, atol=1e-12)
+    dy = synth.random_tensor(24, y.shape).astype(np.float64)
+    yt.backward(_nchw(dy))
+    dx = cnn.conv2d_backward_data(dy, w, (H, W), st, (ph, pw))
+    dw = cnn.conv2d_backward_filter(x, dy, (R, S), st, (ph, pw))
+    np.testing.assert_allclose(dx, _nhwc(xt.grad), rtol=1e-11, atol=1e-11)
+    np.testing.assert_allclose(dw, wt.grad.numpy().transpose(0, 2, 3, 1), rtol=1e-11, atol=1e-11)
+    # the sampled evaluations follow the same geometry
+    geom = (N, H, W, C, K, R, S, st, ph, pw)
+    idx = np.array([[n, p, q, k] for n in range(N) for p in range(y.shape[1]) for q in range(y.shape[2])
+                    for k in range(K)][::3])
+    got = cnn.conv2d_samples("fwd", geom, x.astype(np.float32), w.astype(np.float32), idx,
+                             bias=b.astype(np.float32))
+    ref = cnn.conv2d_forward(x.astype(np.float32), w.astype(np.float32), b.astype(np.float32), st, (ph, pw))
+    np.testing.assert_allclose(got, ref[tuple(idx.T)], rtol=1e-13, atol=1e-13)
+
+
+@pytest.mark.parametrize("cfg", [(3, 1, 1, 7, 7), (3, 1, 1, 5, 8), (2, 2, 0, 8, 6), (3, 2, 1, 9, 9), (5, 3, 2, 11, 10)])
+def test_avgpool_against_torch(cfg):
+    """Average pooling, padded taps left out of the count."""
+    r, st, pad, H, W = cfg
+    x = synth.random_tensor(25, (2, H, W, 3)).astype(np.float64)
+    y = cnn.avgpool_forward(x, r, r, st, pad)
+    xt = _nchw(x).requires_grad_(True)
+    yt = torch.nn.functional.avg_pool2d(xt, r, st, pad, count_include_pad=False)
+    np.testing.assert_allclose(y, _nhwc(yt), rtol=1e-13, atol=1e-13)
+    dy = synth.random_tensor(26, y.shape).astype(np.float64)
+    yt.backward(_nchw(dy))
+    dx = cnn.avgpool_backward(dy, x.shape, r, r, st, pad)
+    np.testing.assert_allclose(dx, _nhwc(xt.grad), rtol=1e-13, atol=1e-13)
+
+
+def test_avgpool_closed_forms():
+    """A constant image pools to itself (corners included, since padding is not
+    counted); each window spreads its gradient with weights summing to one, so
+    the input gradient sums to the output gradient's sum; with a 1 x 1 window
+    the pool is the identity."""
+    x = np.full((2, 6, 5, 3), 2.5)
+    np.testing.assert_array_equal(cnn.avgpool_forward(x, 3, 3, 1, 1), x)
+    dy = synth.random_tensor(27, (2, 6, 5, 3)).astype(np.float64)
+    dx = cnn.avgpool_backward(dy, x.shape, 3, 3, 1, 1)
+    np.testing.assert_allclose(dx.sum(axis=(1, 2)), dy.sum(axis=(1, 2)), rtol=1e-13)
+    # the corner input is covered by 4 windows of 4, 6, 6 and 9 in-image taps
+    w = dy[0, 0, 0, 0] / 4 + dy[0, 0, 1, 0] / 6 + dy[0, 1, 0, 0] / 6 + dy[0, 1, 1, 0] / 9
+    assert dx[0, 0, 0, 0] == pytest.approx(w, rel=1e-14)
+    x = synth.random_tensor(28, (1, 4, 4, 2)).astype(np.float64)
+    np.testing.assert_array_equal(cnn.avgpool_forward(x, 1, 1, 1, 0), x)
+
+
 @pytest.mark.parametrize("cfg", [(2, 2, 0, 8), (3, 2, 0, 13), (3, 2, 1, 12), (3, 2, 0, 55)])
 def test_maxpool_against_torch(cfg):
     r, st, pad, H = cfg
@@ -169,6 +237,55 @@ def _mini_inception():
     return {"name": "mini_inception", "ops": ops, "hwc": (7, 7, 3), "classes": 4}
 
 
+def _mini_inception_v4():
+    """Inception-v4 operators at small size: unpadded stride-2 conv and max-pool
+    reduction, 1 x 3 / 3 x 1 and 1 x 7 / 7 x 1 convs with one-sided padding, an
+    average-pool branch, a split into parallel convs, BN + ReLU after every
+    conv, concatenation, global average pooling."""
+    ops = []
+
+    def add(kind, inp, layer, **kw):
+        d = {"op": kind, "in": inp, "layer": layer}
+        d.update(kw)
+        ops.append(d)
+        return len(ops)
+
+    def cbr(inp, layer, k, r, s, stride, ph, pw):
+        t = add("conv", inp, layer, k=k, r=r, s=s, stride=stride, pad=ph, pad_w=pw, bias=False)
+        return add("relu", add("bn", t, layer), layer)
+
+    t = cbr(0, 1, 5, 3, 3, 2, 0, 0)                        # 11x11 -> 5x5
+    a = add("avgpool", t, 2, r=3, s=3, stride=1, pad=1)
+    a = cbr(a, 2, 3, 1, 1, 1, 0, 0)
+    u = cbr(t, 2, 4, 1, 1, 1, 0, 0)
+    v = cbr(t, 2, 3, 1, 1, 1, 0, 0)
+    u = cbr(u, 3, 4, 1, 7, 1, 0, 3)
+    v1 = cbr(v, 3, 2, 1, 3, 1, 0, 1)
+    v2 = cbr(v, 3, 2, 3, 1, 1, 1, 0)
+    u = cbr(u, 4, 3, 7, 1, 1, 3, 0)
+    t = add("concat", a, 4, others=[u, v1, v2])
+    m = add("maxpool", t, 5, r=3, s=3, stride=2, pad=0)     # 5x5 -> 2x2
+    c = cbr(t, 5, 4, 3, 3, 2, 0, 0)
+    t = add("concat", m, 5, others=[c])
+    t = add("gap", t, 5)
+    add("fc", t, 6, out=4, bias=True)
+    return {"name": "mini_inception_v4", "ops": ops, "hwc": (11, 11, 3), "classes": 4}
+
+
+def test_finite_differences_inception_v4_ops():
+    _fd_check(_mini_inception_v4(), 2, 9, 100, 1e-6)
+
+
+def test_inception_v4_ops_against_torch():
+    spec = _mini_inception_v4()
+    net = cnn.Net(spec, 3)
+    x, y, p = synth.cnn_inputs(10, 3, spec["hwc"], spec["classes"], net.param_specs)
+    loss, g = net.loss_and_grads(x, y, p)
+    lt, gt = _torch_loss(spec, net, x, y, p)
+    assert abs(loss - lt) <= 1e-12 * max(1.0, abs(lt))
+    np.testing.assert_allclose(g, gt, rtol=1e-9, atol=1e-12 * np.abs(gt).max())
+
+
 def test_finite_differences_inception():
     _fd_check(_mini_inception(), 2, 4, 80, 1e-6)
 
@@ -235,13 +352,14 @@ def test_sgd_closed_form():
 
 @pytest.mark.parametrize("name,count", [("tiny", 67642), ("alexnet", 61100840), ("resnet18", 11173962),
                                         ("vgg16", 138357544), ("resnet50", 25557032), ("googlenet", 6998552),
-                                        ("vgg19", 143667240), ("resnet152", 60192808)])
+                                        ("vgg19", 143667240), ("resnet152", 60192808),
+                                        ("inception_v4", 42679816)])
 def test_parameter_counts(name, count):
     net = cnn.Net(nets.get(name), 1)
     assert net.n_params == count
     assert sum(c for _, c in net.layer_ranges.values()) == count
     assert {"tiny": 4, "alexnet": 8, "resnet18": 18, "vgg16": 16, "resnet50": 50, "googlenet": 22, "vgg19": 19,
-            "resnet152": 152}[name] == net.L
+            "resnet152": 152, "inception_v4": 76}[name] == net.L
 
 
 def _torch_loss(spec, net, x, y, p):

@@ -28,7 +28,7 @@ def loss_and_grads(spec, net, x, y, p, dtype=torch.float64):
         if k == "conv":
             w = prm(i, "w").permute(0, 3, 1, 2)
             b = prm(i, "b") if op["bias"] else None
-            o = F.conv2d(a, w, b, stride=op["stride"], padding=op["pad"])
+            o = F.conv2d(a, w, b, stride=op["stride"], padding=(op["pad"], op.get("pad_w", op["pad"])))
         elif k == "fc":
             flat = a.permute(0, 2, 3, 1).reshape(a.shape[0], -1)   # NHWC flatten
             o = F.linear(flat, prm(i, "w"), prm(i, "b") if op["bias"] else None)
@@ -39,6 +39,8 @@ def loss_and_grads(spec, net, x, y, p, dtype=torch.float64):
             o = F.relu(a)
         elif k == "maxpool":
             o = F.max_pool2d(a, op["r"], op["stride"], op["pad"])
+        elif k == "avgpool":
+            o = F.avg_pool2d(a, (op["r"], op["s"]), op["stride"], op["pad"], count_include_pad=False)
         elif k == "gap":
             o = F.adaptive_avg_pool2d(a, 1)
         elif k == "add":
