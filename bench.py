@@ -39,7 +39,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="vgg16", choices=["tiny", "alexnet", "resnet18", "vgg16", "resnet50", "googlenet", "vgg19",
-                                                          "resnet152"])
+                                                          "resnet152", "inception_v4"])
     ap.add_argument("--batch", type=int, default=0, help="0 = the workload's own batch")
     ap.add_argument("--link-gbps", default="100", help="emulated link in Gb/s, or 'pcie' for unpaced copies")
     ap.add_argument("--dt-emul-ms", type=float, default=0.0)
@@ -91,8 +91,8 @@ def measure_convs(D, PN, ops, hwc, batch, reps=3):
     ms_total = 0.0
     per = []
     for _i, g, first in geoms:
-        n, h, w, c, k, r, ss, st, pad = g
-        P, Q = (h + 2 * pad - r) // st + 1, (w + 2 * pad - ss) // st + 1
+        n, h, w, c, k, r, ss, st, pad, pad_w = g
+        P, Q = (h + 2 * pad - r) // st + 1, (w + 2 * pad_w - ss) // st + 1
         sh = D.ConvShape(*g)
         wsb = max(D.lib().dc_conv2d_workspace_bytes(ctypes.byref(sh)), 256)
         ws = torch.empty(wsb + 256, dtype=torch.uint8, device="cuda")

@@ -62,7 +62,8 @@ enum {
     DC_OP_MAXPOOL = 5, /* r x s window, stride, padding; padded positions never win */
     DC_OP_GAP = 6,     /* global average pooling to N x 1 x 1 x C */
     DC_OP_ADD = 7,     /* elementwise sum of in0 and in1 (residual connection) */
-    DC_OP_CONCAT = 8   /* channel concatenation of in0, in1 and, if not -1, in2 and in3 */
+    DC_OP_CONCAT = 8,  /* channel concatenation of in0, in1 and, if not -1, in2 and in3 */
+    DC_OP_AVGPOOL = 9  /* r x s window, stride, padding; the mean over the window's positions inside the input */
 };
 
 /*
@@ -84,12 +85,13 @@ typedef struct dc_op_desc {
     int32_t in0;     /* input tensor id (< own id) */
     int32_t in1;     /* DC_OP_ADD / DC_OP_CONCAT: second input tensor id; otherwise -1 */
     int32_t out_ch;  /* CONV: output channels; FC: output features */
-    int32_t r, s;    /* CONV / MAXPOOL window */
-    int32_t stride;  /* CONV / MAXPOOL */
-    int32_t pad;     /* CONV / MAXPOOL */
+    int32_t r, s;    /* CONV / MAXPOOL / AVGPOOL window (rows, columns) */
+    int32_t stride;  /* CONV / MAXPOOL / AVGPOOL */
+    int32_t pad;     /* CONV / MAXPOOL / AVGPOOL: zero rows above and below */
     int32_t bias;    /* CONV / FC: 1 if the op has a bias */
     int32_t in2;     /* DC_OP_CONCAT: third input tensor id or -1; otherwise -1 */
     int32_t in3;     /* DC_OP_CONCAT: fourth input tensor id or -1; otherwise -1 */
+    int32_t pad_w;   /* CONV: zero columns left and right (pad_w < s); pools: equal to pad */
 } dc_op_desc;
 
 typedef struct dc_model dc_model;

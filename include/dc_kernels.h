@@ -21,17 +21,18 @@ extern "C" {
 #endif
 
 /* Convolution geometry: input n x h x w x c, k filters of r x s x c, stride,
- * zero padding.  Output p x q with p = (h + 2 pad - r) / stride + 1.  An FC
- * layer of in -> out features is the case h = w = r = s = 1, c = in, k = out,
- * stride = 1, pad = 0. */
+ * `pad` zero rows above and below and `pad_w` zero columns left and right
+ * (pad < r, pad_w < s).  Output p x q with p = (h + 2 pad - r) / stride + 1,
+ * q = (w + 2 pad_w - s) / stride + 1.  An FC layer of in -> out features is
+ * the case h = w = r = s = 1, c = in, k = out, stride = 1, pad = pad_w = 0. */
 typedef struct dc_conv_shape {
-    int32_t n, h, w, c, k, r, s, stride, pad;
+    int32_t n, h, w, c, k, r, s, stride, pad, pad_w;
 } dc_conv_shape;
 
 /* Scratch needed by the three conv passes of this shape (split-K partials). */
 size_t dc_conv2d_workspace_bytes(const dc_conv_shape *sh);
 
-/* y[n,p,q,k] = bias[k] + sum over r, s, c of x[n, p*stride+r-pad, q*stride+s-pad, c] * w[k,r,s,c],
+/* y[n,p,q,k] = bias[k] + sum over r, s, c of x[n, p*stride+r-pad, q*stride+s-pad_w, c] * w[k,r,s,c],
  * then max(., 0) if relu; implicit GEMM on fp32 MFMA.  bias may be NULL. */
 int dc_conv2d_forward(const dc_conv_shape *sh, const float *x, const float *w, const float *bias,
                       int relu, float *y, void *ws, size_t ws_bytes, void *stream);
@@ -41,7 +42,7 @@ int dc_conv2d_forward(const dc_conv_shape *sh, const float *x, const float *w, c
 int dc_conv2d_backward_data(const dc_conv_shape *sh, const float *dy, const float *w,
                             int accumulate, float *dx, void *ws, size_t ws_bytes, void *stream);
 
-/* dw[k,r,s,c] = sum over n, p, q of dy[n,p,q,k] * x[n, p*stride+r-pad, q*stride+s-pad, c];
+/* dw[k,r,s,c] = sum over n, p, q of dy[n,p,q,k] * x[n, p*stride+r-pad, q*stride+s-pad_w, c];
  * dbias[k] = sum over n, p, q of dy[n,p,q,k] if dbias != NULL.  Deterministic
  * (fixed-order split-K). */
 int dc_conv2d_backward_filter(const dc_conv_shape *sh, const float *x, const float *dy,
@@ -69,6 +70,13 @@ int dc_maxpool_forward(const dc_pool_shape *sh, const float *x, float *y, uint8_
 /* dx (+)= the sum of dy over the windows whose argmax is this element. */
 int dc_maxpool_backward(const dc_pool_shape *sh, const float *dy, const uint8_t *arg,
                         int accumulate, float *dx, void *stream);
+
+/* Average pooling: y = the mean of x over the window positions that lie
+ * inside the input (padded positions are not counted).  Backward: dx (+)=
+ * the sum, over the windows containing each element, of dy / that window's
+ * count.  Element counts must stay below 2^31 (else DC_EINVAL). */
+int dc_avgpool_forward(const dc_pool_shape *sh, const float *x, float *y, void *stream);
+int dc_avgpool_backward(const dc_pool_shape *sh, const float *dy, int accumulate, float *dx, void *stream);
 
 /* Global average pooling: y[n,c] = mean over hw of x[n,hw,c]; backward spreads dy / hw. */
 int dc_gap_forward(int32_t n, int32_t hw, int32_t c, const float *x, float *y, void *stream);

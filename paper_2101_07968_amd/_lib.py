@@ -16,7 +16,7 @@ import numpy as np
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libdc.so")
 
 DC_OK, DC_EINVAL, DC_EHIP, DC_ENOMEM, DC_ESTATE, DC_ETIMEOUT = range(6)
-DC_OP_CONV, DC_OP_FC, DC_OP_BN, DC_OP_RELU, DC_OP_MAXPOOL, DC_OP_GAP, DC_OP_ADD, DC_OP_CONCAT = range(1, 9)
+DC_OP_CONV, DC_OP_FC, DC_OP_BN, DC_OP_RELU, DC_OP_MAXPOOL, DC_OP_GAP, DC_OP_ADD, DC_OP_CONCAT, DC_OP_AVGPOOL = range(1, 10)
 DC_OPT_LR, DC_OPT_TIMELINE, DC_OPT_TIMEOUT_S, DC_OPT_SGD_THREADS = range(1, 5)
 
 c_i32, c_i64, c_f32, c_f64, c_sz, c_vp = (ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_double,
@@ -30,13 +30,25 @@ class DcError(RuntimeError):
 
 
 class OpDesc(ctypes.Structure):
+    """dc_op_desc; pad_w defaults to pad (square padding) when not given."""
     _fields_ = [("kind", c_i32), ("layer", c_i32), ("in0", c_i32), ("in1", c_i32), ("out_ch", c_i32),
                 ("r", c_i32), ("s", c_i32), ("stride", c_i32), ("pad", c_i32), ("bias", c_i32),
-                ("in2", c_i32), ("in3", c_i32)]
+                ("in2", c_i32), ("in3", c_i32), ("pad_w", c_i32)]
+
+    def __init__(self, *args, **kw):
+        super().__init__(*args, **kw)
+        if len(args) < 13 and "pad_w" not in kw:
+            self.pad_w = self.pad
 
 
 class ConvShape(ctypes.Structure):
-    _fields_ = [(n, c_i32) for n in ("n", "h", "w", "c", "k", "r", "s", "stride", "pad")]
+    """dc_conv_shape; pad_w defaults to pad (square padding) when not given."""
+    _fields_ = [(n, c_i32) for n in ("n", "h", "w", "c", "k", "r", "s", "stride", "pad", "pad_w")]
+
+    def __init__(self, *args, **kw):
+        super().__init__(*args, **kw)
+        if len(args) < 10 and "pad_w" not in kw:
+            self.pad_w = self.pad
 
 
 class PoolShape(ctypes.Structure):
@@ -104,6 +116,8 @@ _SIGS = {
     "dc_relu_backward": (ctypes.c_int, [c_vp, c_vp, ctypes.c_int, c_vp, c_i64, c_vp]),
     "dc_maxpool_forward": (ctypes.c_int, [_P(PoolShape), c_vp, c_vp, c_vp, c_vp]),
     "dc_maxpool_backward": (ctypes.c_int, [_P(PoolShape), c_vp, c_vp, ctypes.c_int, c_vp, c_vp]),
+    "dc_avgpool_forward": (ctypes.c_int, [_P(PoolShape), c_vp, c_vp, c_vp]),
+    "dc_avgpool_backward": (ctypes.c_int, [_P(PoolShape), c_vp, ctypes.c_int, c_vp, c_vp]),
     "dc_gap_forward": (ctypes.c_int, [c_i32, c_i32, c_i32, c_vp, c_vp, c_vp]),
     "dc_gap_backward": (ctypes.c_int, [c_i32, c_i32, c_i32, c_vp, ctypes.c_int, c_vp, c_vp]),
     "dc_add_forward": (ctypes.c_int, [c_vp, c_vp, ctypes.c_int, c_vp, c_i64, c_vp]),

@@ -244,6 +244,23 @@ extern "C" int dc_maxpool_backward(const dc_pool_shape *sh, const float *dy, con
     return maxpool_backward(*sh, dy, arg, accumulate, dx, static_cast<hipStream_t>(stream));
 }
 
+extern "C" int dc_avgpool_forward(const dc_pool_shape *sh, const float *x, float *y, void *stream) {
+    clear_error();
+    DC_TRY(pool_check(sh));
+    if (sh->n > 0 && (!x || !y))
+        return fail(DC_EINVAL, "NULL tensor");
+    return avgpool_forward(*sh, x, y, static_cast<hipStream_t>(stream));
+}
+
+extern "C" int dc_avgpool_backward(const dc_pool_shape *sh, const float *dy, int accumulate, float *dx,
+                                   void *stream) {
+    clear_error();
+    DC_TRY(pool_check(sh));
+    if (sh->n > 0 && (!dy || !dx))
+        return fail(DC_EINVAL, "NULL tensor");
+    return avgpool_backward(*sh, dy, accumulate, dx, static_cast<hipStream_t>(stream));
+}
+
 extern "C" int dc_gap_forward(int32_t n, int32_t hw, int32_t c, const float *x, float *y, void *stream) {
     clear_error();
     if (n < 0 || hw < 1 || c < 1 || (n > 0 && (!x || !y)))

@@ -34,7 +34,7 @@ void clear_error();
 enum Pass { PASS_FWD = 0, PASS_DGRAD = 1, PASS_WGRAD = 2 };
 
 struct ConvGeom {
-    int N, H, W, C, K, R, S, st, pad, P, Q;
+    int N, H, W, C, K, R, S, st, pad, pad_w, P, Q; // pad: rows; pad_w: columns
 };
 
 // Launch configuration of one implicit-GEMM pass, chosen on the host.
@@ -82,6 +82,8 @@ int copy_grad(const float *dy, int accumulate, float *dx, int64_t n, hipStream_t
 int concat_forward(int64_t rows, int c_in, int c_out, int off, const float *x, float *y, hipStream_t s);
 int concat_backward(int64_t rows, int c_in, int c_out, int off, const float *dy, int accumulate, float *dx,
                     hipStream_t s);
+int avgpool_forward(const dc_pool_shape &sh, const float *x, float *y, hipStream_t s);
+int avgpool_backward(const dc_pool_shape &sh, const float *dy, int accumulate, float *dx, hipStream_t s);
 int maxpool_forward(const dc_pool_shape &sh, const float *x, float *y, uint8_t *arg,
                     hipStream_t s);
 int maxpool_backward(const dc_pool_shape &sh, const float *dy, const uint8_t *arg, int accumulate,

@@ -14,6 +14,7 @@
 #include <climits>
 #include <cstdint>
 #include <numeric>
+#include <type_traits>
 
 namespace dc {
 namespace {
@@ -274,6 +275,91 @@ __global__ void maxpool_bwd4_kernel(dc_pool_shape sh, int P, int Q, int c4, int 
             g.x = o.x + g.x; g.y = o.y + g.y; g.z = o.z + g.z; g.w = o.w + g.w;
         }
         dx[e] = g;
+    }
+}
+
+// Average pooling over the window positions that lie inside the input (the
+// padded ones are not counted).  V channels per thread (4 when c % 4 == 0 and
+// the tensors are 16-byte aligned); the host keeps every element count below
+// 2^31.  Backward gathers, for each input element, dy / count of every
+// window that contains it, in window order: deterministic, no atomics.
+__device__ __forceinline__ int pool_count(const dc_pool_shape &sh, int p, int q) {
+    const int h0 = p * sh.stride - sh.pad, w0 = q * sh.stride - sh.pad;
+    const int nh = min(h0 + sh.r, sh.h) - max(h0, 0), nw = min(w0 + sh.s, sh.w) - max(w0, 0);
+    return max(nh, 0) * max(nw, 0);
+}
+
+template <int V>
+__global__ void avgpool_fwd_kernel(dc_pool_shape sh, int P, int Q, int cv, int total, const float *__restrict__ x,
+                                   float *__restrict__ y) {
+    using T = typename std::conditional<V == 4, float4, float>::type;
+    const T *xv = reinterpret_cast<const T *>(x);
+    T *yv = reinterpret_cast<T *>(y);
+    for (int e = blockIdx.x * blockDim.x + threadIdx.x; e < total; e += gridDim.x * blockDim.x) {
+        const int qc = e % cv, pix = e / cv;
+        const int q = pix % Q, t = pix / Q;
+        const int p = t % P, n = t / P;
+        float acc[4] = {0.f, 0.f, 0.f, 0.f};
+        for (int r = 0; r < sh.r; ++r) {
+            const int h = p * sh.stride + r - sh.pad;
+            if ((unsigned)h >= (unsigned)sh.h)
+                continue;
+            for (int s = 0; s < sh.s; ++s) {
+                const int w = q * sh.stride + s - sh.pad;
+                if ((unsigned)w >= (unsigned)sh.w)
+                    continue;
+                const T v = xv[((n * sh.h + h) * sh.w + w) * cv + qc];
+                if constexpr (V == 4) {
+                    acc[0] += v.x; acc[1] += v.y; acc[2] += v.z; acc[3] += v.w;
+                } else {
+                    acc[0] += v;
+                }
+            }
+        }
+        const float inv = 1.0f / (float)max(pool_count(sh, p, q), 1);
+        if constexpr (V == 4)
+            yv[e] = make_float4(acc[0] * inv, acc[1] * inv, acc[2] * inv, acc[3] * inv);
+        else
+            yv[e] = acc[0] * inv;
+    }
+}
+
+template <int V>
+__global__ void avgpool_bwd_kernel(dc_pool_shape sh, int P, int Q, int cv, int total, const float *__restrict__ dy,
+                                   int acc_in, float *__restrict__ dx) {
+    using T = typename std::conditional<V == 4, float4, float>::type;
+    const T *dv = reinterpret_cast<const T *>(dy);
+    T *xv = reinterpret_cast<T *>(dx);
+    for (int e = blockIdx.x * blockDim.x + threadIdx.x; e < total; e += gridDim.x * blockDim.x) {
+        const int qc = e % cv, pix = e / cv;
+        const int w = pix % sh.w, t = pix / sh.w;
+        const int h = t % sh.h, n = t / sh.h;
+        const int hp = h + sh.pad, wp = w + sh.pad;
+        const int p_lo = hp - sh.r + 1 > 0 ? (hp - sh.r + 1 + sh.stride - 1) / sh.stride : 0;
+        const int p_hi = min(P - 1, hp / sh.stride);
+        const int q_lo = wp - sh.s + 1 > 0 ? (wp - sh.s + 1 + sh.stride - 1) / sh.stride : 0;
+        const int q_hi = min(Q - 1, wp / sh.stride);
+        float g[4] = {0.f, 0.f, 0.f, 0.f};
+        for (int p = p_lo; p <= p_hi; ++p)
+            for (int q = q_lo; q <= q_hi; ++q) {
+                const float inv = 1.0f / (float)max(pool_count(sh, p, q), 1);
+                const T d = dv[((n * P + p) * Q + q) * cv + qc];
+                if constexpr (V == 4) {
+                    g[0] += d.x * inv; g[1] += d.y * inv; g[2] += d.z * inv; g[3] += d.w * inv;
+                } else {
+                    g[0] += d * inv;
+                }
+            }
+        if constexpr (V == 4) {
+            float4 o = make_float4(g[0], g[1], g[2], g[3]);
+            if (acc_in) {
+                const float4 prev = xv[e];
+                o.x += prev.x; o.y += prev.y; o.z += prev.z; o.w += prev.w;
+            }
+            xv[e] = o;
+        } else {
+            xv[e] = acc_in ? xv[e] + g[0] : g[0];
+        }
     }
 }
 
@@ -813,6 +899,42 @@ int maxpool_backward(const dc_pool_shape &sh, const float *dy, const uint8_t *ar
         hipLaunchKernelGGL(maxpool_bwd_kernel, dim3(ew_blocks(total)), dim3(EW_THREADS), 0, s, sh, P, Q, dy, arg,
                            accumulate, dx);
     }
+    DC_HIP(hipGetLastError());
+    return DC_OK;
+}
+
+int avgpool_forward(const dc_pool_shape &sh, const float *x, float *y, hipStream_t s) {
+    const int P = (sh.h + 2 * sh.pad - sh.r) / sh.stride + 1;
+    const int Q = (sh.w + 2 * sh.pad - sh.s) / sh.stride + 1;
+    const int64_t total = (int64_t)sh.n * P * Q * sh.c;
+    if (total <= 0)
+        return DC_OK;
+    if ((int64_t)sh.n * sh.h * sh.w * sh.c >= INT_MAX || total >= INT_MAX)
+        return fail(DC_EINVAL, "average pooling of %lld elements exceeds the 2^31 limit", (long long)total);
+    if (sh.c % 4 == 0 && ((uintptr_t)x & 15) == 0 && ((uintptr_t)y & 15) == 0)
+        hipLaunchKernelGGL(avgpool_fwd_kernel<4>, dim3(ew_blocks(total / 4)), dim3(EW_THREADS), 0, s, sh, P, Q,
+                           sh.c / 4, (int)(total / 4), x, y);
+    else
+        hipLaunchKernelGGL(avgpool_fwd_kernel<1>, dim3(ew_blocks(total)), dim3(EW_THREADS), 0, s, sh, P, Q, sh.c,
+                           (int)total, x, y);
+    DC_HIP(hipGetLastError());
+    return DC_OK;
+}
+
+int avgpool_backward(const dc_pool_shape &sh, const float *dy, int accumulate, float *dx, hipStream_t s) {
+    const int P = (sh.h + 2 * sh.pad - sh.r) / sh.stride + 1;
+    const int Q = (sh.w + 2 * sh.pad - sh.s) / sh.stride + 1;
+    const int64_t total = (int64_t)sh.n * sh.h * sh.w * sh.c;
+    if (total <= 0)
+        return DC_OK;
+    if (total >= INT_MAX || (int64_t)sh.n * P * Q * sh.c >= INT_MAX)
+        return fail(DC_EINVAL, "average pooling of %lld elements exceeds the 2^31 limit", (long long)total);
+    if (sh.c % 4 == 0 && ((uintptr_t)dy & 15) == 0 && ((uintptr_t)dx & 15) == 0)
+        hipLaunchKernelGGL(avgpool_bwd_kernel<4>, dim3(ew_blocks(total / 4)), dim3(EW_THREADS), 0, s, sh, P, Q,
+                           sh.c / 4, (int)(total / 4), dy, accumulate, dx);
+    else
+        hipLaunchKernelGGL(avgpool_bwd_kernel<1>, dim3(ew_blocks(total)), dim3(EW_THREADS), 0, s, sh, P, Q, sh.c,
+                           (int)total, dy, accumulate, dx);
     DC_HIP(hipGetLastError());
     return DC_OK;
 }

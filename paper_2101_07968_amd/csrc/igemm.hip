@@ -64,7 +64,7 @@ FDiv make_fdiv(uint32_t d) {
 }
 
 struct Args {
-    int N, H, W, C, K, R, S, st, pad, P, Q;
+    int N, H, W, C, K, R, S, st, pad, pad_w, P, Q;
     int M, Ng, Kg;          // FWD / WGRAD sizes; DGRAD: maxima over phases
     int tiles_m, tiles_n, tiles;
     int splits, kt_per_split, phases;
@@ -93,11 +93,11 @@ __device__ __forceinline__ Phase make_phase(const Args &a, int z) {
     ph.Hh = a.H > rh ? (a.H - rh + a.st - 1) / a.st : 0;
     ph.Wh = a.W > rw ? (a.W - rw + a.st - 1) / a.st : 0;
     ph.r0 = (rh + a.pad) % a.st;
-    ph.s0 = (rw + a.pad) % a.st;
+    ph.s0 = (rw + a.pad_w) % a.st;
     ph.Rt = ph.r0 < a.R ? (a.R - ph.r0 + a.st - 1) / a.st : 0;
     ph.St = ph.s0 < a.S ? (a.S - ph.s0 + a.st - 1) / a.st : 0;
     ph.dh = (rh + a.pad - ph.r0) / a.st;
-    ph.dw = (rw + a.pad - ph.s0) / a.st;
+    ph.dw = (rw + a.pad_w - ph.s0) / a.st;
     ph.M = a.N * ph.Hh * ph.Wh;
     ph.Kg = ph.Rt * ph.St * a.K;
     return ph;
@@ -248,7 +248,7 @@ __global__ __launch_bounds__(NTHR, TU ? 4 : 1) void igemm_kernel(Args a) {
                 int q = rem - p * a.Q;
                 a_n[f] = n;
                 a_h[f] = p * a.st - a.pad;
-                a_w[f] = q * a.st - a.pad;
+                a_w[f] = q * a.st - a.pad_w;
             } else {
                 int hw = ph.Hh * ph.Wh;
                 int n = hw ? mm / hw : 0;
@@ -339,7 +339,7 @@ __global__ __launch_bounds__(NTHR, TU ? 4 : 1) void igemm_kernel(Args a) {
             bq[f] = rem - pp * a.Q;
             bp[f] = pp;
             bhh[f] = pp * a.st - a.pad + b_r[0];
-            bww[f] = bq[f] * a.st - a.pad + b_s[0];
+            bww[f] = bq[f] * a.st - a.pad_w + b_s[0];
             boff[f] = ((n * a.H + bhh[f]) * a.W + bww[f]) * a.C + b_c[0];
         }
     };
@@ -585,7 +585,7 @@ __global__ __launch_bounds__(NTHR, TU ? 4 : 1) void igemm_kernel(Args a) {
                 int rem = m2 - n * a.P * a.Q;
                 int p = a.fQ.div(rem);
                 int q = rem - p * a.Q;
-                int hb = p * a.st - a.pad, wb = q * a.st - a.pad;
+                int hb = p * a.st - a.pad, wb = q * a.st - a.pad_w;
                 if (BV) {
                     int h = hb + b_r[0], w = wb + b_s[0];
                     bool ok = pok && b_cok[0] && (unsigned)h < (unsigned)a.H && (unsigned)w < (unsigned)a.W;
@@ -902,7 +902,7 @@ void launch_p(const Args &a, const GemmPlan &pl, int grid_x, hipStream_t s) {
 Args make_args(const ConvGeom &g, const GemmPlan &pl) {
     Args a{};
     a.N = g.N; a.H = g.H; a.W = g.W; a.C = g.C; a.K = g.K; a.R = g.R; a.S = g.S;
-    a.st = g.st; a.pad = g.pad; a.P = g.P; a.Q = g.Q;
+    a.st = g.st; a.pad = g.pad; a.pad_w = g.pad_w; a.P = g.P; a.Q = g.Q;
     a.M = pl.M; a.Ng = pl.Ng; a.Kg = pl.Kg;
     a.tiles_m = pl.tiles_m; a.tiles_n = pl.tiles_n; a.tiles = pl.tiles_m * pl.tiles_n;
     a.splits = pl.splits; a.kt_per_split = pl.kt_per_split; a.phases = pl.phases;
@@ -962,14 +962,14 @@ int run(const ConvGeom &g, const GemmPlan &pl, Args a, void *ws, hipStream_t s) 
 
 bool conv_geom_from_shape(const dc_conv_shape &sh, ConvGeom *g) {
     if (sh.n < 0 || sh.h < 1 || sh.w < 1 || sh.c < 1 || sh.k < 1 || sh.r < 1 || sh.s < 1 ||
-        sh.stride < 1 || sh.pad < 0 || sh.pad >= sh.r || sh.pad >= sh.s)
+        sh.stride < 1 || sh.pad < 0 || sh.pad >= sh.r || sh.pad_w < 0 || sh.pad_w >= sh.s)
         return false;
-    if (sh.h + 2 * sh.pad < sh.r || sh.w + 2 * sh.pad < sh.s)
+    if (sh.h + 2 * sh.pad < sh.r || sh.w + 2 * sh.pad_w < sh.s)
         return false;
     g->N = sh.n; g->H = sh.h; g->W = sh.w; g->C = sh.c; g->K = sh.k;
-    g->R = sh.r; g->S = sh.s; g->st = sh.stride; g->pad = sh.pad;
+    g->R = sh.r; g->S = sh.s; g->st = sh.stride; g->pad = sh.pad; g->pad_w = sh.pad_w;
     g->P = (sh.h + 2 * sh.pad - sh.r) / sh.stride + 1;
-    g->Q = (sh.w + 2 * sh.pad - sh.s) / sh.stride + 1;
+    g->Q = (sh.w + 2 * sh.pad_w - sh.s) / sh.stride + 1;
     // every index the kernels form must stay below 2^31
     int64_t big = std::max<int64_t>({(int64_t)sh.n * sh.h * sh.w * sh.c, (int64_t)sh.n * g->P * g->Q * sh.k,
                                      (int64_t)sh.k * sh.r * sh.s * sh.c});

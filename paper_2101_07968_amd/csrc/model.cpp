@@ -27,7 +27,7 @@ int check_desc(const dc_op_desc *ops, int n_ops, int batch, int in_h, int in_w, 
     int prev_layer = 0;
     for (int i = 0; i < n_ops; ++i) {
         const dc_op_desc &d = ops[i];
-        if (d.kind < DC_OP_CONV || d.kind > DC_OP_CONCAT)
+        if (d.kind < DC_OP_CONV || d.kind > DC_OP_AVGPOOL)
             return fail(DC_EINVAL, "op %d: unknown kind %d", i, d.kind);
         if (d.in0 < 0 || d.in0 > i)
             return fail(DC_EINVAL, "op %d: input tensor %d is not an earlier tensor", i, d.in0);
@@ -91,7 +91,7 @@ static int build_model(dc_model *m, const dc_op_desc *ops, int n_ops) {
         case DC_OP_FC: {
             dc_conv_shape sh;
             if (o.d.kind == DC_OP_CONV) {
-                sh = dc_conv_shape{in.n, in.h, in.w, in.c, o.d.out_ch, o.d.r, o.d.s, o.d.stride, o.d.pad};
+                sh = dc_conv_shape{in.n, in.h, in.w, in.c, o.d.out_ch, o.d.r, o.d.s, o.d.stride, o.d.pad, o.d.pad_w};
             } else {
                 sh = dc_conv_shape{in.n, 1, 1, in.h * in.w * in.c, o.d.out_ch, 1, 1, 1, 0};
             }
@@ -119,10 +119,12 @@ static int build_model(dc_model *m, const dc_op_desc *ops, int n_ops) {
             break;
         case DC_OP_RELU:
             break;
-        case DC_OP_MAXPOOL: {
+        case DC_OP_MAXPOOL:
+        case DC_OP_AVGPOOL: {
             if (o.d.r < 1 || o.d.s < 1 || o.d.stride < 1 || o.d.pad < 0 || o.d.pad >= o.d.r || o.d.pad >= o.d.s ||
-                o.d.r * o.d.s > 256 || in.h + 2 * o.d.pad < o.d.r || in.w + 2 * o.d.pad < o.d.s)
-                return fail(DC_EINVAL, "op %d: invalid max-pool geometry", i);
+                o.d.r * o.d.s > 256 || in.h + 2 * o.d.pad < o.d.r || in.w + 2 * o.d.pad < o.d.s ||
+                o.d.pad_w != o.d.pad)
+                return fail(DC_EINVAL, "op %d: invalid pooling geometry (pad_w must equal pad)", i);
             o.pool = dc_pool_shape{in.n, in.h, in.w, in.c, o.d.r, o.d.s, o.d.stride, o.d.pad};
             out.h = (in.h + 2 * o.d.pad - o.d.r) / o.d.stride + 1;
             out.w = (in.w + 2 * o.d.pad - o.d.s) / o.d.stride + 1;
@@ -242,6 +244,9 @@ int run_forward_layer(dc_model *m, int l, const float *x, const int32_t *y, hipS
         case DC_OP_MAXPOOL:
             DC_TRY(maxpool_forward(o.pool, in, out, reinterpret_cast<uint8_t *>(m->ws + o.aux), s));
             break;
+        case DC_OP_AVGPOOL:
+            DC_TRY(avgpool_forward(o.pool, in, out, s));
+            break;
         case DC_OP_GAP:
             DC_TRY(gap_forward(ti.n, ti.h * ti.w, ti.c, in, out, s));
             break;
@@ -296,6 +301,9 @@ int run_backward_layer(dc_model *m, int l, const float *x, hipStream_t s) {
             break;
         case DC_OP_MAXPOOL:
             DC_TRY(maxpool_backward(o.pool, dy, reinterpret_cast<const uint8_t *>(m->ws + o.aux), o.acc_in[0], dx, s));
+            break;
+        case DC_OP_AVGPOOL:
+            DC_TRY(avgpool_backward(o.pool, dy, o.acc_in[0], dx, s));
             break;
         case DC_OP_GAP:
             DC_TRY(gap_backward(ti.n, ti.h * ti.w, ti.c, dy, o.acc_in[0], dx, s));

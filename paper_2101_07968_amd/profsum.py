@@ -82,8 +82,8 @@ def conv_bytes(geoms):
     """Algorithmic bytes of each conv pass launch: every operand read once, the result written once."""
     out = []
     for _i, g, first in geoms:
-        n, h, w, c, k, r, s, st, pad = g
-        P, Q = (h + 2 * pad - r) // st + 1, (w + 2 * pad - s) // st + 1
+        n, h, w, c, k, r, s, st, pad, pad_w = g
+        P, Q = (h + 2 * pad - r) // st + 1, (w + 2 * pad_w - s) // st + 1
         x, y, wt = n * h * w * c * 4, n * P * Q * k * 4, k * r * s * c * 4
         out.append(("fwd", x + wt + y))
         out.append(("wgrad", x + y + wt))
@@ -153,8 +153,8 @@ def cmd_mfma(a):
     ops, hwc, _ = PN.build(a.workload)
     algo = 0.0
     for _i, g, first in PN.conv_geoms(ops, hwc, a.batch):
-        n, h, w, c, k, r, s_, st, pad = g
-        P, Q = (h + 2 * pad - r) // st + 1, (w + 2 * pad - s_) // st + 1
+        n, h, w, c, k, r, s_, st, pad, pad_w = g
+        P, Q = (h + 2 * pad - r) // st + 1, (w + 2 * pad_w - s_) // st + 1
         algo += 2.0 * n * P * Q * k * r * s_ * c * (2 if first else 3)
     launches = len(gem) / (len(PN.conv_geoms(ops, hwc, a.batch)) * 3 - sum(1 for *_, f in
                                                                           PN.conv_geoms(ops, hwc, a.batch) if f))

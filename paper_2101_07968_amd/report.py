@@ -233,7 +233,7 @@ def non_gemm(D, PN, torch, name, batch=None, reps=3):
         t[1] += nbytes
         t[2] += ms
 
-    for (kind, _l, src, other, out_ch, r, ss, stride, pad, bias, in2, in3), (ho, wo, co) in zip(ops, shp[1:]):
+    for (kind, _l, src, other, out_ch, r, ss, stride, pad, bias, in2, in3, _pw), (ho, wo, co) in zip(ops, shp[1:]):
         h, w, c = shp[src]
         ne_in, ne_out = n * h * w * c, n * ho * wo * co
         if kind == D.DC_OP_RELU:

@@ -144,6 +144,14 @@ def test_model_validation_rejects_bad_descriptions():
     # ADD of different shapes
     assert _create([conv, (D.DC_OP_ADD, 1, 1, 0, 0, 0, 0, 0, 0, 0)])[0] == D.DC_EINVAL
     assert b"ADD" in D.lib().dc_last_error()
+    # column padding as large as the filter's width (1 x 3 filter padded by 3 columns)
+    wide = (D.DC_OP_CONV, 1, 0, -1, 4, 1, 3, 1, 0, 1, -1, -1, 3)
+    assert _create([wide, (D.DC_OP_FC, 2, 1, -1, 10, 0, 0, 0, 0, 1)])[0] == D.DC_EINVAL
+    # pools pad rows and columns alike
+    for kind in (D.DC_OP_MAXPOOL, D.DC_OP_AVGPOOL):
+        pool = (kind, 1, 1, -1, 0, 3, 3, 1, 1, 0, -1, -1, 0)
+        assert _create([conv, pool, (D.DC_OP_FC, 2, 2, -1, 10, 0, 0, 0, 0, 1)])[0] == D.DC_EINVAL
+        assert b"pad_w" in D.lib().dc_last_error()
 
 
 @pytest.mark.parametrize("block", range(10))

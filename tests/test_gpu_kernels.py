@@ -6,7 +6,8 @@ order sqrt(number of sequential fp32 additions) * 2^-24.  The bars below are
 1e-5 * max(1, sqrt(K / 256)), capped at 2e-4 for the longest reductions (up to
 1.6 M terms), well inside the 1e-3 the full iteration must meet.  Max-pool
 forward picks values, so it must be bit-exact; its argmax is decided in
-float32 on both sides.
+float32 on both sides.  Average pooling sums at most a window's taps, so its
+bar is 1e-6.
 """
 import ctypes
 import math
@@ -27,8 +28,17 @@ def tol(k_terms):
     return min(2e-4, 1e-5 * max(1.0, math.sqrt(k_terms / 256.0)))
 
 
-def conv_shape(n, h, w, c, k, r, st, pad):
-    return D.ConvShape(n, h, w, c, k, r, r, st, pad)
+def geom10(shape):
+    """(n, h, w, c, k, r, s, stride, pad, pad_w) from a square 8-tuple
+    (n, h, w, c, k, r, stride, pad) or a full 10-tuple."""
+    if len(shape) == 8:
+        n, h, w, c, k, r, st, pad = shape
+        return (n, h, w, c, k, r, r, st, pad, pad)
+    return tuple(shape)
+
+
+def conv_shape(*shape):
+    return D.ConvShape(*geom10(shape))
 
 
 def out_hw(h, r, st, pad):
@@ -38,8 +48,8 @@ def out_hw(h, r, st, pad):
 def run_conv(shape, x, w, b, dy, relu, acc_init):
     """All three passes on the GPU; returns (y, dx, dw, db) as numpy."""
     sh = conv_shape(*shape)
-    n, h, wd, c, k, r, st, pad = shape
-    P, Q = out_hw(h, r, st, pad), out_hw(wd, r, st, pad)
+    n, h, wd, c, k, r, s, st, pad, pad_w = geom10(shape)
+    P, Q = out_hw(h, r, st, pad), out_hw(wd, s, st, pad_w)
     ws_t, ws, wsb = scratch(D.lib().dc_conv2d_workspace_bytes(ctypes.byref(sh)))
     xd, wd_, bd, dyd = dev(x), dev(w), dev(b), dev(dy)
     y = zeros((n, P, Q, k))
@@ -48,7 +58,7 @@ def run_conv(shape, x, w, b, dy, relu, acc_init):
     dx = dev(acc_init) if acc_init is not None else zeros((n, h, wd, c))
     D.call("dc_conv2d_backward_data", ctypes.byref(sh), dyd.data_ptr(), wd_.data_ptr(),
            1 if acc_init is not None else 0, dx.data_ptr(), ws, wsb, stream())
-    dw = zeros((k, r, r, c))
+    dw = zeros((k, r, s, c))
     db = zeros((k,))
     D.call("dc_conv2d_backward_filter", ctypes.byref(sh), xd.data_ptr(), dyd.data_ptr(), dw.data_ptr(),
            db.data_ptr(), ws, wsb, stream())
@@ -80,32 +90,43 @@ SMALL = [
     # a single output pixel; a stride larger than the filter (dgrad phases with no tap)
     (2, 3, 3, 8, 16, 3, 1, 0),
     (2, 9, 9, 4, 8, 1, 3, 0),
+    # rectangular filters, row and column padding apart (n, h, w, c, k, r, s, stride, pad, pad_w):
+    # the 1 x 7 / 7 x 1 / 1 x 3 / 3 x 1 convs and an unpadded strided 3 x 3
+    (2, 17, 17, 32, 48, 1, 7, 1, 0, 3),
+    (2, 17, 17, 32, 40, 7, 1, 1, 3, 0),
+    (2, 8, 8, 64, 32, 1, 3, 1, 0, 1),
+    (2, 8, 8, 48, 64, 3, 1, 1, 1, 0),
+    (2, 11, 13, 6, 10, 1, 7, 1, 0, 3),
+    (3, 9, 10, 5, 7, 7, 1, 1, 3, 0),
+    (2, 19, 18, 16, 24, 3, 5, 2, 1, 2),
+    (2, 15, 15, 16, 24, 3, 3, 2, 0, 0),
+    (3, 21, 20, 16, 32, 1, 3, 1, 0, 1),
 ]
 
 
 @pytest.mark.parametrize("shape", SMALL, ids=[str(s) for s in SMALL])
 @pytest.mark.parametrize("variant", ["plain", "relu_acc"])
 def test_conv_small(shape, variant):
-    n, h, w, c, k, r, st, pad = shape
-    P, Q = out_hw(h, r, st, pad), out_hw(w, r, st, pad)
+    n, h, w, c, k, r, s, st, pad, pad_w = geom10(shape)
+    P, Q = out_hw(h, r, st, pad), out_hw(w, s, st, pad_w)
     seed = sum(shape) * 7 + (variant == "relu_acc")
     x = synth.random_tensor(seed, (n, h, w, c))
-    wt = synth.random_tensor(seed + 1, (k, r, r, c))
+    wt = synth.random_tensor(seed + 1, (k, r, s, c))
     b = synth.random_tensor(seed + 2, (k,))
     dy = synth.random_tensor(seed + 3, (n, P, Q, k))
     relu = 1 if variant == "relu_acc" else 0
     acc0 = synth.random_tensor(seed + 4, (n, h, w, c)) if variant == "relu_acc" else None
     y, dx, dw, db = run_conv(shape, x, wt, b, dy, relu, acc0)
-    y_ref = OC.conv2d_forward(x, wt, b, st, pad)
+    y_ref = OC.conv2d_forward(x, wt, b, st, (pad, pad_w))
     if relu:
         y_ref = np.maximum(y_ref, 0)
-    dx_ref = OC.conv2d_backward_data(dy, wt, (h, w), st, pad)
+    dx_ref = OC.conv2d_backward_data(dy, wt, (h, w), st, (pad, pad_w))
     if acc0 is not None:
         dx_ref = dx_ref + acc0
-    dw_ref = OC.conv2d_backward_filter(x, dy, (r, r), st, pad)
+    dw_ref = OC.conv2d_backward_filter(x, dy, (r, s), st, (pad, pad_w))
     db_ref = dy.astype(np.float64).sum(axis=(0, 1, 2))
-    assert rel_err(y, y_ref) <= tol(r * r * c)
-    assert rel_err(dx, dx_ref) <= tol(r * r * k)
+    assert rel_err(y, y_ref) <= tol(r * s * c)
+    assert rel_err(dx, dx_ref) <= tol(r * s * k)
     assert rel_err(dw, dw_ref) <= tol(n * P * Q)
     assert rel_err(db, db_ref) <= tol(n * P * Q)
 
@@ -114,16 +135,16 @@ def _full_size_geoms():
     """Every distinct conv / FC geometry of the workloads at their own batch."""
     seen, out = set(), []
     for name, batch in (("tiny", 4), ("alexnet", 32), ("resnet18", 128), ("vgg16", 32), ("resnet50", 64),
-                        ("googlenet", 32), ("vgg19", 32), ("resnet152", 32)):
+                        ("googlenet", 32), ("vgg19", 32), ("resnet152", 32), ("inception_v4", 32)):
         net = OC.Net(ON.get(name), batch)
         for i, op in enumerate(net.ops):
             if op["op"] not in ("conv", "fc"):
                 continue
             n, h, w, c = net.shapes[op["in"]]
             if op["op"] == "conv":
-                g = (n, h, w, c, op["k"], op["r"], op["stride"], op["pad"])
+                g = (n, h, w, c, op["k"], op["r"], op["s"], op["stride"], op["pad"], op.get("pad_w", op["pad"]))
             else:
-                g = (n, 1, 1, h * w * c, op["out"], 1, 1, 0)
+                g = (n, 1, 1, h * w * c, op["out"], 1, 1, 1, 0, 0)
             if g not in seen:
                 seen.add(g)
                 out.append((name, g))
@@ -143,25 +164,25 @@ def _sample(rng, shape, count):
 @pytest.mark.parametrize("case", FULL, ids=[f"{n}-{g}" for n, g in FULL])
 def test_conv_full_size_sampled(case):
     name, shape = case
-    n, h, w, c, k, r, st, pad = shape
-    P, Q = out_hw(h, r, st, pad), out_hw(w, r, st, pad)
-    seed = abs(hash(shape)) % 10000
+    n, h, w, c, k, r, s, st, pad, pad_w = shape
+    P, Q = out_hw(h, r, st, pad), out_hw(w, s, st, pad_w)
+    seed = sum((i + 1) * v for i, v in enumerate(shape)) % 10000
     x = synth.random_tensor(seed, (n, h, w, c))
-    wt = synth.random_tensor(seed + 1, (k, r, r, c), scale=math.sqrt(2.0 / (r * r * c)))
+    wt = synth.random_tensor(seed + 1, (k, r, s, c), scale=math.sqrt(2.0 / (r * s * c)))
     b = synth.random_tensor(seed + 2, (k,))
     dy = synth.random_tensor(seed + 3, (n, P, Q, k), scale=1e-3)
     print(f"conv {name} {shape}", flush=True)
     y, dx, dw, db = run_conv(shape, x, wt, b, dy, 0, None)
     rng = np.random.default_rng(seed)
-    geom = (n, h, w, c, k, r, r, st, pad)
+    geom = shape
     i = _sample(rng, y.shape, 48)
     ref = OC.conv2d_samples("fwd", geom, x, wt, i, b)
     got = y[tuple(i.T)]
-    assert np.abs(got - ref).max() <= tol(r * r * c) * np.abs(y).max()
+    assert np.abs(got - ref).max() <= tol(r * s * c) * np.abs(y).max()
     i = _sample(rng, dx.shape, 48)
     ref = OC.conv2d_samples("dgrad", geom, dy, wt, i)
     got = dx[tuple(i.T)]
-    assert np.abs(got - ref).max() <= tol(r * r * k) * np.abs(dx).max()
+    assert np.abs(got - ref).max() <= tol(r * s * k) * np.abs(dx).max()
     i = _sample(rng, dw.shape, 32)
     ref = OC.conv2d_samples("wgrad", geom, x, dy, i)
     got = dw[tuple(i.T)]
@@ -235,6 +256,40 @@ def test_maxpool(cfg):
     dxa = dev(acc0)
     D.call("dc_maxpool_backward", ctypes.byref(sh), dyd.data_ptr(), arg.data_ptr(), 1, dxa.data_ptr(), stream())
     assert rel_err(host(dxa), dx_ref + acc0) <= 1e-6
+
+
+AVGPOOLS = [(2, 8, 8, 5, 3, 1, 1), (2, 9, 7, 12, 3, 1, 1), (3, 13, 13, 16, 3, 2, 1), (2, 12, 12, 7, 2, 2, 0),
+            (32, 35, 35, 384, 3, 1, 1), (32, 17, 17, 1024, 3, 1, 1), (32, 8, 8, 1536, 3, 1, 1),
+            (2, 11, 10, 6, 5, 3, 2), (1, 1, 1, 4, 3, 1, 1)]
+
+
+@pytest.mark.parametrize("cfg", AVGPOOLS, ids=[str(p) for p in AVGPOOLS])
+def test_avgpool(cfg):
+    """Average pooling over the in-image taps, forward and backward (also accumulating)."""
+    n, h, w, c, r, st, pad = cfg
+    x = synth.random_tensor(15, (n, h, w, c))
+    P, Q = out_hw(h, r, st, pad), out_hw(w, r, st, pad)
+    dy = synth.random_tensor(16, (n, P, Q, c))
+    sh = D.PoolShape(n, h, w, c, r, r, st, pad)
+    xd, dyd = dev(x), dev(dy)
+    y = zeros((n, P, Q, c))
+    D.call("dc_avgpool_forward", ctypes.byref(sh), xd.data_ptr(), y.data_ptr(), stream())
+    assert rel_err(host(y), OC.avgpool_forward(x, r, r, st, pad)) <= 1e-6
+    dx_ref = OC.avgpool_backward(dy, x.shape, r, r, st, pad)
+    dx = zeros((n, h, w, c))
+    D.call("dc_avgpool_backward", ctypes.byref(sh), dyd.data_ptr(), 0, dx.data_ptr(), stream())
+    assert rel_err(host(dx), dx_ref) <= 1e-6
+    acc0 = synth.random_tensor(17, (n, h, w, c))
+    dxa = dev(acc0)
+    D.call("dc_avgpool_backward", ctypes.byref(sh), dyd.data_ptr(), 1, dxa.data_ptr(), stream())
+    assert rel_err(host(dxa), dx_ref + acc0) <= 1e-6
+
+
+def test_avgpool_rejects_bad_shapes():
+    sh = D.PoolShape(2, 4, 4, 3, 3, 3, 1, 3)    # pad >= window
+    assert D.lib().dc_avgpool_forward(ctypes.byref(sh), 1, 1, None) == D.DC_EINVAL
+    sh = D.PoolShape(0, 4, 4, 3, 3, 3, 1, 1)    # empty batch: nothing to do
+    assert D.lib().dc_avgpool_forward(ctypes.byref(sh), None, None, stream()) == D.DC_OK
 
 
 @pytest.mark.parametrize("cfg", [(3, 4, 4, 10), (128, 4, 4, 512), (64, 7, 7, 2048)])

@@ -3,7 +3,7 @@
 * Parity (loss within 1e-4 relative; every parameter tensor's gradient and
   post-step weight within 1e-3 max relative error, or within 5x the scatter of
   float32 evaluations of the same iteration where that scatter exceeds 1e-3)
-  on all five workloads: the tiny one at its own batch of 4, the others at
+  on every workload: the tiny one at its own batch of 4, the others at
   reduced batches that the oracle finishes in seconds.
 * Scheduling leaves the numbers untouched: results are bit-identical for the
   sequential, layer-by-layer, DP and random segmentations, here and at the
@@ -53,7 +53,7 @@ def plans_for(L, seed=0):
 
 
 PARITY = [("tiny", 4), ("alexnet", 2), ("resnet18", 8), ("resnet50", 2), ("vgg16", 1), ("googlenet", 2),
-          ("vgg19", 1), ("resnet152", 2), ("tiny", 1), ("resnet18", 1)]
+          ("vgg19", 1), ("resnet152", 2), ("inception_v4", 1), ("tiny", 1), ("resnet18", 1)]
 
 
 def fp32_spread(spec, onet, x, y, params, g_ref):
@@ -144,7 +144,7 @@ def test_results_do_not_depend_on_segmentation(name, batch):
 
 
 FULL = [("tiny", 4, 0), ("alexnet", 32, 1), ("resnet18", 128, 2), ("vgg16", 32, 3), ("resnet50", 64, 4),
-        ("googlenet", 32, 5), ("vgg19", 32, 6), ("resnet152", 32, 7)]
+        ("googlenet", 32, 5), ("vgg19", 32, 6), ("resnet152", 32, 7), ("inception_v4", 32, 8)]
 
 
 @pytest.mark.parametrize("name,batch,seed", FULL, ids=[f"{n}-b{b}" for n, b, _ in FULL])
@@ -296,14 +296,15 @@ def test_degenerate_models():
     cases = [
         ({"name": "fc1", "ops": [{"op": "fc", "in": 0, "layer": 1, "out": 10, "bias": True}],
           "hwc": (4, 4, 3), "classes": 10},
-         [(D.DC_OP_FC, 1, 0, -1, 10, 0, 0, 0, 0, 1, -1, -1)], 1),
+         [(D.DC_OP_FC, 1, 0, -1, 10, 0, 0, 0, 0, 1, -1, -1, 0)], 1),
         ({"name": "pix1", "ops": [
             {"op": "conv", "in": 0, "layer": 1, "k": 8, "r": 3, "s": 3, "stride": 1, "pad": 0, "bias": True},
             {"op": "relu", "in": 1, "layer": 1},
             {"op": "fc", "in": 2, "layer": 2, "out": 5, "bias": True}],
           "hwc": (3, 3, 4), "classes": 5},
-         [(D.DC_OP_CONV, 1, 0, -1, 8, 3, 3, 1, 0, 1, -1, -1), (D.DC_OP_RELU, 1, 1, -1, 0, 0, 0, 0, 0, 0, -1, -1),
-          (D.DC_OP_FC, 2, 2, -1, 5, 0, 0, 0, 0, 1, -1, -1)], 3),
+         [(D.DC_OP_CONV, 1, 0, -1, 8, 3, 3, 1, 0, 1, -1, -1, 0),
+          (D.DC_OP_RELU, 1, 1, -1, 0, 0, 0, 0, 0, 0, -1, -1, 0),
+          (D.DC_OP_FC, 2, 2, -1, 5, 0, 0, 0, 0, 1, -1, -1, 0)], 3),
     ]
     for spec, ops, batch in cases:
         print(f"degenerate {spec['name']} batch {batch}", flush=True)
