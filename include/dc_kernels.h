@@ -49,9 +49,28 @@ int dc_conv2d_backward_filter(const dc_conv_shape *sh, const float *x, const flo
                               float *dw, float *dbias, void *ws, size_t ws_bytes, void *stream);
 
 /* Launch plan the conv passes use for this shape (pass: 0 forward, 1 data
- * gradient, 2 filter gradient).  out[0..6] = workgroup tile M, tile N, split-K
- * factor, GEMM M, GEMM N, GEMM K, stride phases.  For inspection and tuning. */
+ * gradient, 2 filter gradient).  out[0..7] = workgroup tile M, tile N, split-K
+ * factor, GEMM M, GEMM N, GEMM K, stride phases, and where the plan came from
+ * (0 the occupancy cost model, 1 the library's table of measured plans, 2 a
+ * plan pinned with dc_conv2d_set_plan).  out holds at least 8 int32.  Host
+ * only; for inspection and tuning. */
 int dc_conv2d_plan_info(const dc_conv_shape *sh, int pass, int32_t *out);
+
+/* Every plan the pass can be launched with for this shape, as (tile M, tile N,
+ * split-K factor) triples: writes min(cap, count) triples to out (3 int32
+ * each; out may be NULL when cap is 0) and the number available to *count.
+ * Host only. */
+int dc_conv2d_plan_candidates(const dc_conv_shape *sh, int pass, int32_t *out, int cap, int32_t *count);
+
+/* Pins the plan of one pass of one shape for the rest of the process: the conv
+ * entry points, dc_conv2d_workspace_bytes and models created afterwards use
+ * it (models already created keep their plans).  (mt, nt, splits) must be one
+ * of dc_conv2d_plan_candidates' triples, else DC_EINVAL.  mt = 0 removes the
+ * pin; mt = -1 pins the occupancy cost model's own choice, bypassing the table
+ * of measured plans.  Every plan computes the same sums; they differ in speed
+ * and in the rounding order of split-K partial sums.  Thread-safe.  Host
+ * only; for tuning (timing candidates through the conv entry points). */
+int dc_conv2d_set_plan(const dc_conv_shape *sh, int pass, int mt, int nt, int splits);
 
 /* y = max(x, 0) over n floats. */
 int dc_relu_forward(const float *x, float *y, int64_t n, void *stream);

@@ -109,6 +109,8 @@ _SIGS = {
     "dc_timeline": (ctypes.c_int, [c_vp, _P(c_i64), ctypes.c_int]),
     "dc_conv2d_workspace_bytes": (c_sz, [_P(ConvShape)]),
     "dc_conv2d_plan_info": (ctypes.c_int, [_P(ConvShape), ctypes.c_int, _P(c_i32)]),
+    "dc_conv2d_plan_candidates": (ctypes.c_int, [_P(ConvShape), ctypes.c_int, _P(c_i32), ctypes.c_int, _P(c_i32)]),
+    "dc_conv2d_set_plan": (ctypes.c_int, [_P(ConvShape), ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int]),
     "dc_conv2d_forward": (ctypes.c_int, [_P(ConvShape), c_vp, c_vp, c_vp, ctypes.c_int, c_vp, c_vp, c_sz, c_vp]),
     "dc_conv2d_backward_data": (ctypes.c_int, [_P(ConvShape), c_vp, c_vp, ctypes.c_int, c_vp, c_vp, c_sz, c_vp]),
     "dc_conv2d_backward_filter": (ctypes.c_int, [_P(ConvShape), c_vp, c_vp, c_vp, c_vp, c_vp, c_sz, c_vp]),
@@ -262,11 +264,28 @@ def dc_plan_eval(prof, p, g):
 # ---------------------------------------------------------------- model
 
 def conv_plan_info(shape, pas):
-    """(tile M, tile N, splits, GEMM M, GEMM N, GEMM K, phases) of one conv pass."""
-    out = (c_i32 * 7)()
+    """(tile M, tile N, splits, GEMM M, GEMM N, GEMM K, phases, source) of one conv pass;
+    source 0 = cost model, 1 = table of measured plans, 2 = pinned."""
+    out = (c_i32 * 8)()
     sh = ConvShape(*shape)
     call("dc_conv2d_plan_info", ctypes.byref(sh), pas, out)
     return tuple(out)
+
+
+def conv_plan_candidates(shape, pas):
+    """Every (tile M, tile N, splits) the pass can be launched with for this shape."""
+    sh = ConvShape(*shape)
+    n = c_i32()
+    call("dc_conv2d_plan_candidates", ctypes.byref(sh), pas, None, 0, ctypes.byref(n))
+    out = (c_i32 * (3 * n.value))()
+    call("dc_conv2d_plan_candidates", ctypes.byref(sh), pas, out, n.value, ctypes.byref(n))
+    return [tuple(out[3 * i:3 * i + 3]) for i in range(n.value)]
+
+
+def conv_set_plan(shape, pas, mt, nt=0, splits=0):
+    """Pin a pass's plan for this process (mt = 0 unpins, mt = -1 pins the cost model's choice)."""
+    sh = ConvShape(*shape)
+    call("dc_conv2d_set_plan", ctypes.byref(sh), pas, mt, nt, splits)
 
 
 def link(bytes_per_s=1e9, dt_emul_ns=0, paced=True):

@@ -148,10 +148,41 @@ extern "C" int dc_conv2d_plan_info(const dc_conv_shape *sh, int pass, int32_t *o
     if (pass < 0 || pass > 2 || !out)
         return fail(DC_EINVAL, "pass must be 0, 1 or 2 and out non-NULL");
     GemmPlan pl = plan_gemm(g, pass);
-    const int32_t v[7] = {pl.mt, pl.nt, pl.splits, pl.M, pl.Ng, pl.Kg, pl.phases};
-    for (int i = 0; i < 7; ++i)
+    const int32_t v[8] = {pl.mt, pl.nt, pl.splits, pl.M, pl.Ng, pl.Kg, pl.phases, pl.source};
+    for (int i = 0; i < 8; ++i)
         out[i] = v[i];
     return DC_OK;
+}
+
+extern "C" int dc_conv2d_plan_candidates(const dc_conv_shape *sh, int pass, int32_t *out, int cap, int32_t *count) {
+    clear_error();
+    ConvGeom g;
+    DC_TRY(conv_setup(sh, &g));
+    if (pass < 0 || pass > 2 || !count || cap < 0 || (cap > 0 && !out))
+        return fail(DC_EINVAL, "pass must be 0, 1 or 2, count non-NULL and out non-NULL when cap > 0");
+    *count = plan_candidates(g, pass, out, cap);
+    return DC_OK;
+}
+
+extern "C" int dc_conv2d_set_plan(const dc_conv_shape *sh, int pass, int mt, int nt, int splits) {
+    clear_error();
+    ConvGeom g;
+    DC_TRY(conv_setup(sh, &g));
+    if (pass < 0 || pass > 2)
+        return fail(DC_EINVAL, "pass must be 0, 1 or 2");
+    if (mt == 0 || mt == -1) {
+        pin_plan(g, pass, mt, 0, 0);
+        return DC_OK;
+    }
+    const int n = plan_candidates(g, pass, nullptr, 0);
+    std::vector<int32_t> c(3 * (size_t)n);
+    plan_candidates(g, pass, c.data(), n);
+    for (int i = 0; i < n; ++i)
+        if (c[3 * i] == mt && c[3 * i + 1] == nt && c[3 * i + 2] == splits) {
+            pin_plan(g, pass, mt, nt, splits);
+            return DC_OK;
+        }
+    return fail(DC_EINVAL, "plan (%d, %d, split %d) is not a candidate for this shape and pass", mt, nt, splits);
 }
 
 extern "C" int dc_conv2d_forward(const dc_conv_shape *sh, const float *x, const float *w, const float *bias, int relu,

@@ -53,10 +53,26 @@ struct GemmPlan {
     size_t pad_x_off;     // workspace offsets of the padded x and of the padded w (FWD) or dw (WGRAD)
     size_t pad_w_off;
     size_t ws_bytes;      // split-K partial sums, then the padded copies
+    int source;           // PLAN_MODEL, PLAN_TABLE or PLAN_PINNED
 };
+
+enum PlanSource { PLAN_MODEL = 0, PLAN_TABLE = 1, PLAN_PINNED = 2 };
 
 bool conv_geom_from_shape(const dc_conv_shape &sh, ConvGeom *g);
 GemmPlan plan_gemm(const ConvGeom &g, int pass);
+// Every (tile M, tile N, split-K factor) the planner can launch for this pass;
+// writes up to cap triples and returns how many there are.
+int plan_candidates(const ConvGeom &g, int pass, int32_t *out, int cap);
+
+// Plans chosen by measurement, looked up before the cost model: first a plan
+// pinned for this process (pin_plan), then the table built into the library.
+// Returns PLAN_PINNED or PLAN_TABLE with (mt, nt, splits) in out, PLAN_MODEL
+// when neither holds the shape, or -1 when the shape is pinned to the cost
+// model itself.
+int lookup_plan(const ConvGeom &g, int pass, int out[3]);
+// mt > 0 pins (mt, nt, splits); mt == 0 removes the pin; mt == -1 pins the
+// cost model's choice (the built-in table is then skipped for this shape).
+void pin_plan(const ConvGeom &g, int pass, int mt, int nt, int splits);
 
 int conv_forward(const ConvGeom &g, const GemmPlan &pl, const float *x, const float *w,
                  const float *bias, int relu, float *y, void *ws, hipStream_t s);

@@ -976,7 +976,9 @@ bool conv_geom_from_shape(const dc_conv_shape &sh, ConvGeom *g) {
     return big < INT_MAX;
 }
 
-static GemmPlan plan_core(const ConvGeom &g, int pass) {
+// force (mt, nt, splits), if given, restricts the choice to that plan; the
+// result then has mt == 0 when the shape cannot run it.
+static GemmPlan plan_core(const ConvGeom &g, int pass, const int *force) {
     GemmPlan pl{};
     pl.pass = pass;
     pl.phases = 1;
@@ -1025,6 +1027,8 @@ static GemmPlan plan_core(const ConvGeom &g, int pass) {
     const int ktiles = std::max(1, (pl.Kg + KT - 1) / KT);
     for (int c = 0; c < 4; ++c) {
         int mt = cand[c][0], nt = cand[c][1];
+        if (force && (mt != force[0] || nt != force[1]))
+            continue;
         int tm = (pl.M + mt - 1) / mt, tn = (pl.Ng + nt - 1) / nt;
         int64_t tiles = (int64_t)tm * tn * pl.phases;
         for (int sp = 1; sp <= 1024; sp *= 2) {
@@ -1032,6 +1036,13 @@ static GemmPlan plan_core(const ConvGeom &g, int pass) {
                 break;
             int kps = (ktiles + sp - 1) / sp;
             int spe = (ktiles + kps - 1) / kps;
+            if (force) {
+                if (spe != force[2])
+                    continue;
+                pl.mt = mt; pl.nt = nt; pl.kt = KT; pl.splits = spe; pl.kt_per_split = kps;
+                pl.tiles_m = tm; pl.tiles_n = tn;
+                break;
+            }
             int64_t wgs = tiles * spe;
             const int64_t per_cu = (wgs + 255) / 256; // workgroups the busiest CU works through
             const int64_t full = per_cu / occ[c], rem = per_cu % occ[c];
@@ -1055,6 +1066,33 @@ static GemmPlan plan_core(const ConvGeom &g, int pass) {
     return pl;
 }
 
+// The (tile, split) pairs the search above visits, with repeats of the same
+// effective split removed.
+static int candidates_core(const ConvGeom &g, int pass, int32_t *out, int cap) {
+    const GemmPlan base = plan_core(g, pass, nullptr);
+    static const int cand[4][2] = {{128, 128}, {128, 64}, {64, 128}, {64, 64}};
+    const int ktiles = std::max(1, (base.Kg + 15) / 16);
+    int n = 0;
+    for (int c = 0; c < 4; ++c) {
+        int last = 0;
+        for (int sp = 1; sp <= 1024; sp *= 2) {
+            if (sp > 1 && (ktiles / sp) < 4)
+                break;
+            const int kps = (ktiles + sp - 1) / sp, spe = (ktiles + kps - 1) / kps;
+            if (spe == last)
+                continue;
+            last = spe;
+            if (n < cap && out) {
+                out[3 * n] = cand[c][0];
+                out[3 * n + 1] = cand[c][1];
+                out[3 * n + 2] = spe;
+            }
+            ++n;
+        }
+    }
+    return n;
+}
+
 static size_t round256(size_t b) { return (b + 255) / 256 * 256; }
 
 // Forward and wgrad with C % 4 != 0 run on channel-padded copies of x (and of
@@ -1072,11 +1110,26 @@ static ConvGeom padded(const ConvGeom &g) {
     return gp;
 }
 
+int plan_candidates(const ConvGeom &g, int pass, int32_t *out, int cap) {
+    return candidates_core(pads_channels(g, pass) ? padded(g) : g, pass, out, cap);
+}
+
 GemmPlan plan_gemm(const ConvGeom &g, int pass) {
-    if (!pads_channels(g, pass))
-        return plan_core(g, pass);
-    const ConvGeom gp = padded(g);
-    GemmPlan pl = plan_core(gp, pass);
+    const bool pads = pads_channels(g, pass);
+    const ConvGeom gp = pads ? padded(g) : g;
+    int force[3];
+    const int src = lookup_plan(g, pass, force);
+    GemmPlan pl{};
+    if (src == PLAN_TABLE || src == PLAN_PINNED) {
+        pl = plan_core(gp, pass, force);
+        pl.source = src;
+    }
+    if (pl.mt == 0) { // no measured plan, or one this shape cannot run
+        pl = plan_core(gp, pass, nullptr);
+        pl.source = PLAN_MODEL;
+    }
+    if (!pads)
+        return pl;
     pl.cpad = gp.C;
     pl.pad_x_off = round256(pl.ws_bytes);
     pl.pad_w_off = pl.pad_x_off + round256((size_t)g.N * g.H * g.W * gp.C * sizeof(float));

@@ -131,6 +131,59 @@ def test_conv_small(shape, variant):
     assert rel_err(db, db_ref) <= tol(n * P * Q)
 
 
+PLAN_SHAPES = [
+    (4, 14, 14, 64, 96, 3, 3, 1, 1, 1),    # K = 576: split-K up to 8 in forward and dgrad
+    (3, 15, 15, 32, 48, 3, 3, 2, 1, 1),    # strided: four dgrad phases
+    (2, 17, 17, 32, 48, 1, 7, 1, 0, 3),    # 1 x 7 filter, columns padded only
+    (2, 20, 20, 3, 16, 3, 3, 1, 1, 1),     # C = 3: channel-padded forward and wgrad
+]
+
+
+@pytest.mark.parametrize("shape", PLAN_SHAPES, ids=[str(s) for s in PLAN_SHAPES])
+def test_every_plan_matches_oracle(shape):
+    """Each (tile, split-K) plan the planner may pick, pinned in turn, gives the
+    oracle's result to the pass's bar: the table of measured plans can choose
+    any of them."""
+    n, h, w, c, k, r, s, st, pad, pad_w = shape
+    P, Q = out_hw(h, r, st, pad), out_hw(w, s, st, pad_w)
+    seed = sum(shape)
+    x = synth.random_tensor(seed, (n, h, w, c))
+    wt = synth.random_tensor(seed + 1, (k, r, s, c))
+    b = synth.random_tensor(seed + 2, (k,))
+    dy = synth.random_tensor(seed + 3, (n, P, Q, k))
+    refs = [OC.conv2d_forward(x, wt, b, st, (pad, pad_w)),
+            OC.conv2d_backward_data(dy, wt, (h, w), st, (pad, pad_w)),
+            OC.conv2d_backward_filter(x, dy, (r, s), st, (pad, pad_w))]
+    bars = [tol(r * s * c), tol(r * s * k), tol(n * P * Q)]
+    sh = conv_shape(*shape)
+    xd, wd_, bd, dyd = dev(x), dev(wt), dev(b), dev(dy)
+    tried = 0
+    for pas in range(3):
+        for plan in D.conv_plan_candidates(shape, pas):
+            D.conv_set_plan(shape, pas, *plan)
+            try:
+                assert D.conv_plan_info(shape, pas)[:3] == plan
+                ws_t, ws, wsb = scratch(D.lib().dc_conv2d_workspace_bytes(ctypes.byref(sh)))
+                if pas == 0:
+                    out = zeros((n, P, Q, k))
+                    D.call("dc_conv2d_forward", ctypes.byref(sh), xd.data_ptr(), wd_.data_ptr(), bd.data_ptr(), 0,
+                           out.data_ptr(), ws, wsb, stream())
+                elif pas == 1:
+                    out = zeros((n, h, w, c))
+                    D.call("dc_conv2d_backward_data", ctypes.byref(sh), dyd.data_ptr(), wd_.data_ptr(), 0,
+                           out.data_ptr(), ws, wsb, stream())
+                else:
+                    out = zeros((k, r, s, c))
+                    D.call("dc_conv2d_backward_filter", ctypes.byref(sh), xd.data_ptr(), dyd.data_ptr(),
+                           out.data_ptr(), None, ws, wsb, stream())
+                err = rel_err(host(out), refs[pas])
+                assert err <= bars[pas], (pas, plan, err)
+                tried += 1
+            finally:
+                D.conv_set_plan(shape, pas, 0)
+    assert tried >= 3 * 4
+
+
 def _full_size_geoms():
     """Every distinct conv / FC geometry of the workloads at their own batch."""
     seen, out = set(), []
