@@ -378,8 +378,9 @@ class Net:
             t.append(y)
         return t, cache
 
-    def loss_and_grads(self, x, y, params):
-        """One forward and backward pass: returns (loss, flat float64 gradient)."""
+    def loss_and_grads(self, x, y, params, keep=False):
+        """One forward and backward pass: returns (loss, flat float64 gradient), and
+        with keep=True also (tensors, caches, tensor gradients) of the pass."""
         params = np.asarray(params, dtype=np.float64)
         t, cache = self.forward(x, params)
         N = self.batch
@@ -444,6 +445,8 @@ class Net:
                     ci = t[tid].shape[3]
                     acc(tid, dy[..., lo:lo + ci])
                     lo += ci
+        if keep:
+            return loss, grads, t, cache, g
         return loss, grads
 
     def loss(self, x, y, params):
