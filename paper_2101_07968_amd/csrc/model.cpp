@@ -180,6 +180,22 @@ static int build_model(dc_model *m, const dc_op_desc *ops, int n_ops) {
         if (!written[t] && t != n_ops)
             return fail(DC_EINVAL, "tensor %d is never used", t);
 
+    // forward ReLU folding (see OpInfo::relu_into)
+    std::vector<int> consumers(n_ops + 1, 0);
+    for (const OpInfo &o : m->ops)
+        for (int k = 0; k < o.n_in; ++k)
+            if (o.in[k] >= 0)
+                ++consumers[o.in[k]];
+    for (int i = 0; i + 1 < n_ops; ++i) {
+        OpInfo &o = m->ops[i], &nx = m->ops[i + 1];
+        const int kd = o.d.kind;
+        if ((kd == DC_OP_CONV || kd == DC_OP_FC || kd == DC_OP_BN || kd == DC_OP_ADD) && !o.fwd_folded &&
+            nx.d.kind == DC_OP_RELU && nx.d.in0 == o.out && consumers[o.out] == 1 && nx.d.layer == o.d.layer) {
+            o.relu_into = nx.out;
+            nx.fwd_folded = true;
+        }
+    }
+
     // workspace layout
     size_t off = 0;
     auto take = [&](size_t bytes) {
@@ -223,18 +239,21 @@ int run_forward_layer(dc_model *m, int l, const float *x, const int32_t *y, hipS
     const float *P = m->dparams();
     for (int i = m->layer_first[l]; i <= m->layer_last[l]; ++i) {
         OpInfo &o = m->ops[i];
+        if (o.fwd_folded)
+            continue; // computed by the producer (OpInfo::relu_into)
         const float *in = o.d.in0 == 0 ? x : m->act(o.d.in0);
-        float *out = m->act(o.out);
+        const int relu = o.relu_into >= 0 ? 1 : 0;
+        float *out = m->act(relu ? o.relu_into : o.out);
         const TensorInfo &ti = m->tensors[o.d.in0];
         switch (o.d.kind) {
         case DC_OP_CONV:
         case DC_OP_FC:
-            DC_TRY(conv_forward(o.geom, o.fwd, in, P + o.w_off, o.b_off != NONE ? P + o.b_off : nullptr, 0, out,
+            DC_TRY(conv_forward(o.geom, o.fwd, in, P + o.w_off, o.b_off != NONE ? P + o.b_off : nullptr, relu, out,
                                 m->scratch(), s));
             break;
         case DC_OP_BN: {
             float *mean = reinterpret_cast<float *>(m->ws + o.aux);
-            DC_TRY(bn_forward((int64_t)ti.n * ti.h * ti.w, ti.c, in, P + o.w_off, P + o.b_off, 1e-5f, 0, out, mean,
+            DC_TRY(bn_forward((int64_t)ti.n * ti.h * ti.w, ti.c, in, P + o.w_off, P + o.b_off, 1e-5f, relu, out, mean,
                               mean + ti.c, m->scratch(), s));
             break;
         }
@@ -251,7 +270,7 @@ int run_forward_layer(dc_model *m, int l, const float *x, const int32_t *y, hipS
             DC_TRY(gap_forward(ti.n, ti.h * ti.w, ti.c, in, out, s));
             break;
         case DC_OP_ADD:
-            DC_TRY(add_forward(in, m->act(o.d.in1), 0, out, ti.size(), s));
+            DC_TRY(add_forward(in, m->act(o.d.in1), relu, out, ti.size(), s));
             break;
         case DC_OP_CONCAT: {
             const TensorInfo &to = m->tensors[o.out];

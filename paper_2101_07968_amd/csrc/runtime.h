@@ -34,6 +34,14 @@ struct OpInfo {
     int ch_off[4] = {0, 0, 0, 0};    // CONCAT: channel offset of each input in the output
     bool grad_in[4] = {false, false, false, false};
     int acc_in[4] = {0, 0, 0, 0};    // backward adds into the input gradient
+    // Forward ReLU folded into its producer: a CONV / FC / BN / ADD whose only
+    // consumer is the next op, a ReLU of the same layer, writes max(., 0)
+    // straight into the ReLU's output (relu_into = that tensor), and the ReLU
+    // does nothing in the forward pass.  The producer's own output tensor is
+    // then never written; nothing reads it (the ReLU's backward reads the
+    // ReLU's output, the producer's backward reads its inputs).
+    int relu_into = -1;
+    bool fwd_folded = false;
 };
 
 } // namespace dc

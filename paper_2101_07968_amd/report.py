@@ -359,6 +359,7 @@ def main():
     ap.add_argument("--non-gemm", default="", help="comma list of workloads: bandwidth of the HBM-bound kernels")
     ap.add_argument("--dt-sweep", action="store_true",
                     help="VGG-16 at 100 Gb/s and unpaced with an emulated per-transfer overhead of 1 and 10 ms")
+    ap.add_argument("--unpaced", action="store_true", help="run the --only workloads on unpaced copies")
     ap.add_argument("--out", default="")
     a = ap.parse_args()
     import torch
@@ -366,7 +367,7 @@ def main():
     import synth
     from . import _lib as D
     from . import nets as PN
-    cases = [(n, PN.WORKLOADS[n]["link"], True, 0) for n in a.only.split(",") if n]
+    cases = [(n, PN.WORKLOADS[n]["link"], not a.unpaced, 0) for n in a.only.split(",") if n]
     if a.vgg_sweep:
         cases = [c for c in cases if c[0] != "vgg16"]
         cases += [("vgg16", g * 1e9 / 8, True, 0) for g in (0.1, 1, 10, 100)] + [("vgg16", 0, False, 0)]
