@@ -178,10 +178,11 @@ def adapt(D, PN, synth, torch, name, rates_gbps, steps):
     return "\n".join(lines)
 
 
-def planner_scaling(D, synth, Ls, reps=20):
+def planner_scaling(D, PN, synth, Ls, reps=20):
     """Host time of the DP (Eq. 8 + 9) and of iBatch (Algorithms 1 + 2) against L on
     generated profiles (the study of Fig. 12 / Table I), median of `reps` calls,
-    minus the median time of a one-layer call (the ctypes round trip)."""
+    minus the median time of a one-layer call (the ctypes round trip).  The L of
+    the paper's four evaluation networks are always included and labelled."""
     def med(f, prof):
         ts = []
         for _ in range(reps):
@@ -192,12 +193,17 @@ def planner_scaling(D, synth, Ls, reps=20):
     one = D.Profile(*synth.random_profile(0, 1)[:4], 0)
     base = min(med(D.dc_plan, one), med(D.dc_plan_ibatch, one))
     lines = ["| L | DP forward + backward (us) | iBatch forward + backward (us) |", "|---|---|---|"]
-    for L in Ls:
+    named = {}
+    for name in ("vgg19", "googlenet", "inception_v4", "resnet152"):
+        ops, _, _ = PN.build(name)
+        named.setdefault(max(o[1] for o in ops), []).append(name)
+    for L in sorted(set(Ls) | set(named)):
         pt, fc, bc, gt, dt = synth.random_profile(1000 + L, L, hi=10 ** 7, dt_hi=10 ** 6)
         prof = D.Profile(pt, fc, bc, gt, dt)
         a = max(0.0, med(D.dc_plan, prof) - base) / 1e3
         b = max(0.0, med(D.dc_plan_ibatch, prof) - base) / 1e3
-        lines.append(f"| {L} | {a:.1f} | {b:.1f} |")
+        label = f"{L} ({', '.join(named[L])})" if L in named else f"{L}"
+        lines.append(f"| {label} | {a:.1f} | {b:.1f} |")
         print(lines[-1], file=sys.stderr, flush=True)
     return "\n".join(lines)
 
@@ -409,7 +415,7 @@ def main():
         del src, dst
         text = "\n\n".join(non_gemm(D, PN, torch, w) for w in a.non_gemm.split(","))
     if a.planner_scaling:
-        text = planner_scaling(D, synth, [4, 8, 16, 18, 50, 100, 160, 200, 300])
+        text = planner_scaling(D, PN, synth, [4, 8, 16, 18, 50, 100, 160, 200, 300])
     if a.adapt:
         text = adapt(D, PN, synth, torch, a.adapt, [float(g) for g in a.adapt_rates.split(",")], a.steps)
     print(text)

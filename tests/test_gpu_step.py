@@ -245,6 +245,31 @@ def test_watchdog_times_out_and_gpu_drains():
     assert np.isfinite(st["loss"])
 
 
+@pytest.mark.parametrize("name,batch", [("tiny", 4), ("resnet18", 8)])
+def test_checkpoint_resume_is_bit_exact(name, batch):
+    """The parameter server holds the whole training state (BatchNorm keeps no
+    running statistics): two steps equal one step, a dc_ps_read checkpoint
+    written into a fresh model with dc_ps_write, and a second step there."""
+    model, onet, xd, yd, x, y, params = setup_model(name, batch, seed=11)
+    x2, y2, _ = synth.cnn_inputs(12, batch, onet.spec["hwc"], onet.classes, onet.param_specs)
+    x2d, y2d = dev(x2), dev(y2)
+    plan = plans_for(model.L, seed=2)["random"]
+    model.step(xd, yd, plan, UNPACED)
+    ckpt, _ = model.ps_read()
+    st_a = model.step(x2d, y2d, plan, UNPACED)
+    p_a, g_a = model.ps_read()
+    model.close()
+    ops, hwc, classes = PN.build(name)
+    fresh = D.Model(ops, batch, hwc, classes)
+    fresh.ps_write(ckpt)
+    st_b = fresh.step(x2d, y2d, plan, UNPACED)
+    p_b, g_b = fresh.ps_read()
+    assert st_b["loss"] == st_a["loss"]
+    np.testing.assert_array_equal(g_b, g_a)
+    np.testing.assert_array_equal(p_b, p_a)
+    fresh.close()
+
+
 def test_dynamic_step_plans_in_idle_windows():
     """dc_step_dynamic (idle-event trigger, Sec. IV-C): same decisions as dc_plan,
     same numbers as dc_step, and planning finished while a transfer was in flight."""
