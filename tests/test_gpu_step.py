@@ -300,7 +300,7 @@ def test_replanning_follows_the_link():
     """Re-profiling after the link changes (once-per-epoch cadence, Sec. IV-C) re-plans
     exactly as the oracle does on the new profile."""
     model, onet, xd, yd, x, y, params = setup_model("resnet18", 32, seed=6)
-    plans = {}
+    plans, profs = {}, {}
     for rate in (1.25e10 / 8 * 8, 1.25e8):
         lnk = D.link(rate, 0, paced=True)
         prof = model.profile(xd, yd, lnk, reps=2)
@@ -311,8 +311,14 @@ def test_replanning_follows_the_link():
         ratio = prof.pt.sum() / np.array(model.layer_bytes()).sum()
         assert abs(ratio * rate / 1e9 - 1) < 1e-3
         plans[rate] = plan.decisions()
-    # the fast link is worth splitting, the slow one barely
-    assert sum(plans[1.25e10 / 8 * 8][0]) >= sum(plans[1.25e8][0])
+        profs[rate] = (prof.pt.tolist(), prof.fc.tolist(), prof.bc.tolist(), prof.gt.tolist(), prof.dt)
+    # on each link's profile, its own plan is at least as good under f_m as the
+    # plan made for the other link: re-planning never loses (Sec. IV-B-3)
+    for rate, other in ((1.25e10, 1.25e8), (1.25e8, 1.25e10)):
+        pr = profs[rate]
+        own = OP.fm(*pr, *plans[rate])
+        stale = OP.fm(*pr, *plans[other])
+        assert own <= stale, (rate, own, stale)
 
 
 def test_degenerate_models():
