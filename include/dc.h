@@ -129,7 +129,12 @@ enum {
     DC_OPT_LR = 1,          /* SGD learning rate at the server (default 0.01) */
     DC_OPT_TIMELINE = 2,    /* 1: dc_step records per-layer timestamps (default 0) */
     DC_OPT_TIMEOUT_S = 3,   /* watchdog for one dc_step / dc_profile in seconds (default 600) */
-    DC_OPT_SGD_THREADS = 4  /* host threads of the server update (default: hardware threads, max 16) */
+    DC_OPT_SGD_THREADS = 4, /* host threads of the server update (default: hardware threads, max 16) */
+    DC_OPT_GRAPHS = 5       /* 1: each layer's forward and backward kernels run as one captured HIP graph
+                               launch (default 0: launched one by one).  The graphs are captured at the first
+                               dc_step / dc_profile for a workspace and batch address (a one-time cost) and
+                               recaptured when either changes; results are identical either way.  A graph
+                               launch costs more than it saves unless a layer is many kernels of ~1 us */
 };
 int dc_model_set_option(dc_model *m, int option, double value);
 

@@ -17,7 +17,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libdc.so")
 
 DC_OK, DC_EINVAL, DC_EHIP, DC_ENOMEM, DC_ESTATE, DC_ETIMEOUT = range(6)
 DC_OP_CONV, DC_OP_FC, DC_OP_BN, DC_OP_RELU, DC_OP_MAXPOOL, DC_OP_GAP, DC_OP_ADD, DC_OP_CONCAT, DC_OP_AVGPOOL = range(1, 10)
-DC_OPT_LR, DC_OPT_TIMELINE, DC_OPT_TIMEOUT_S, DC_OPT_SGD_THREADS = range(1, 5)
+DC_OPT_LR, DC_OPT_TIMELINE, DC_OPT_TIMEOUT_S, DC_OPT_SGD_THREADS, DC_OPT_GRAPHS = range(1, 6)
 
 c_i32, c_i64, c_f32, c_f64, c_sz, c_vp = (ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_double,
                                           ctypes.c_size_t, ctypes.c_void_p)

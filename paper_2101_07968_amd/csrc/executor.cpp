@@ -198,7 +198,7 @@ int step_impl(dc_model *m, const dc_batch *b, dc_plan_t *plan, const dc_profile_
         }
         if (m->timeline)
             DC_HIP(hipEventRecord(m->ev_fwd_start[l], cs));
-        DC_TRY(run_forward_layer(m, l, b->x_dev, b->y_dev, cs));
+        DC_TRY(launch_forward_layer(m, l, b->x_dev, b->y_dev, cs));
         if (m->timeline || l == L)
             DC_HIP(hipEventRecord(m->ev_fwd_end[l], cs));
     }
@@ -216,7 +216,7 @@ int step_impl(dc_model *m, const dc_batch *b, dc_plan_t *plan, const dc_profile_
     // backward, closing push segments as their lowest layer finishes
     size_t k = 0;
     for (int l = L; l >= 1; --l) {
-        DC_TRY(run_backward_layer(m, l, b->x_dev, cs));
+        DC_TRY(launch_backward_layer(m, l, b->x_dev, cs));
         if (m->timeline)
             DC_HIP(hipEventRecord(m->ev_bwd_end[l], cs));
         if (k < pushes.size() && pushes[k].lo == l) {
@@ -446,19 +446,19 @@ extern "C" int dc_profile(dc_model *m, const dc_batch *b, const dc_link *link, i
     // every parameter on the device, then one untimed pass
     DC_HIP(hipMemcpyAsync(m->dparams(), m->ps_params, m->n_params * sizeof(float), hipMemcpyHostToDevice, cs));
     for (int l = 1; l <= L; ++l)
-        DC_TRY(run_forward_layer(m, l, b->x_dev, b->y_dev, cs));
+        DC_TRY(launch_forward_layer(m, l, b->x_dev, b->y_dev, cs));
     for (int l = L; l >= 1; --l)
-        DC_TRY(run_backward_layer(m, l, b->x_dev, cs));
+        DC_TRY(launch_backward_layer(m, l, b->x_dev, cs));
     DC_HIP(hipStreamSynchronize(cs));
     std::vector<double> fsum(L + 1, 0.0), bsum(L + 1, 0.0);
     for (int r = 0; r < reps; ++r) {
         DC_HIP(hipEventRecord(m->ev_fwd_end[0], cs));
         for (int l = 1; l <= L; ++l) {
-            DC_TRY(run_forward_layer(m, l, b->x_dev, b->y_dev, cs));
+            DC_TRY(launch_forward_layer(m, l, b->x_dev, b->y_dev, cs));
             DC_HIP(hipEventRecord(m->ev_fwd_end[l], cs));
         }
         for (int l = L; l >= 1; --l) {
-            DC_TRY(run_backward_layer(m, l, b->x_dev, cs));
+            DC_TRY(launch_backward_layer(m, l, b->x_dev, cs));
             DC_HIP(hipEventRecord(m->ev_bwd_end[l], cs));
         }
         DC_HIP(hipEventSynchronize(m->ev_bwd_end[1]));

@@ -345,6 +345,82 @@ int run_backward_layer(dc_model *m, int l, const float *x, hipStream_t s) {
     return DC_OK;
 }
 
+// ---------------------------------------------------------------- per-layer HIP graphs
+
+void drop_graphs(dc_model *m) {
+    for (auto *v : {&m->g_fwd, &m->g_bwd})
+        for (auto &g : *v)
+            if (g) {
+                (void)hipGraphExecDestroy(g);
+                g = nullptr;
+            }
+    m->g_ws = nullptr;
+    m->g_x = nullptr;
+    m->g_y = nullptr;
+}
+
+// Capture the work of one layer and direction on the private stream.  The
+// capture is always ended, also when enqueueing fails, so the stream never
+// stays in capture mode.
+static int capture_layer(dc_model *m, int l, bool fwd, const float *x, const int32_t *y, hipGraphExec_t *out) {
+    DC_HIP(hipStreamBeginCapture(m->cap_s, hipStreamCaptureModeThreadLocal));
+    const int st = fwd ? run_forward_layer(m, l, x, y, m->cap_s) : run_backward_layer(m, l, x, m->cap_s);
+    hipGraph_t g = nullptr;
+    const hipError_t e = hipStreamEndCapture(m->cap_s, &g);
+    if (st != DC_OK) {
+        if (g)
+            (void)hipGraphDestroy(g);
+        return st;
+    }
+    if (e != hipSuccess)
+        return hip_fail(e, "hipStreamEndCapture");
+    const hipError_t ei = hipGraphInstantiate(out, g, nullptr, nullptr, 0);
+    (void)hipGraphDestroy(g);
+    if (ei != hipSuccess)
+        return hip_fail(ei, "hipGraphInstantiate");
+    return DC_OK;
+}
+
+static int ensure_graphs(dc_model *m, const float *x, const int32_t *y) {
+    if (m->g_ws == m->ws && m->g_x == x && m->g_y == y && (int)m->g_fwd.size() == m->L + 1)
+        return DC_OK;
+    drop_graphs(m);
+    if (!m->cap_s)
+        DC_HIP(hipStreamCreateWithFlags(&m->cap_s, hipStreamNonBlocking));
+    m->g_fwd.assign(m->L + 1, nullptr);
+    m->g_bwd.assign(m->L + 1, nullptr);
+    for (int l = 1; l <= m->L; ++l) {
+        int st = capture_layer(m, l, true, x, y, &m->g_fwd[l]);
+        if (st == DC_OK)
+            st = capture_layer(m, l, false, x, y, &m->g_bwd[l]);
+        if (st != DC_OK) {
+            drop_graphs(m);
+            return st;
+        }
+    }
+    m->g_ws = m->ws;
+    m->g_x = x;
+    m->g_y = y;
+    return DC_OK;
+}
+
+int launch_forward_layer(dc_model *m, int l, const float *x, const int32_t *y, hipStream_t s) {
+    if (!m->use_graphs)
+        return run_forward_layer(m, l, x, y, s);
+    DC_TRY(ensure_graphs(m, x, y));
+    DC_HIP(hipGraphLaunch(m->g_fwd[l], s));
+    return DC_OK;
+}
+
+int launch_backward_layer(dc_model *m, int l, const float *x, hipStream_t s) {
+    // the forward call for the same batch captured the graphs; without them
+    // (graphs off, or a batch the forward pass has not seen) launch directly
+    if (!m->use_graphs || m->g_ws != m->ws || m->g_x != x || (int)m->g_bwd.size() != m->L + 1)
+        return run_backward_layer(m, l, x, s);
+    DC_HIP(hipGraphLaunch(m->g_bwd[l], s));
+    return DC_OK;
+}
+
 } // namespace dc
 
 // ---------------------------------------------------------------- C ABI: model and parameter server
@@ -434,6 +510,9 @@ extern "C" void dc_model_destroy(dc_model *m) {
                 (void)hipEventDestroy(ev);
     if (m->ev_t0)
         (void)hipEventDestroy(m->ev_t0);
+    drop_graphs(m);
+    if (m->cap_s)
+        (void)hipStreamDestroy(m->cap_s);
     if (m->pull_s)
         (void)hipStreamDestroy(m->pull_s);
     if (m->push_s)
@@ -460,6 +539,7 @@ extern "C" int dc_model_bind_workspace(dc_model *m, void *dev, size_t bytes) {
         return fail(DC_EINVAL, "workspace must be 256-byte aligned");
     if (bytes < m->ws_need)
         return fail(DC_ENOMEM, "workspace has %zu bytes, the model needs %zu", bytes, m->ws_need);
+    drop_graphs(m); // they hold the old workspace's addresses
     m->ws = static_cast<char *>(dev);
     m->ws_bytes = bytes;
     return DC_OK;
@@ -491,6 +571,9 @@ extern "C" int dc_model_set_option(dc_model *m, int option, double value) {
         if (!(value > 0))
             return fail(DC_EINVAL, "timeout must be positive");
         m->timeout_s = value;
+        return DC_OK;
+    case DC_OPT_GRAPHS:
+        m->use_graphs = value != 0.0;
         return DC_OK;
     case DC_OPT_SGD_THREADS: {
         int t = (int)value;

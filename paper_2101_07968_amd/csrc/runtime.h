@@ -83,6 +83,18 @@ struct dc_model {
     std::vector<int64_t> timeline_ns;
     bool timeline_valid = false;
 
+    // Per-layer HIP graphs (DC_OPT_GRAPHS): the kernels of each layer's
+    // forward and backward mini-procedures, captured once on a private
+    // stream and replayed with one launch each.  They hold the workspace and
+    // batch addresses they were captured with and are rebuilt when those
+    // change.
+    int use_graphs = 0;
+    hipStream_t cap_s = nullptr;
+    std::vector<hipGraphExec_t> g_fwd, g_bwd; // index 1..L
+    const char *g_ws = nullptr;
+    const float *g_x = nullptr;
+    const int32_t *g_y = nullptr;
+
     float *dparams() const { return reinterpret_cast<float *>(ws + off_params); }
     float *dgrads() const { return reinterpret_cast<float *>(ws + off_grads); }
     float *act(int t) const { return reinterpret_cast<float *>(ws + tensors[t].act); }
@@ -98,4 +110,9 @@ namespace dc {
 int run_forward_layer(dc_model *m, int l, const float *x, const int32_t *y, hipStream_t s);
 // Enqueue the backward mini-procedures of layer l (x: the input batch).
 int run_backward_layer(dc_model *m, int l, const float *x, hipStream_t s);
+// The same work through the layer's HIP graph when DC_OPT_GRAPHS is on (the
+// graphs are captured at the first call for a workspace and batch).
+int launch_forward_layer(dc_model *m, int l, const float *x, const int32_t *y, hipStream_t s);
+int launch_backward_layer(dc_model *m, int l, const float *x, hipStream_t s);
+void drop_graphs(dc_model *m);
 } // namespace dc

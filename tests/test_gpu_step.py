@@ -270,6 +270,36 @@ def test_checkpoint_resume_is_bit_exact(name, batch):
     fresh.close()
 
 
+@pytest.mark.parametrize("name,batch", [("tiny", 4), ("resnet18", 8), ("googlenet", 2)])
+def test_layer_graphs_replay_the_eager_iteration(name, batch):
+    """DC_OPT_GRAPHS: each layer's kernels replayed from a captured HIP graph give
+    bit-identical steps to launching them one by one, over several replays with
+    the other model's eager work in between, and after a new batch address
+    forces a recapture."""
+    g_model, onet, xd, yd, x, y, params = setup_model(name, batch, seed=13)
+    g_model.set_option(D.DC_OPT_GRAPHS, 1)
+    ops, hwc, classes = PN.build(name)
+    e_model = D.Model(ops, batch, hwc, classes)
+    e_model.set_option(D.DC_OPT_GRAPHS, 0)
+    e_model.ps_write(params)
+    plan = plans_for(g_model.L, seed=4)["random"]
+    x2, y2, _ = synth.cnn_inputs(14, batch, hwc, classes, onet.param_specs)
+    batches = [(xd, yd), (xd, yd), (dev(x2), dev(y2)), (xd, yd)]
+    for i, (bx, by) in enumerate(batches):
+        st_g = g_model.step(bx, by, plan, UNPACED)
+        st_e = e_model.step(bx, by, plan, UNPACED)
+        p_g, g_g = g_model.ps_read()
+        p_e, g_e = e_model.ps_read()
+        assert st_g["loss"] == st_e["loss"], i
+        np.testing.assert_array_equal(g_g, g_e, err_msg=str(i))
+        np.testing.assert_array_equal(p_g, p_e, err_msg=str(i))
+    # profiles come from the same (graph) launches the steps use
+    prof = g_model.profile(xd, yd, UNPACED, reps=1)
+    assert (prof.fc > 0).all() and (prof.bc > 0).all()
+    g_model.close()
+    e_model.close()
+
+
 def test_dynamic_step_plans_in_idle_windows():
     """dc_step_dynamic (idle-event trigger, Sec. IV-C): same decisions as dc_plan,
     same numbers as dc_step, and planning finished while a transfer was in flight."""
