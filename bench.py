@@ -65,9 +65,8 @@ def calibration_copy(D, nbytes=256 << 20):
 
 def traffic_from_profiles(name, batch):
     """HBM bytes per igemm launch from the committed rocprofv3 counter summary, if it
-    was taken on the current kernel source; else None."""
-    import hashlib
-    src = os.path.join(ROOT, "paper_2101_07968_amd", "csrc", "igemm.hip")
+    was taken on the current kernel and plan-table sources; else None."""
+    from paper_2101_07968_amd.profsum import gemm_sources_sha256
     path = os.path.join(ROOT, "profiles", f"igemm_{name}_b{batch}_traffic.txt")
     if not os.path.exists(path):
         return None
@@ -76,8 +75,7 @@ def traffic_from_profiles(name, batch):
         if "=" in line and not line.startswith("#"):
             k, v = line.strip().split("=", 1)
             kv[k.strip()] = v.strip()
-    sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
-    if kv.get("igemm_source_sha256") != sha:
+    if kv.get("gemm_sources_sha256") != gemm_sources_sha256():
         return None
     return float(kv["hbm_bytes_per_launch"]), float(kv["algorithmic_bytes_per_launch"])
 

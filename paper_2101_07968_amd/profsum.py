@@ -34,6 +34,18 @@ import re
 HERE = os.path.dirname(os.path.abspath(__file__))
 
 
+GEMM_SOURCES = ("igemm.hip", "plan_table.cpp", "plan_table.inc")
+
+
+def gemm_sources_sha256():
+    """One hash over the conv GEMM kernels and their launch-plan table: a counter
+    summary is only valid for the sources it was taken on."""
+    h = hashlib.sha256()
+    for name in GEMM_SOURCES:
+        h.update(open(os.path.join(HERE, "csrc", name), "rb").read())
+    return h.hexdigest()
+
+
 def short(name):
     name = name.replace("dc::(anonymous namespace)::", "")
     name = re.sub(r"\(.*$", "", name) if not is_gemm(name) else name.split("(")[0]
@@ -107,7 +119,7 @@ def cmd_traffic(a):
     ops, hwc, _ = PN.build(a.workload)
     passes = conv_bytes(PN.conv_geoms(ops, hwc, a.batch))
     algo = sum(b for _, b in passes) / len(passes)
-    sha = hashlib.sha256(open(os.path.join(HERE, "csrc", "igemm.hip"), "rb").read()).hexdigest()
+    sha = gemm_sources_sha256()
     print(f"# HBM traffic of the implicit-GEMM kernel, {a.workload} batch {a.batch}")
     print(f"# commands: {a.cmd}")
     print(f"# calibration: {a.cal_bytes} B copy read as FETCH_SIZE {cal_f[0]:.1f} KiB, WRITE_SIZE {cal_w[0]:.1f} KiB")
@@ -118,7 +130,7 @@ def cmd_traffic(a):
     print(f"hbm_bytes_per_launch={hbm:.0f}")
     print(f"algorithmic_bytes_per_launch={algo:.0f}")
     print(f"hbm_over_algorithmic={hbm / algo:.3f}")
-    print(f"igemm_source_sha256={sha}")
+    print(f"gemm_sources_sha256={sha}")
 
 
 def _trace_durations(path, keep):
@@ -174,7 +186,7 @@ def cmd_mfma(a):
     print(f"gpu_active_cycles_per_xcd={active / a.xcds:.4e} (over {sum(dur) / 1e6:.2f} ms: "
           f"{active / a.xcds / sum(dur):.2f} GHz)")
     print(f"mfma_busy_percent={100.0 * busy / (active / a.xcds * simds):.1f}")
-    print(f"igemm_source_sha256={hashlib.sha256(open(os.path.join(HERE, 'csrc', 'igemm.hip'), 'rb').read()).hexdigest()}")
+    print(f"gemm_sources_sha256={gemm_sources_sha256()}")
 
 
 def cmd_hbm(a):
