@@ -87,9 +87,12 @@ int colsum(int64_t rows, int c, const float *x, float *out, void *ws, hipStream_
 size_t bn_ws_bytes(int64_t rows, int c);
 int bn_forward(int64_t rows, int c, const float *x, const float *gamma, const float *beta,
                float eps, int relu, float *y, float *mean, float *invstd, void *ws, hipStream_t s);
+// relu_y, if given, is the output of a ReLU applied to this BN's output: dy is
+// then the ReLU's output gradient and passes through the ReLU's backward
+// (kept where relu_y > 0) on the way in, so no separate ReLU pass is needed.
 int bn_backward(int64_t rows, int c, const float *dy, const float *x, const float *gamma,
                 const float *mean, const float *invstd, int accumulate, float *dx, float *dgamma,
-                float *dbeta, void *ws, hipStream_t s);
+                float *dbeta, void *ws, hipStream_t s, const float *relu_y = nullptr);
 int relu_forward(const float *x, float *y, int64_t n, hipStream_t s);
 int relu_backward(const float *dy, const float *y, int accumulate, float *dx, int64_t n,
                   hipStream_t s);

@@ -401,7 +401,7 @@ template <int MODE>
 __global__ __launch_bounds__(EW_THREADS) void colred_partial_kernel(
     int64_t rows, int c, int64_t rows_per_chunk, const float *__restrict__ x, const float *__restrict__ dy,
     const float *__restrict__ mean, const float *__restrict__ invstd, float *__restrict__ part0,
-    float *__restrict__ part1) {
+    float *__restrict__ part1, const float *__restrict__ relu_y) {
     __shared__ float s0[RL][CG];
     __shared__ float s1[RL][CG];
     const int lane_c = threadIdx.x % CG, rl = threadIdx.x / CG;
@@ -420,7 +420,7 @@ __global__ __launch_bounds__(EW_THREADS) void colred_partial_kernel(
                 float d = x[o] - mu;
                 a0 += d * d;
             } else {
-                float g = dy[o];
+                float g = relu_y ? relu_grad(dy[o], relu_y[o]) : dy[o];
                 a0 += g;
                 a1 += g * ((x[o] - mu) * is);
             }
@@ -505,14 +505,16 @@ __global__ void bn_apply_kernel(int64_t rows, int c, const float *__restrict__ x
 __global__ void bn_bwd_apply_kernel(int64_t rows, int c, const float *__restrict__ dy, const float *__restrict__ x,
                                     const float *__restrict__ gamma, const float *__restrict__ mean,
                                     const float *__restrict__ invstd, const float *__restrict__ dgamma,
-                                    const float *__restrict__ dbeta, int acc, float *__restrict__ dx) {
+                                    const float *__restrict__ dbeta, int acc, float *__restrict__ dx,
+                                    const float *__restrict__ relu_y) {
     const int64_t total = rows * c;
     const float inv_rows = 1.0f / (float)rows;
     for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total; e += (int64_t)gridDim.x * blockDim.x) {
         int ch = (int)(e % c);
         float is = invstd[ch];
         float xhat = (x[e] - mean[ch]) * is;
-        float g = gamma[ch] * is * (dy[e] - dbeta[ch] * inv_rows - xhat * dgamma[ch] * inv_rows);
+        const float d = relu_y ? relu_grad(dy[e], relu_y[e]) : dy[e];
+        float g = gamma[ch] * is * (d - dbeta[ch] * inv_rows - xhat * dgamma[ch] * inv_rows);
         dx[e] = acc ? dx[e] + g : g;
     }
 }
@@ -526,6 +528,17 @@ __global__ void bn_bwd_apply_kernel(int64_t rows, int c, const float *__restrict
 // slots.  Mode 0: sum x.  Mode 1: sum (x - K) and sum (x - K)^2 with K the
 // channel's value in row 0, a shift that keeps the one-pass variance free of
 // cancellation.  Mode 2: sum dy and sum dy * (x - mean) * invstd.
+// The float4 of dy at element o, passed through ReLU's backward (kept where
+// the ReLU's output relu_y is positive) when relu_y is given.
+__device__ __forceinline__ float4 dy4_at(const float *dy, const float *relu_y, int64_t o) {
+    float4 d = *reinterpret_cast<const float4 *>(dy + o);
+    if (relu_y) {
+        const float4 y = *reinterpret_cast<const float4 *>(relu_y + o);
+        d = make_float4(relu_grad(d.x, y.x), relu_grad(d.y, y.y), relu_grad(d.z, y.z), relu_grad(d.w, y.w));
+    }
+    return d;
+}
+
 template <int MODE>
 __device__ __forceinline__ void col4_acc(float4 &a0, float4 &a1, const float4 v, const float4 d, const float4 mu,
                                          const float4 is) {
@@ -552,7 +565,7 @@ template <int MODE>
 __global__ __launch_bounds__(EW_THREADS) void colred4_partial_kernel(
     int64_t rows, int c, int64_t rpc, int g, int rl_n, const float *__restrict__ x, const float *__restrict__ dy,
     const float *__restrict__ mean, const float *__restrict__ invstd, float *__restrict__ part0,
-    float *__restrict__ part1) {
+    float *__restrict__ part1, const float *__restrict__ relu_y) {
     __shared__ float4 s0[EW_THREADS];
     __shared__ float4 s1[EW_THREADS];
     const int t = threadIdx.x;
@@ -576,15 +589,15 @@ __global__ __launch_bounds__(EW_THREADS) void colred4_partial_kernel(
             const int64_t o0 = r * c + ch, o1 = (r + rl_n) * c + ch;
             const float4 v0 = *reinterpret_cast<const float4 *>(x + o0);
             const float4 v1 = *reinterpret_cast<const float4 *>(x + o1);
-            const float4 d0 = MODE == 2 ? *reinterpret_cast<const float4 *>(src + o0) : z4;
-            const float4 d1 = MODE == 2 ? *reinterpret_cast<const float4 *>(src + o1) : z4;
+            const float4 d0 = MODE == 2 ? dy4_at(src, relu_y, o0) : z4;
+            const float4 d1 = MODE == 2 ? dy4_at(src, relu_y, o1) : z4;
             col4_acc<MODE>(a0, a1, v0, d0, mu, is);
             col4_acc<MODE>(b0, b1, v1, d1, mu, is);
         }
         if (r < r1) {
             const int64_t o0 = r * c + ch;
             const float4 v0 = *reinterpret_cast<const float4 *>(x + o0);
-            const float4 d0 = MODE == 2 ? *reinterpret_cast<const float4 *>(src + o0) : z4;
+            const float4 d0 = MODE == 2 ? dy4_at(src, relu_y, o0) : z4;
             col4_acc<MODE>(a0, a1, v0, d0, mu, is);
         }
     }
@@ -637,14 +650,19 @@ __global__ void bn_bwd_apply4_kernel(int64_t n4, int c4, int64_t rows, const flo
                                      const float4 *__restrict__ x, const float4 *__restrict__ gamma,
                                      const float4 *__restrict__ mean, const float4 *__restrict__ invstd,
                                      const float4 *__restrict__ dgamma, const float4 *__restrict__ dbeta, int acc,
-                                     float4 *__restrict__ dx) {
+                                     float4 *__restrict__ dx, const float4 *__restrict__ relu_y) {
     const int64_t t0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     const int q = (int)(t0 % c4);
     const float inv_rows = 1.0f / (float)rows;
     const float4 g = gamma[q], m = mean[q], is = invstd[q], dg = dgamma[q], db = dbeta[q];
     for (int64_t i = t0; i < n4; i += stride) {
-        const float4 d = dy[i], v = x[i];
+        float4 d = dy[i];
+        const float4 v = x[i];
+        if (relu_y) {
+            const float4 y = relu_y[i];
+            d = make_float4(relu_grad(d.x, y.x), relu_grad(d.y, y.y), relu_grad(d.z, y.z), relu_grad(d.w, y.w));
+        }
         float4 o;
         o.x = bn_dx(d.x, v.x, g.x, m.x, is.x, dg.x, db.x, inv_rows);
         o.y = bn_dx(d.y, v.y, g.y, m.y, is.y, dg.y, db.y, inv_rows);
@@ -974,14 +992,14 @@ int colsum(int64_t rows, int c, const float *x, float *out, void *ws, hipStream_
         Col4Plan p = col4_plan(rows, c);
         hipLaunchKernelGGL(colred4_partial_kernel<0>, dim3(p.nchunks, p.blocks), dim3(EW_THREADS), 0, s, rows, c,
                            p.rpc, p.g, p.rl_n, x, (const float *)nullptr, (const float *)nullptr,
-                           (const float *)nullptr, part, (float *)nullptr);
+                           (const float *)nullptr, part, (float *)nullptr, (const float *)nullptr);
         nchunks = p.nchunks;
     } else {
         ColPlan p = col_plan(rows, c);
         dim3 g1(p.nchunks, (c + CG - 1) / CG);
         hipLaunchKernelGGL(colred_partial_kernel<0>, g1, dim3(EW_THREADS), 0, s, rows, c, p.rows_per_chunk, x,
                            (const float *)nullptr, (const float *)nullptr, (const float *)nullptr, part,
-                           (float *)nullptr);
+                           (float *)nullptr, (const float *)nullptr);
         nchunks = p.nchunks;
     }
     DC_HIP(hipGetLastError());
@@ -1005,7 +1023,7 @@ int bn_forward(int64_t rows, int c, const float *x, const float *gamma, const fl
         Col4Plan p = col4_plan(rows, c);
         hipLaunchKernelGGL(colred4_partial_kernel<1>, dim3(p.nchunks, p.blocks), dim3(EW_THREADS), 0, s, rows, c,
                            p.rpc, p.g, p.rl_n, x, (const float *)nullptr, (const float *)nullptr,
-                           (const float *)nullptr, part, part1);
+                           (const float *)nullptr, part, part1, (const float *)nullptr);
         DC_HIP(hipGetLastError());
         hipLaunchKernelGGL(colred_final_kernel<4>, dim3(c), dim3(EW_THREADS), 0, s, p.nchunks, c, rows, eps, part,
                            (const float *)part1, mean, invstd, x);
@@ -1021,13 +1039,15 @@ int bn_forward(int64_t rows, int c, const float *x, const float *gamma, const fl
     ColPlan p = col_plan(rows, c);
     dim3 g1(p.nchunks, (c + CG - 1) / CG);
     hipLaunchKernelGGL(colred_partial_kernel<0>, g1, dim3(EW_THREADS), 0, s, rows, c, p.rows_per_chunk, x,
-                       (const float *)nullptr, (const float *)nullptr, (const float *)nullptr, part, (float *)nullptr);
+                       (const float *)nullptr, (const float *)nullptr, (const float *)nullptr, part, (float *)nullptr,
+                       (const float *)nullptr);
     DC_HIP(hipGetLastError());
     hipLaunchKernelGGL(colred_final_kernel<1>, dim3(c), dim3(EW_THREADS), 0, s, p.nchunks, c, rows, eps, part,
                        (const float *)nullptr, mean, (float *)nullptr, (const float *)nullptr);
     DC_HIP(hipGetLastError());
     hipLaunchKernelGGL(colred_partial_kernel<1>, g1, dim3(EW_THREADS), 0, s, rows, c, p.rows_per_chunk, x,
-                       (const float *)nullptr, (const float *)mean, (const float *)nullptr, part, (float *)nullptr);
+                       (const float *)nullptr, (const float *)mean, (const float *)nullptr, part, (float *)nullptr,
+                       (const float *)nullptr);
     DC_HIP(hipGetLastError());
     hipLaunchKernelGGL(colred_final_kernel<2>, dim3(c), dim3(EW_THREADS), 0, s, p.nchunks, c, rows, eps, part,
                        (const float *)nullptr, invstd, (float *)nullptr, (const float *)nullptr);
@@ -1040,25 +1060,27 @@ int bn_forward(int64_t rows, int c, const float *x, const float *gamma, const fl
 }
 
 int bn_backward(int64_t rows, int c, const float *dy, const float *x, const float *gamma, const float *mean,
-                const float *invstd, int accumulate, float *dx, float *dgamma, float *dbeta, void *ws, hipStream_t s) {
+                const float *invstd, int accumulate, float *dx, float *dgamma, float *dbeta, void *ws, hipStream_t s,
+                const float *relu_y) {
     if (rows <= 0 || c <= 0)
         return DC_OK;
     float *part0 = static_cast<float *>(ws);
     float *part1 = reinterpret_cast<float *>(static_cast<char *>(ws) +
                                              align256((size_t)col_slots(rows, c) * c * sizeof(float)));
     const bool v4 = col4_ok(c, dy, x) && col4_ok(c, gamma, mean) && col4_ok(c, invstd, dgamma) &&
-                    col4_ok(c, dbeta, part0) && col4_ok(c, part1) && (!dx || col4_ok(c, dx));
+                    col4_ok(c, dbeta, part0) && col4_ok(c, part1) && (!dx || col4_ok(c, dx)) &&
+                    (!relu_y || col4_ok(c, relu_y));
     int nchunks;
     if (v4) {
         Col4Plan p = col4_plan(rows, c);
         hipLaunchKernelGGL(colred4_partial_kernel<2>, dim3(p.nchunks, p.blocks), dim3(EW_THREADS), 0, s, rows, c,
-                           p.rpc, p.g, p.rl_n, x, dy, mean, invstd, part0, part1);
+                           p.rpc, p.g, p.rl_n, x, dy, mean, invstd, part0, part1, relu_y);
         nchunks = p.nchunks;
     } else {
         ColPlan p = col_plan(rows, c);
         dim3 g1(p.nchunks, (c + CG - 1) / CG);
         hipLaunchKernelGGL(colred_partial_kernel<2>, g1, dim3(EW_THREADS), 0, s, rows, c, p.rows_per_chunk, x, dy,
-                           mean, invstd, part0, part1);
+                           mean, invstd, part0, part1, relu_y);
         nchunks = p.nchunks;
     }
     DC_HIP(hipGetLastError());
@@ -1072,11 +1094,12 @@ int bn_backward(int64_t rows, int c, const float *dy, const float *x, const floa
                                rows, reinterpret_cast<const float4 *>(dy), reinterpret_cast<const float4 *>(x),
                                reinterpret_cast<const float4 *>(gamma), reinterpret_cast<const float4 *>(mean),
                                reinterpret_cast<const float4 *>(invstd), reinterpret_cast<const float4 *>(dgamma),
-                               reinterpret_cast<const float4 *>(dbeta), accumulate, reinterpret_cast<float4 *>(dx));
+                               reinterpret_cast<const float4 *>(dbeta), accumulate, reinterpret_cast<float4 *>(dx),
+                               reinterpret_cast<const float4 *>(relu_y));
         } else {
             int64_t total = rows * c;
             hipLaunchKernelGGL(bn_bwd_apply_kernel, dim3(ew_blocks(total)), dim3(EW_THREADS), 0, s, rows, c, dy, x,
-                               gamma, mean, invstd, dgamma, dbeta, accumulate, dx);
+                               gamma, mean, invstd, dgamma, dbeta, accumulate, dx, relu_y);
         }
         DC_HIP(hipGetLastError());
     }

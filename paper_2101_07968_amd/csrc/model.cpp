@@ -193,6 +193,7 @@ static int build_model(dc_model *m, const dc_op_desc *ops, int n_ops) {
             nx.d.kind == DC_OP_RELU && nx.d.in0 == o.out && consumers[o.out] == 1 && nx.d.layer == o.d.layer) {
             o.relu_into = nx.out;
             nx.fwd_folded = true;
+            nx.bwd_folded = kd == DC_OP_BN;
         }
     }
 
@@ -311,11 +312,16 @@ int run_backward_layer(dc_model *m, int l, const float *x, hipStream_t s) {
             break;
         case DC_OP_BN: {
             const float *mean = reinterpret_cast<const float *>(m->ws + o.aux);
-            DC_TRY(bn_backward((int64_t)ti.n * ti.h * ti.w, ti.c, dy, in, P + o.w_off, mean, mean + ti.c, o.acc_in[0],
-                               dx, G + o.w_off, G + o.b_off, m->scratch(), s));
+            // a folded ReLU: take its output gradient and mask it on the way in
+            const bool fold = o.relu_into >= 0 && m->ops[i + 1].bwd_folded;
+            DC_TRY(bn_backward((int64_t)ti.n * ti.h * ti.w, ti.c, fold ? m->grad(o.relu_into) : dy, in, P + o.w_off,
+                               mean, mean + ti.c, o.acc_in[0], dx, G + o.w_off, G + o.b_off, m->scratch(), s,
+                               fold ? m->act(o.relu_into) : nullptr));
             break;
         }
         case DC_OP_RELU:
+            if (o.bwd_folded)
+                break; // done by the BN that produced its input
             DC_TRY(relu_backward(dy, m->act(o.out), o.acc_in[0], dx, ti.size(), s));
             break;
         case DC_OP_MAXPOOL:

@@ -42,6 +42,10 @@ struct OpInfo {
     // ReLU's output, the producer's backward reads its inputs).
     int relu_into = -1;
     bool fwd_folded = false;
+    // Backward ReLU folding, for a BN with relu_into set: the BN's backward
+    // reads the ReLU's output gradient and masks it with the ReLU's output,
+    // and the ReLU's backward (bwd_folded) does nothing.
+    bool bwd_folded = false;
 };
 
 } // namespace dc
