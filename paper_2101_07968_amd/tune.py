@@ -10,7 +10,7 @@ interleaved rounds; the median decides.  A shape enters the table only when
 its winner beats the cost model's choice by more than --margin, so timing
 noise does not churn plans.  Needs a GPU; run from the repository root:
 
-    python -m paper_2101_07968_amd.tune --out gpurun_out/plan_table.inc
+    python -m paper_2101_07968_amd.tune --out plan_table.inc
 
 then copy the output over ``paper_2101_07968_amd/csrc/plan_table.inc`` and
 rebuild.
