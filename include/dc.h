@@ -106,6 +106,9 @@ typedef struct dc_model dc_model;
  */
 int dc_model_create(const dc_op_desc *ops, int n_ops, int batch, int in_h, int in_w, int in_c,
                     int classes, dc_model **out);
+/* Waits for the library's own work (side streams, and what dc_step queued last
+ * on the caller's stream), then frees the model.  The caller's workspace and
+ * any other work on its stream stay the caller's to synchronise. */
 void dc_model_destroy(dc_model *m);
 
 int dc_model_num_layers(const dc_model *m);      /* L */

@@ -226,6 +226,7 @@ int step_impl(dc_model *m, const dc_batch *b, dc_plan_t *plan, const dc_profile_
     }
     float *loss_host = m->probe_host; // first float of the pinned probe buffer
     DC_HIP(hipMemcpyAsync(loss_host, m->dloss(), sizeof(float), hipMemcpyDeviceToHost, cs));
+    DC_HIP(hipEventRecord(m->ev_cs_done, cs));
     // push stream
     for (size_t i = 0; i < pushes.size(); ++i) {
         size_t off;

@@ -492,6 +492,8 @@ extern "C" int dc_model_create(const dc_op_desc *ops, int n_ops, int batch, int 
             return cleanup(hip_fail(e, "hipEventCreate"));
     if ((e = hipEventCreate(&m->ev_t0)) != hipSuccess)
         return cleanup(hip_fail(e, "hipEventCreate"));
+    if ((e = hipEventCreate(&m->ev_cs_done)) != hipSuccess)
+        return cleanup(hip_fail(e, "hipEventCreate"));
     int wall = wall_clock_hz(&m->wall_hz);
     if (wall != DC_OK)
         return cleanup(wall);
@@ -509,6 +511,10 @@ extern "C" void dc_model_destroy(dc_model *m) {
         (void)hipStreamSynchronize(m->pull_s);
     if (m->push_s)
         (void)hipStreamSynchronize(m->push_s);
+    // a step that ended on the watchdog can leave the loss copy into
+    // probe_host queued on the caller's stream
+    if (m->ev_cs_done)
+        (void)hipEventSynchronize(m->ev_cs_done);
     for (auto *v : {&m->ev_pull_start, &m->ev_pull_done, &m->ev_bwd_done, &m->ev_push_start, &m->ev_push_done,
                     &m->ev_fwd_start, &m->ev_fwd_end, &m->ev_bwd_end})
         for (auto ev : *v)
@@ -516,6 +522,8 @@ extern "C" void dc_model_destroy(dc_model *m) {
                 (void)hipEventDestroy(ev);
     if (m->ev_t0)
         (void)hipEventDestroy(m->ev_t0);
+    if (m->ev_cs_done)
+        (void)hipEventDestroy(m->ev_cs_done);
     drop_graphs(m);
     if (m->cap_s)
         (void)hipStreamDestroy(m->cap_s);

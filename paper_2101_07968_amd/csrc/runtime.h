@@ -76,6 +76,9 @@ struct dc_model {
     std::vector<hipEvent_t> ev_pull_start, ev_pull_done, ev_bwd_done, ev_push_start, ev_push_done;
     std::vector<hipEvent_t> ev_fwd_start, ev_fwd_end, ev_bwd_end; // per layer, index 1..L (+ [0] / [L+1] sentinels)
     hipEvent_t ev_t0 = nullptr;
+    // last work dc_step enqueues on the caller's stream (the loss copy into
+    // probe_host); dc_model_destroy waits for it before freeing that buffer
+    hipEvent_t ev_cs_done = nullptr;
 
     double lr = 0.01;
     int timeline = 0;
