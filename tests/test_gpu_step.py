@@ -245,6 +245,24 @@ def test_watchdog_times_out_and_gpu_drains():
     assert np.isfinite(st["loss"])
 
 
+def test_destroy_right_after_watchdog():
+    """A step that ends on the watchdog leaves pulls, pushes and the loss
+    copy in flight; destroying the model at once must wait for the library's
+    own work before it frees the pinned buffers, and a new model then runs."""
+    import torch
+    model, onet, xd, yd, x, y, params = setup_model("tiny", 4, seed=0)
+    model.set_option(D.DC_OPT_TIMEOUT_S, 0.02)
+    with pytest.raises(D.DcError) as e:
+        model.step(xd, yd, D.Plan(4), D.link(2e6, 0, paced=True))
+    assert e.value.status == D.DC_ETIMEOUT
+    model.close()
+    torch.cuda.synchronize()
+    model2, onet, xd, yd, x, y, params = setup_model("tiny", 4, seed=0)
+    st = model2.step(xd, yd, D.Plan(4), UNPACED)
+    loss_ref, _, _ = onet.step(x, y, params)
+    assert abs(st["loss"] - loss_ref) <= 1e-4 * abs(loss_ref)
+
+
 @pytest.mark.parametrize("name,batch", [("tiny", 4), ("resnet18", 8)])
 def test_checkpoint_resume_is_bit_exact(name, batch):
     """The parameter server holds the whole training state (BatchNorm keeps no
