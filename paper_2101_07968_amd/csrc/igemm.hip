@@ -165,7 +165,12 @@ __device__ __forceinline__ float epilogue(const Args &a, int pass, float v, int 
 //  * forward with C % KT == 0, dgrad with K % KT == 0 and C % 4 == 0: every K
 //    stage lies inside one filter tap, so the tap and first channel of a
 //    stage are workgroup-uniform scalars and every stage is full; a
-//    fragment's offset is its row's base offset plus a per-stage delta;
+//    fragment's offset is its row's base offset plus a per-stage delta.  The
+//    stages run through every tap of one block of KT channels before the next
+//    block: the taps' overlapping input windows are then re-read while they
+//    are still in L2 (with channels innermost, the resident workgroups sweep
+//    all channels between two taps, more than an XCD's L2 holds, and the
+//    forward / dgrad passes fetched 4x more from memory);
 //  * wgrad with K % 4 == 0, C % 4 == 0 and Q >= KT: every B fragment's pixel
 //    advances by KT per stage (at most one row wrap), so its (q, p), input
 //    origin and offset are carried from stage to stage with uniform
@@ -370,29 +375,23 @@ __global__ __launch_bounds__(NTHR, TU ? 4 : 1) void igemm_kernel(Args a) {
 
     // TU stage cursor, uniform over the workgroup: first channel c0 of the
     // next stage to load and its tap, (r, s) for the forward pass or (tr, ts)
-    // for dgrad.  Set once by division, then advanced one stage at a time.
+    // for dgrad.  Stage kt covers channel block kt / T and tap kt % T (T taps,
+    // row-major).  Set once by division, then advanced one stage at a time.
+    constexpr bool FW = PASS == PASS_FWD;
     int cur_c0 = 0, cur_t1 = 0, cur_t2 = 0;
     auto cursor_init = [&](int kt) {
-        const int kbase = kt * KT;
-        if (PASS == PASS_FWD) {
-            const int tap = a.fC.div(kbase);
-            cur_c0 = kbase - tap * a.C;
-            cur_t1 = a.fS.div(tap);
-            cur_t2 = tap - cur_t1 * a.S;
-        } else {
-            const int tt = a.fK.div(kbase);
-            cur_c0 = kbase - tt * a.K;
-            cur_t1 = ph.St ? tt / ph.St : 0;
-            cur_t2 = tt - cur_t1 * ph.St;
-        }
+        const int t1n = FW ? a.R : ph.Rt, t2n = FW ? a.S : ph.St;
+        const int cb = kt / (t1n * t2n), tap = kt - cb * (t1n * t2n);
+        cur_c0 = cb * KT;
+        cur_t1 = tap / t2n;
+        cur_t2 = tap - cur_t1 * t2n;
     };
     auto cursor_next = [&]() {
-        cur_c0 += KT;
-        if (cur_c0 == (PASS == PASS_FWD ? a.C : a.K)) {
-            cur_c0 = 0;
-            if (++cur_t2 == (PASS == PASS_FWD ? a.S : ph.St)) {
-                cur_t2 = 0;
-                ++cur_t1;
+        if (++cur_t2 == (FW ? a.S : ph.St)) {
+            cur_t2 = 0;
+            if (++cur_t1 == (FW ? a.R : ph.Rt)) {
+                cur_t1 = 0;
+                cur_c0 += KT;
             }
         }
     };
@@ -519,7 +518,7 @@ __global__ __launch_bounds__(NTHR, TU ? 4 : 1) void igemm_kernel(Args a) {
 #pragma unroll
             for (int f = 0; f < FB; ++f) {
                 const bool jok = tn * NT + b_row[f] < a.Ng;
-                rb[f] = bld4(rs_b, (unsigned)(b_base[f] + kbase), jok);
+                rb[f] = bld4(rs_b, (unsigned)(b_base[f] + (cur_t1 * a.S + cur_t2) * a.C + cur_c0), jok);
             }
         } else if (PASS == PASS_FWD) { // B = W[k][kk], k-contiguous
 #pragma unroll
