@@ -244,6 +244,31 @@ def test_conv_full_size_sampled(case):
     assert rel_err(db, db_ref) <= tol(n * P * Q)
 
 
+def test_conv_operand_over_2gb_sampled():
+    """A 2.2 GB input (553,648,128 floats): past the lean mode's 2 GB limit, so
+    every pass runs on 64-bit element offsets that cross the 2^31-byte mark.
+    Sampled outputs, including the first and last element of each result,
+    against the oracle."""
+    shape = (66, 256, 256, 128, 16, 1, 1, 1, 0, 0)
+    n, h, w, c, k, r, s, st, pad, pad_w = shape
+    assert 4 * n * h * w * c >= 2 ** 31
+    print("conv over 2 GB: generating inputs", flush=True)
+    x = synth.random_tensor(90, (n, h, w, c))
+    wt = synth.random_tensor(91, (k, r, s, c), scale=math.sqrt(2.0 / (r * s * c)))
+    b = synth.random_tensor(92, (k,))
+    dy = synth.random_tensor(93, (n, h, w, k), scale=1e-3)
+    print("conv over 2 GB: running the three passes", flush=True)
+    y, dx, dw, db = run_conv(shape, x, wt, b, dy, 0, None)
+    print("conv over 2 GB: checking samples", flush=True)
+    rng = np.random.default_rng(94)
+    i = _sample(rng, y.shape, 48)
+    assert np.abs(y[tuple(i.T)] - OC.conv2d_samples("fwd", shape, x, wt, i, b)).max() <= tol(c) * np.abs(y).max()
+    i = _sample(rng, dx.shape, 48)
+    assert np.abs(dx[tuple(i.T)] - OC.conv2d_samples("dgrad", shape, dy, wt, i)).max() <= tol(k) * np.abs(dx).max()
+    i = _sample(rng, dw.shape, 32)
+    assert np.abs(dw[tuple(i.T)] - OC.conv2d_samples("wgrad", shape, x, dy, i)).max() <= tol(n * h * w) * np.abs(dw).max()
+
+
 def test_conv_rejects_bad_shapes_and_accepts_empty():
     sh = conv_shape(2, 4, 4, 3, 5, 3, 1, 3)  # pad >= r
     assert D.lib().dc_conv2d_forward(ctypes.byref(sh), 1, 1, None, 0, 1, None, 0, None) == D.DC_EINVAL
