@@ -343,6 +343,14 @@ class Model:
         return p, g
 
     def _batch(self, x, y):
+        """dc_batch of a float32 NHWC input and int32 labels, both contiguous device tensors."""
+        import torch
+        h, w, c = self.hwc
+        for t, dt, n, name in ((x, torch.float32, self.batch * h * w * c, "x"), (y, torch.int32, self.batch, "y")):
+            if not (isinstance(t, torch.Tensor) and t.is_cuda and t.dtype == dt and t.is_contiguous()
+                    and t.numel() == n):
+                raise DcError(DC_EINVAL, "dc_batch", f"{name} must be a contiguous {dt} device tensor of {n} "
+                              f"elements (batch {self.batch}, input {h}x{w}x{c})")
         return Batch(ptr(x), ptr(y), int(x.shape[0]))
 
     def profile(self, x, y, lnk, reps=3, stream=None):

@@ -255,6 +255,11 @@ def test_argument_errors():
     with pytest.raises(D.DcError) as e:
         model.step(xd, yd, D.Plan(4), D.link(0, 0, paced=True))
     assert e.value.status == D.DC_EINVAL
+    # the binding rejects inputs the library would misread: wrong dtype, host memory, strided views
+    for bad_x, bad_y in ((xd.double(), yd), (xd, yd.long()), (xd.cpu(), yd), (xd.transpose(1, 2), yd)):
+        with pytest.raises(D.DcError) as e:
+            model.step(bad_x, bad_y, D.Plan(4), UNPACED)
+        assert e.value.status == D.DC_EINVAL
     with pytest.raises(D.DcError) as e:
         model.set_option(D.DC_OPT_TIMEOUT_S, -1)
     assert e.value.status == D.DC_EINVAL
