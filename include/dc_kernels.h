@@ -130,8 +130,10 @@ int dc_batchnorm_backward(int64_t rows, int32_t c, const float *dy, const float 
                           size_t ws_bytes, void *stream);
 
 /* loss[0] = mean over n of (logsumexp(z_i) - z_i[y_i]); dz = (softmax(z) - onehot(y)) / n.
- * logits n x classes; labels outside [0, classes) give DC_EINVAL only if
- * checked by the caller: the kernel clamps nothing and treats them as no target. */
+ * logits n x classes.  Labels are not range-checked: a label outside
+ * [0, classes) is taken as "no target" (that sample contributes
+ * logsumexp(z_i) to the loss and softmax(z_i) / n to dz), and no memory
+ * outside the logits is read. */
 size_t dc_softmax_xent_workspace_bytes(int32_t n);
 int dc_softmax_xent(int32_t n, int32_t classes, const float *logits, const int32_t *labels,
                     float *loss, float *dlogits, void *ws, size_t ws_bytes, void *stream);
