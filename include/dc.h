@@ -269,7 +269,11 @@ typedef struct dc_step_stats {
  * range as soon as it lands.  Returns when every push and every update is
  * done.  `stream` is the compute stream.  The results do not depend on the
  * decisions.  Errors: DC_EINVAL (plan L or batch size mismatch, bad link),
- * DC_ESTATE (no workspace), DC_EHIP, DC_ETIMEOUT.
+ * DC_ESTATE (no workspace), DC_EHIP, DC_ETIMEOUT.  After DC_ETIMEOUT (the
+ * DC_OPT_TIMEOUT_S watchdog), copies and kernels of the iteration may still
+ * be running; they end on their own (every pacing wait is bounded), the
+ * server update of the unfinished segments is not applied, and
+ * dc_model_destroy waits for them.
  */
 int dc_step(dc_model *m, const dc_batch *b, const dc_plan_t *plan, const dc_link *link,
             void *stream, dc_step_stats *out);
