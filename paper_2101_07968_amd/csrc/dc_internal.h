@@ -105,8 +105,10 @@ int avgpool_forward(const dc_pool_shape &sh, const float *x, float *y, hipStream
 int avgpool_backward(const dc_pool_shape &sh, const float *dy, int accumulate, float *dx, hipStream_t s);
 int maxpool_forward(const dc_pool_shape &sh, const float *x, float *y, uint8_t *arg,
                     hipStream_t s);
+// relu_y, if given, is the pool's output: dx is then the gradient of the
+// input of a ReLU whose output the pool read, masked by that ReLU.
 int maxpool_backward(const dc_pool_shape &sh, const float *dy, const uint8_t *arg, int accumulate,
-                     float *dx, hipStream_t s);
+                     float *dx, hipStream_t s, const float *relu_y = nullptr);
 int gap_forward(int n, int hw, int c, const float *x, float *y, hipStream_t s);
 int gap_backward(int n, int hw, int c, const float *dy, int accumulate, float *dx, hipStream_t s);
 size_t xent_ws_bytes(int n);

@@ -170,8 +170,13 @@ __global__ void maxpool_fwd_kernel(dc_pool_shape sh, int P, int Q, const float *
     }
 }
 
+// MASK: dx is the gradient of a ReLU's input whose output the pool read; a
+// window adds its dy only where its maximum (the pool's output y) is > 0,
+// which is the ReLU's mask at the window's argmax.
+template <bool MASK>
 __global__ void maxpool_bwd_kernel(dc_pool_shape sh, int P, int Q, const float *__restrict__ dy,
-                                   const uint8_t *__restrict__ arg, int acc, float *__restrict__ dx) {
+                                   const uint8_t *__restrict__ arg, int acc, float *__restrict__ dx,
+                                   const float *__restrict__ y) {
     const int64_t total = (int64_t)sh.n * sh.h * sh.w * sh.c;
     for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total; e += (int64_t)gridDim.x * blockDim.x) {
         int c = (int)(e % sh.c);
@@ -191,7 +196,7 @@ __global__ void maxpool_bwd_kernel(dc_pool_shape sh, int P, int Q, const float *
             for (int q = q_lo; q <= q_hi; ++q) {
                 int64_t o = (((int64_t)n * P + p) * Q + q) * sh.c + c;
                 int a = (hp - p * sh.stride) * sh.s + (wp - q * sh.stride);
-                if (arg[o] == a)
+                if (arg[o] == a && (!MASK || y[o] > 0.f))
                     g += dy[o];
             }
         dx[e] = acc ? dx[e] + g : g;
@@ -239,9 +244,10 @@ __global__ void maxpool_fwd4_kernel(dc_pool_shape sh, int P, int Q, int c4, int 
     }
 }
 
+template <bool MASK>
 __global__ void maxpool_bwd4_kernel(dc_pool_shape sh, int P, int Q, int c4, int total4,
                                     const float4 *__restrict__ dy, const uchar4 *__restrict__ arg, int acc,
-                                    float4 *__restrict__ dx) {
+                                    float4 *__restrict__ dx, const float4 *__restrict__ y) {
     for (int e = blockIdx.x * blockDim.x + threadIdx.x; e < total4; e += gridDim.x * blockDim.x) {
         const int q4 = e % c4;
         const int pix = e / c4;
@@ -261,13 +267,14 @@ __global__ void maxpool_bwd4_kernel(dc_pool_shape sh, int P, int Q, int c4, int 
                 const int a = (hp - p * sh.stride) * sh.s + (wp - q * sh.stride);
                 const uchar4 ar = arg[o];
                 const float4 d = dy[o];
-                if (ar.x == a)
+                const float4 ym = MASK ? y[o] : make_float4(1.f, 1.f, 1.f, 1.f);
+                if (ar.x == a && ym.x > 0.f)
                     g.x += d.x;
-                if (ar.y == a)
+                if (ar.y == a && ym.y > 0.f)
                     g.y += d.y;
-                if (ar.z == a)
+                if (ar.z == a && ym.z > 0.f)
                     g.z += d.z;
-                if (ar.w == a)
+                if (ar.w == a && ym.w > 0.f)
                     g.w += d.w;
             }
         if (acc) {
@@ -902,20 +909,30 @@ int maxpool_forward(const dc_pool_shape &sh, const float *x, float *y, uint8_t *
 }
 
 int maxpool_backward(const dc_pool_shape &sh, const float *dy, const uint8_t *arg, int accumulate, float *dx,
-                     hipStream_t s) {
+                     hipStream_t s, const float *relu_y) {
     int P = (sh.h + 2 * sh.pad - sh.r) / sh.stride + 1;
     int Q = (sh.w + 2 * sh.pad - sh.s) / sh.stride + 1;
     int64_t total = (int64_t)sh.n * sh.h * sh.w * sh.c;
     if (total <= 0)
         return DC_OK;
-    if (pool4_ok(sh, P, Q, dy, dx, arg)) {
+    if (pool4_ok(sh, P, Q, dy, dx, arg) && ((uintptr_t)relu_y & 15) == 0) {
         const int total4 = (int)(total / 4);
-        hipLaunchKernelGGL(maxpool_bwd4_kernel, dim3(ew_blocks(total4)), dim3(EW_THREADS), 0, s, sh, P, Q, sh.c / 4,
-                           total4, reinterpret_cast<const float4 *>(dy), reinterpret_cast<const uchar4 *>(arg),
-                           accumulate, reinterpret_cast<float4 *>(dx));
+        const auto *dy4 = reinterpret_cast<const float4 *>(dy);
+        const auto *arg4 = reinterpret_cast<const uchar4 *>(arg);
+        const auto *y4 = reinterpret_cast<const float4 *>(relu_y);
+        auto *dx4 = reinterpret_cast<float4 *>(dx);
+        if (relu_y)
+            hipLaunchKernelGGL(maxpool_bwd4_kernel<true>, dim3(ew_blocks(total4)), dim3(EW_THREADS), 0, s, sh, P, Q,
+                               sh.c / 4, total4, dy4, arg4, accumulate, dx4, y4);
+        else
+            hipLaunchKernelGGL(maxpool_bwd4_kernel<false>, dim3(ew_blocks(total4)), dim3(EW_THREADS), 0, s, sh, P, Q,
+                               sh.c / 4, total4, dy4, arg4, accumulate, dx4, y4);
+    } else if (relu_y) {
+        hipLaunchKernelGGL(maxpool_bwd_kernel<true>, dim3(ew_blocks(total)), dim3(EW_THREADS), 0, s, sh, P, Q, dy, arg,
+                           accumulate, dx, relu_y);
     } else {
-        hipLaunchKernelGGL(maxpool_bwd_kernel, dim3(ew_blocks(total)), dim3(EW_THREADS), 0, s, sh, P, Q, dy, arg,
-                           accumulate, dx);
+        hipLaunchKernelGGL(maxpool_bwd_kernel<false>, dim3(ew_blocks(total)), dim3(EW_THREADS), 0, s, sh, P, Q, dy,
+                           arg, accumulate, dx, relu_y);
     }
     DC_HIP(hipGetLastError());
     return DC_OK;

@@ -197,6 +197,15 @@ static int build_model(dc_model *m, const dc_op_desc *ops, int n_ops) {
         }
     }
 
+    for (int i = 0; i + 1 < n_ops; ++i) {
+        OpInfo &r = m->ops[i], &mp = m->ops[i + 1];
+        if (r.d.kind == DC_OP_RELU && !r.bwd_folded && r.grad_in[0] && mp.d.kind == DC_OP_MAXPOOL &&
+            mp.d.in0 == r.out && consumers[r.out] == 1 && mp.d.layer == r.d.layer) {
+            mp.relu_bwd_from = i;
+            r.bwd_folded = true;
+        }
+    }
+
     // workspace layout
     size_t off = 0;
     auto take = [&](size_t bytes) {
@@ -321,11 +330,18 @@ int run_backward_layer(dc_model *m, int l, const float *x, hipStream_t s) {
         }
         case DC_OP_RELU:
             if (o.bwd_folded)
-                break; // done by the BN that produced its input
+                break; // done by the BN that produced its input, or by the max-pool that reads its output
             DC_TRY(relu_backward(dy, m->act(o.out), o.acc_in[0], dx, ti.size(), s));
             break;
         case DC_OP_MAXPOOL:
-            DC_TRY(maxpool_backward(o.pool, dy, reinterpret_cast<const uint8_t *>(m->ws + o.aux), o.acc_in[0], dx, s));
+            if (o.relu_bwd_from >= 0) { // through the folded ReLU into its input's gradient
+                const OpInfo &r = m->ops[o.relu_bwd_from];
+                DC_TRY(maxpool_backward(o.pool, dy, reinterpret_cast<const uint8_t *>(m->ws + o.aux), r.acc_in[0],
+                                        m->grad(r.d.in0), s, m->act(o.out)));
+            } else {
+                DC_TRY(maxpool_backward(o.pool, dy, reinterpret_cast<const uint8_t *>(m->ws + o.aux), o.acc_in[0], dx,
+                                        s));
+            }
             break;
         case DC_OP_AVGPOOL:
             DC_TRY(avgpool_backward(o.pool, dy, o.acc_in[0], dx, s));

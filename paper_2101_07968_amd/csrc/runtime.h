@@ -46,6 +46,14 @@ struct OpInfo {
     // reads the ReLU's output gradient and masks it with the ReLU's output,
     // and the ReLU's backward (bwd_folded) does nothing.
     bool bwd_folded = false;
+    // Backward ReLU folding into a max-pool: a ReLU (not folded into a BN)
+    // whose only consumer is the next op, a MAXPOOL of the same layer.  The
+    // pool's backward writes the ReLU's input gradient directly, adding a
+    // window's dy only where the window's maximum (the pool's output) is
+    // positive; that maximum is the ReLU's output at the argmax, so this is
+    // exactly the ReLU's mask.  relu_bwd_from is the ReLU's op index, set on
+    // the MAXPOOL; the ReLU gets bwd_folded.
+    int relu_bwd_from = -1;
 };
 
 } // namespace dc
