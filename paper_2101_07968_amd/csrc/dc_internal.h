@@ -76,8 +76,10 @@ void pin_plan(const ConvGeom &g, int pass, int mt, int nt, int splits);
 
 int conv_forward(const ConvGeom &g, const GemmPlan &pl, const float *x, const float *w,
                  const float *bias, int relu, float *y, void *ws, hipStream_t s);
+// relu_mask, if given, is the output of a ReLU whose input gradient dx is:
+// dx (+)= (relu_mask > 0 ? dgrad : 0), laid out like dx.
 int conv_dgrad(const ConvGeom &g, const GemmPlan &pl, const float *dy, const float *w,
-               int accumulate, float *dx, void *ws, hipStream_t s);
+               int accumulate, float *dx, void *ws, hipStream_t s, const float *relu_mask = nullptr);
 int conv_wgrad(const ConvGeom &g, const GemmPlan &pl, const float *x, const float *dy, float *dw,
                void *ws, hipStream_t s);
 

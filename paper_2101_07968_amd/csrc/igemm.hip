@@ -76,6 +76,7 @@ struct Args {
     int relu, accumulate;
     FDiv fC, fS, fK, fQ, fPQ;
     unsigned a_bytes, b_bytes; // sizes of A and B (lean mode: each below 2^31)
+    const float *relu_mask;    // DGRAD, may be null: zero dx where this tensor (laid out like dx) is not > 0
 };
 
 // Per-phase geometry of dgrad (stride residues rh, rw).
@@ -154,6 +155,9 @@ __device__ __forceinline__ float epilogue(const Args &a, int pass, float v, int 
         if (a.relu)
             v = fmaxf(v, 0.0f);
     } else if (pass == PASS_DGRAD) {
+        // a folded ReLU's backward: its output gradient v, kept where its output is positive
+        if (a.relu_mask && !(a.relu_mask[dst - a.out] > 0.0f))
+            v = 0.0f;
         if (a.accumulate)
             v += *dst;
     }
@@ -1167,9 +1171,9 @@ int conv_forward(const ConvGeom &g, const GemmPlan &pl, const float *x, const fl
 }
 
 int conv_dgrad(const ConvGeom &g, const GemmPlan &pl, const float *dy, const float *w,
-               int accumulate, float *dx, void *ws, hipStream_t s) {
+               int accumulate, float *dx, void *ws, hipStream_t s, const float *relu_mask) {
     Args a = make_args(g, pl);
-    a.A = dy; a.B = w; a.out = dx; a.accumulate = accumulate;
+    a.A = dy; a.B = w; a.out = dx; a.accumulate = accumulate; a.relu_mask = relu_mask;
     return run(g, pl, a, ws, s);
 }
 

@@ -205,6 +205,15 @@ static int build_model(dc_model *m, const dc_op_desc *ops, int n_ops) {
             r.bwd_folded = true;
         }
     }
+    for (int i = 0; i + 1 < n_ops; ++i) {
+        OpInfo &r = m->ops[i], &cv = m->ops[i + 1];
+        if (r.d.kind == DC_OP_RELU && !r.bwd_folded && r.grad_in[0] &&
+            (cv.d.kind == DC_OP_CONV || cv.d.kind == DC_OP_FC) && cv.d.in0 == r.out && cv.grad_in[0] &&
+            consumers[r.out] == 1) {
+            cv.dgrad_relu_from = i;
+            r.bwd_folded = true;
+        }
+    }
 
     // workspace layout
     size_t off = 0;
@@ -316,8 +325,13 @@ int run_backward_layer(dc_model *m, int l, const float *x, hipStream_t s) {
             DC_TRY(conv_wgrad(o.geom, o.wgrad, in, dy, G + o.w_off, m->scratch(), s));
             if (o.b_off != NONE)
                 DC_TRY(colsum((int64_t)to.n * to.h * to.w, to.c, dy, G + o.b_off, m->scratch(), s));
-            if (dx)
+            if (o.dgrad_relu_from >= 0) { // through the folded ReLU into its input's gradient
+                const OpInfo &r = m->ops[o.dgrad_relu_from];
+                DC_TRY(conv_dgrad(o.geom, o.dgrad, dy, P + o.w_off, r.acc_in[0], m->grad(r.d.in0), m->scratch(), s,
+                                  m->act(r.out)));
+            } else if (dx) {
                 DC_TRY(conv_dgrad(o.geom, o.dgrad, dy, P + o.w_off, o.acc_in[0], dx, m->scratch(), s));
+            }
             break;
         case DC_OP_BN: {
             const float *mean = reinterpret_cast<const float *>(m->ws + o.aux);
@@ -330,7 +344,7 @@ int run_backward_layer(dc_model *m, int l, const float *x, hipStream_t s) {
         }
         case DC_OP_RELU:
             if (o.bwd_folded)
-                break; // done by the BN that produced its input, or by the max-pool that reads its output
+                break; // done by the BN that produced its input, or by the max-pool / GEMM that reads its output
             DC_TRY(relu_backward(dy, m->act(o.out), o.acc_in[0], dx, ti.size(), s));
             break;
         case DC_OP_MAXPOOL:

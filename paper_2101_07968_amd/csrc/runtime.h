@@ -54,6 +54,11 @@ struct OpInfo {
     // exactly the ReLU's mask.  relu_bwd_from is the ReLU's op index, set on
     // the MAXPOOL; the ReLU gets bwd_folded.
     int relu_bwd_from = -1;
+    // The same for a ReLU whose only consumer is the next op, a CONV / FC
+    // (possibly of the next layer): its data gradient is the ReLU's output
+    // gradient, so the GEMM's epilogue keeps it where the ReLU's output is
+    // positive and writes the ReLU's input gradient.  Set on the CONV / FC.
+    int dgrad_relu_from = -1;
 };
 
 } // namespace dc
