@@ -100,6 +100,9 @@ int relu_backward(const float *dy, const float *y, int accumulate, float *dx, in
                   hipStream_t s);
 int add_forward(const float *a, const float *b, int relu, float *y, int64_t n, hipStream_t s);
 int copy_grad(const float *dy, int accumulate, float *dx, int64_t n, hipStream_t s);
+// Backward of relu(a + b): dx0 (+)= dx1 (+)= (y > 0 ? dy : 0); a null dx is skipped.
+int add_relu_backward(const float *dy, const float *y, int acc0, float *dx0, int acc1, float *dx1, int64_t n,
+                      hipStream_t s);
 int concat_forward(int64_t rows, int c_in, int c_out, int off, const float *x, float *y, hipStream_t s);
 int concat_backward(int64_t rows, int c_in, int c_out, int off, const float *dy, int accumulate, float *dx,
                     hipStream_t s);

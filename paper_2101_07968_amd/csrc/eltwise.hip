@@ -62,6 +62,46 @@ __global__ void relu_bwd_kernel(const float *__restrict__ dy, const float *__res
     }
 }
 
+// Backward of relu(a + b) into both inputs at once: dx0 (+)= m and dx1 (+)=
+// m with m = (y > 0 ? dy : 0), y the ReLU's output.  One read of dy and y
+// replaces a ReLU pass and two copies.  dx0 and dx1 may be the same tensor (a
+// thread updates both in order) or null (no gradient wanted).
+__global__ void add_relu_bwd_kernel(const float *__restrict__ dy, const float *__restrict__ y, int acc0, float *dx0,
+                                    int acc1, float *dx1, int64_t n, int64_t n4) {
+    const float4 *d4 = reinterpret_cast<const float4 *>(dy);
+    const float4 *y4 = reinterpret_cast<const float4 *>(y);
+    float4 *a4 = reinterpret_cast<float4 *>(dx0);
+    float4 *b4 = reinterpret_cast<float4 *>(dx1);
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += (int64_t)gridDim.x * blockDim.x) {
+        const float4 d = d4[i], v = y4[i];
+        float4 g;
+        g.x = relu_grad(d.x, v.x); g.y = relu_grad(d.y, v.y); g.z = relu_grad(d.z, v.z); g.w = relu_grad(d.w, v.w);
+        if (a4) {
+            float4 o = g;
+            if (acc0) {
+                const float4 p = a4[i];
+                o.x += p.x; o.y += p.y; o.z += p.z; o.w += p.w;
+            }
+            a4[i] = o;
+        }
+        if (b4) {
+            float4 o = g;
+            if (acc1) {
+                const float4 p = b4[i];
+                o.x += p.x; o.y += p.y; o.z += p.z; o.w += p.w;
+            }
+            b4[i] = o;
+        }
+    }
+    for (int64_t i = 4 * n4 + (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+        const float g = relu_grad(dy[i], y[i]);
+        if (dx0)
+            dx0[i] = acc0 ? g + dx0[i] : g;
+        if (dx1)
+            dx1[i] = acc1 ? g + dx1[i] : g;
+    }
+}
+
 __global__ void add_fwd_kernel(const float *__restrict__ a, const float *__restrict__ b, int relu,
                                float *__restrict__ y, int64_t n, int64_t n4) {
     const float4 *a4 = reinterpret_cast<const float4 *>(a);
@@ -839,6 +879,17 @@ int add_forward(const float *a, const float *b, int relu, float *y, int64_t n, h
     if (n <= 0)
         return DC_OK;
     hipLaunchKernelGGL(add_fwd_kernel, dim3(ew_blocks(n, 4)), dim3(EW_THREADS), 0, s, a, b, relu, y, n, vec4(n, a, b, y));
+    DC_HIP(hipGetLastError());
+    return DC_OK;
+}
+
+int add_relu_backward(const float *dy, const float *y, int acc0, float *dx0, int acc1, float *dx1, int64_t n,
+                      hipStream_t s) {
+    if (n <= 0)
+        return DC_OK;
+    const int64_t n4 = al16(dx0) && al16(dx1) ? vec4(n, dy, y) : 0;
+    hipLaunchKernelGGL(add_relu_bwd_kernel, dim3(ew_blocks(n, 4)), dim3(EW_THREADS), 0, s, dy, y, acc0, dx0, acc1, dx1,
+                       n, n4);
     DC_HIP(hipGetLastError());
     return DC_OK;
 }

@@ -193,7 +193,7 @@ static int build_model(dc_model *m, const dc_op_desc *ops, int n_ops) {
             nx.d.kind == DC_OP_RELU && nx.d.in0 == o.out && consumers[o.out] == 1 && nx.d.layer == o.d.layer) {
             o.relu_into = nx.out;
             nx.fwd_folded = true;
-            nx.bwd_folded = kd == DC_OP_BN;
+            nx.bwd_folded = kd == DC_OP_BN || kd == DC_OP_ADD;
         }
     }
 
@@ -364,8 +364,13 @@ int run_backward_layer(dc_model *m, int l, const float *x, hipStream_t s) {
             DC_TRY(gap_backward(ti.n, ti.h * ti.w, ti.c, dy, o.acc_in[0], dx, s));
             break;
         case DC_OP_ADD:
-            DC_TRY(copy_grad(dy, o.acc_in[0], dx, ti.size(), s));
-            DC_TRY(copy_grad(dy, o.acc_in[1], m->grad(o.d.in1), ti.size(), s));
+            if (o.relu_into >= 0 && m->ops[i + 1].bwd_folded) { // the folded ReLU's gradient, masked, into both inputs
+                DC_TRY(add_relu_backward(m->grad(o.relu_into), m->act(o.relu_into), o.acc_in[0], dx, o.acc_in[1],
+                                         o.grad_in[1] ? m->grad(o.d.in1) : nullptr, ti.size(), s));
+            } else {
+                DC_TRY(copy_grad(dy, o.acc_in[0], dx, ti.size(), s));
+                DC_TRY(copy_grad(dy, o.acc_in[1], m->grad(o.d.in1), ti.size(), s));
+            }
             break;
         case DC_OP_CONCAT:
             for (int k = 0; k < o.n_in; ++k) {

@@ -42,9 +42,9 @@ struct OpInfo {
     // ReLU's output, the producer's backward reads its inputs).
     int relu_into = -1;
     bool fwd_folded = false;
-    // Backward ReLU folding, for a BN with relu_into set: the BN's backward
-    // reads the ReLU's output gradient and masks it with the ReLU's output,
-    // and the ReLU's backward (bwd_folded) does nothing.
+    // Backward ReLU folding, for a BN or ADD with relu_into set: the
+    // producer's backward reads the ReLU's output gradient and masks it with
+    // the ReLU's output, and the ReLU's backward (bwd_folded) does nothing.
     bool bwd_folded = false;
     // Backward ReLU folding into a max-pool: a ReLU (not folded into a BN)
     // whose only consumer is the next op, a MAXPOOL of the same layer.  The
