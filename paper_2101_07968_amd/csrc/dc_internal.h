@@ -104,8 +104,10 @@ int copy_grad(const float *dy, int accumulate, float *dx, int64_t n, hipStream_t
 int add_relu_backward(const float *dy, const float *y, int acc0, float *dx0, int acc1, float *dx1, int64_t n,
                       hipStream_t s);
 int concat_forward(int64_t rows, int c_in, int c_out, int off, const float *x, float *y, hipStream_t s);
+// relu_y, if given (laid out like dx), masks dy: dx is then the gradient of
+// the input of a ReLU whose output was this concatenation's input.
 int concat_backward(int64_t rows, int c_in, int c_out, int off, const float *dy, int accumulate, float *dx,
-                    hipStream_t s);
+                    hipStream_t s, const float *relu_y = nullptr);
 int avgpool_forward(const dc_pool_shape &sh, const float *x, float *y, hipStream_t s);
 int avgpool_backward(const dc_pool_shape &sh, const float *dy, int accumulate, float *dx, hipStream_t s);
 int maxpool_forward(const dc_pool_shape &sh, const float *x, float *y, uint8_t *arg,

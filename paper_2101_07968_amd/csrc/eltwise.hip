@@ -153,9 +153,12 @@ __global__ void concat_kernel(int64_t rows, int c_in, int c_out, int off, const 
     }
 }
 
+// relu_y (may be null, laid out like dx): dx is the gradient of the input of
+// a ReLU whose output was this concatenation's input; dy is kept where
+// relu_y > 0.
 template <int V>
 __global__ void concat_bwd_kernel(int64_t rows, int c_in, int c_out, int off, const float *__restrict__ dy, int acc,
-                                  float *__restrict__ dx) {
+                                  float *__restrict__ dx, const float *__restrict__ relu_y) {
     const int cv = c_in / V;
     const int64_t total = rows * cv;
     for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total; e += (int64_t)gridDim.x * blockDim.x) {
@@ -163,6 +166,10 @@ __global__ void concat_bwd_kernel(int64_t rows, int c_in, int c_out, int off, co
         int c = (int)(e - m * cv) * V;
         if (V == 4) {
             float4 g = *reinterpret_cast<const float4 *>(dy + m * c_out + off + c);
+            if (relu_y) {
+                const float4 v = *reinterpret_cast<const float4 *>(relu_y + m * c_in + c);
+                g.x = relu_grad(g.x, v.x); g.y = relu_grad(g.y, v.y); g.z = relu_grad(g.z, v.z); g.w = relu_grad(g.w, v.w);
+            }
             float4 *o = reinterpret_cast<float4 *>(dx + m * c_in + c);
             if (acc) {
                 float4 p = *o;
@@ -171,6 +178,8 @@ __global__ void concat_bwd_kernel(int64_t rows, int c_in, int c_out, int off, co
             *o = g;
         } else {
             float g = dy[m * c_out + off + c];
+            if (relu_y)
+                g = relu_grad(g, relu_y[m * c_in + c]);
             dx[m * c_in + c] = acc ? dx[m * c_in + c] + g : g;
         }
     }
@@ -921,15 +930,15 @@ int concat_forward(int64_t rows, int c_in, int c_out, int off, const float *x, f
 }
 
 int concat_backward(int64_t rows, int c_in, int c_out, int off, const float *dy, int accumulate, float *dx,
-                    hipStream_t s) {
+                    hipStream_t s, const float *relu_y) {
     if (rows <= 0 || c_in <= 0)
         return DC_OK;
-    if (concat_vec(c_in, c_out, off, dy, dx))
+    if (concat_vec(c_in, c_out, off, dy, dx) && al16(relu_y))
         hipLaunchKernelGGL(concat_bwd_kernel<4>, dim3(ew_blocks(rows * c_in, 4)), dim3(EW_THREADS), 0, s, rows, c_in,
-                           c_out, off, dy, accumulate, dx);
+                           c_out, off, dy, accumulate, dx, relu_y);
     else
         hipLaunchKernelGGL(concat_bwd_kernel<1>, dim3(ew_blocks(rows * c_in)), dim3(EW_THREADS), 0, s, rows, c_in,
-                           c_out, off, dy, accumulate, dx);
+                           c_out, off, dy, accumulate, dx, relu_y);
     DC_HIP(hipGetLastError());
     return DC_OK;
 }

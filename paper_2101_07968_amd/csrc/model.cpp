@@ -205,13 +205,33 @@ static int build_model(dc_model *m, const dc_op_desc *ops, int n_ops) {
             r.bwd_folded = true;
         }
     }
-    for (int i = 0; i + 1 < n_ops; ++i) {
-        OpInfo &r = m->ops[i], &cv = m->ops[i + 1];
-        if (r.d.kind == DC_OP_RELU && !r.bwd_folded && r.grad_in[0] &&
-            (cv.d.kind == DC_OP_CONV || cv.d.kind == DC_OP_FC) && cv.d.in0 == r.out && cv.grad_in[0] &&
-            consumers[r.out] == 1) {
-            cv.dgrad_relu_from = i;
+    // A ReLU whose only consumer is a CONV / FC or a CONCAT: that op's backward
+    // applies the mask.  The ReLU's input gradient then receives this
+    // contribution at the consumer's turn instead of the ReLU's; that keeps the
+    // order of contributions when the consumer is the next op, or when the
+    // ReLU is the only reader of its input (one contribution in all).
+    std::vector<int> consumer_of(n_ops + 1, -1);
+    for (int j = 0; j < n_ops; ++j)
+        for (int k = 0; k < m->ops[j].n_in; ++k)
+            if (m->ops[j].in[k] >= 0)
+                consumer_of[m->ops[j].in[k]] = j;
+    for (int i = 0; i < n_ops; ++i) {
+        OpInfo &r = m->ops[i];
+        if (r.d.kind != DC_OP_RELU || r.bwd_folded || !r.grad_in[0] || consumers[r.out] != 1)
+            continue;
+        const int j = consumer_of[r.out];
+        if (j < 0 || (j != i + 1 && consumers[r.d.in0] != 1))
+            continue;
+        OpInfo &c = m->ops[j];
+        if ((c.d.kind == DC_OP_CONV || c.d.kind == DC_OP_FC) && c.d.in0 == r.out && c.grad_in[0]) {
+            c.dgrad_relu_from = i;
             r.bwd_folded = true;
+        } else if (c.d.kind == DC_OP_CONCAT) {
+            for (int k = 0; k < c.n_in; ++k)
+                if (c.in[k] == r.out && c.grad_in[k]) {
+                    c.concat_relu_from[k] = i;
+                    r.bwd_folded = true;
+                }
         }
     }
 
@@ -344,7 +364,7 @@ int run_backward_layer(dc_model *m, int l, const float *x, hipStream_t s) {
         }
         case DC_OP_RELU:
             if (o.bwd_folded)
-                break; // done by the BN that produced its input, or by the max-pool / GEMM that reads its output
+                break; // done by the BN / add that produced its input, or by the op that reads its output
             DC_TRY(relu_backward(dy, m->act(o.out), o.acc_in[0], dx, ti.size(), s));
             break;
         case DC_OP_MAXPOOL:
@@ -377,8 +397,14 @@ int run_backward_layer(dc_model *m, int l, const float *x, hipStream_t s) {
                 if (!o.grad_in[k])
                     continue;
                 const TensorInfo &tk = m->tensors[o.in[k]];
-                DC_TRY(concat_backward((int64_t)tk.n * tk.h * tk.w, tk.c, to.c, o.ch_off[k], dy, o.acc_in[k],
-                                       m->grad(o.in[k]), s));
+                if (o.concat_relu_from[k] >= 0) { // through the folded ReLU into its input's gradient
+                    const OpInfo &r = m->ops[o.concat_relu_from[k]];
+                    DC_TRY(concat_backward((int64_t)tk.n * tk.h * tk.w, tk.c, to.c, o.ch_off[k], dy, r.acc_in[0],
+                                           m->grad(r.d.in0), s, m->act(r.out)));
+                } else {
+                    DC_TRY(concat_backward((int64_t)tk.n * tk.h * tk.w, tk.c, to.c, o.ch_off[k], dy, o.acc_in[k],
+                                           m->grad(o.in[k]), s));
+                }
             }
             break;
         }

@@ -59,6 +59,10 @@ struct OpInfo {
     // gradient, so the GEMM's epilogue keeps it where the ReLU's output is
     // positive and writes the ReLU's input gradient.  Set on the CONV / FC.
     int dgrad_relu_from = -1;
+    // The same for a ReLU whose output is input k of a CONCAT (its only
+    // consumer): the concatenation's backward masks that slice of its output
+    // gradient and writes the ReLU's input gradient.
+    int concat_relu_from[4] = {-1, -1, -1, -1};
 };
 
 } // namespace dc
