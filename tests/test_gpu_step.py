@@ -406,6 +406,60 @@ def test_replanning_follows_the_link():
         assert own <= stale, (rate, own, stale)
 
 
+def test_relu_folds_on_odd_graphs():
+    """The ReLU backward folds on graphs the workloads do not contain, against the oracle:
+    * a conv output read by a ReLU -> max-pool and twice by add(t, t) -> ReLU: the masked pool
+      accumulates into a gradient the fused add-ReLU wrote through two aliased outputs;
+    * a ReLU whose only consumer is a concatenation three ops later (non-adjacent fold);
+    * a ReLU -> conv whose input is also read by a residual add: the masked data-gradient
+      epilogue accumulates."""
+    C, R, MP, A, CAT, F = D.DC_OP_CONV, D.DC_OP_RELU, D.DC_OP_MAXPOOL, D.DC_OP_ADD, D.DC_OP_CONCAT, D.DC_OP_FC
+    conv = lambda i, l, k, r, pad: {"op": "conv", "in": i, "layer": l, "k": k, "r": r, "s": r, "stride": 1,
+                                    "pad": pad, "bias": True}
+    relu = lambda i, l: {"op": "relu", "in": i, "layer": l}
+    pool = lambda i, l: {"op": "maxpool", "in": i, "layer": l, "r": 2, "s": 2, "stride": 2, "pad": 0}
+    cases = [
+        ({"name": "folds1", "hwc": (8, 8, 4), "classes": 5, "ops": [
+            conv(0, 1, 8, 3, 1), relu(1, 1), pool(2, 1),
+            {"op": "add", "in": 1, "other": 1, "layer": 1}, relu(4, 1), pool(5, 1),
+            {"op": "concat", "in": 3, "others": [6], "layer": 1},
+            conv(7, 2, 8, 3, 1), relu(8, 2), conv(7, 2, 4, 1, 0), relu(10, 2),
+            {"op": "concat", "in": 9, "others": [11], "layer": 2},
+            {"op": "fc", "in": 12, "layer": 3, "out": 5, "bias": True}]},
+         [(C, 1, 0, -1, 8, 3, 3, 1, 1, 1, -1, -1, 1), (R, 1, 1, -1, 0, 0, 0, 0, 0, 0, -1, -1, 0),
+          (MP, 1, 2, -1, 0, 2, 2, 2, 0, 0, -1, -1, 0), (A, 1, 1, 1, 0, 0, 0, 0, 0, 0, -1, -1, 0),
+          (R, 1, 4, -1, 0, 0, 0, 0, 0, 0, -1, -1, 0), (MP, 1, 5, -1, 0, 2, 2, 2, 0, 0, -1, -1, 0),
+          (CAT, 1, 3, 6, 0, 0, 0, 0, 0, 0, -1, -1, 0),
+          (C, 2, 7, -1, 8, 3, 3, 1, 1, 1, -1, -1, 1), (R, 2, 8, -1, 0, 0, 0, 0, 0, 0, -1, -1, 0),
+          (C, 2, 7, -1, 4, 1, 1, 1, 0, 1, -1, -1, 0), (R, 2, 10, -1, 0, 0, 0, 0, 0, 0, -1, -1, 0),
+          (CAT, 2, 9, 11, 0, 0, 0, 0, 0, 0, -1, -1, 0), (F, 3, 12, -1, 5, 0, 0, 0, 0, 1, -1, -1, 0)]),
+        ({"name": "folds2", "hwc": (6, 6, 4), "classes": 5, "ops": [
+            conv(0, 1, 8, 3, 1), relu(1, 1), conv(2, 2, 8, 3, 1),
+            {"op": "add", "in": 3, "other": 1, "layer": 2}, relu(4, 2),
+            {"op": "fc", "in": 5, "layer": 3, "out": 5, "bias": True}]},
+         [(C, 1, 0, -1, 8, 3, 3, 1, 1, 1, -1, -1, 1), (R, 1, 1, -1, 0, 0, 0, 0, 0, 0, -1, -1, 0),
+          (C, 2, 2, -1, 8, 3, 3, 1, 1, 1, -1, -1, 1), (A, 2, 3, 1, 0, 0, 0, 0, 0, 0, -1, -1, 0),
+          (R, 2, 4, -1, 0, 0, 0, 0, 0, 0, -1, -1, 0), (F, 3, 5, -1, 5, 0, 0, 0, 0, 1, -1, -1, 0)]),
+    ]
+    for spec, ops in cases:
+        for batch in (1, 3):
+            print(f"folds {spec['name']} batch {batch}", flush=True)
+            hwc, classes = spec["hwc"], spec["classes"]
+            specs = PN.param_specs(ops, hwc)
+            onet = OC.Net(spec, batch)
+            assert specs == onet.param_specs
+            x, y, params = synth.cnn_inputs(31 + batch, batch, hwc, classes, specs)
+            model = D.Model(ops, batch, hwc, classes)
+            model.ps_write(params)
+            st = model.step(dev(x), dev(y), plans_for(model.L, seed=batch)["random"], UNPACED)
+            p_new, g = model.ps_read()
+            loss_ref, g_ref, p_ref = onet.step(x, y, params)
+            assert abs(st["loss"] - loss_ref) <= 1e-4 * abs(loss_ref)
+            assert rel_err(g, g_ref) <= 1e-3
+            assert rel_err(p_new, p_ref) <= 1e-3
+            model.close()
+
+
 def test_degenerate_models():
     """L = 1 (one FC layer: no segment decision to make) at batch 1, and a two-layer
     conv net whose conv output is a single pixel, each against the oracle."""
