@@ -97,6 +97,22 @@ typedef struct dc_op_desc {
 typedef struct dc_model dc_model;
 
 /*
+ * One contribution to a tensor's gradient in the backward pass: the chain-rule
+ * term of op `origin_op` for its input `tensor`, performed by the launch of op
+ * `exec_op` (a ReLU's term can be carried out by the op that reads its
+ * output, or by the BN / ADD that produced its input).  accumulate = 1 adds
+ * it to what earlier contributions wrote, 0 writes it.  fused = 1: the term is
+ * formed inside that launch and never stored.
+ */
+typedef struct dc_grad_contrib {
+    int32_t tensor;
+    int32_t origin_op;
+    int32_t exec_op;
+    int32_t accumulate;
+    int32_t fused;
+} dc_grad_contrib;
+
+/*
  * Build a model for `batch` images of in_h x in_w x in_c and `classes`
  * classes.  Allocates the pinned parameter-server buffers (parameters and
  * gradients, zero-filled) and the library's side streams and events on the
@@ -110,6 +126,22 @@ int dc_model_create(const dc_op_desc *ops, int n_ops, int batch, int in_h, int i
  * on the caller's stream), then frees the model.  The caller's workspace and
  * any other work on its stream stay the caller's to synchronise. */
 void dc_model_destroy(dc_model *m);
+
+/*
+ * The backward pass's tensor-gradient contributions for a network, in the
+ * order the launches of dc_step make them (layers L..1, each layer's ops last
+ * to first).  The description is validated as by dc_model_create; no HIP call
+ * is made and no device is needed.  Sec. III-A's backward procedure applies
+ * the chain rule op by op in reverse; a tensor read by several ops receives
+ * their terms in reverse op order, the first written and the rest added, so
+ * each gradient is one fixed sum whatever the segmentation.  This call shows
+ * where a folded ReLU's term is carried out.  Writes up to `cap` entries to
+ * `out` (caller-owned; may be NULL when cap is 0) and the number of entries
+ * into *n_out.  Errors: those of dc_model_create's validation; DC_EINVAL when
+ * cap is smaller than the number of entries (*n_out is still set).
+ */
+int dc_backward_schedule(const dc_op_desc *ops, int n_ops, int batch, int in_h, int in_w, int in_c, int classes,
+                         dc_grad_contrib *out, int cap, int *n_out);
 
 int dc_model_num_layers(const dc_model *m);      /* L */
 size_t dc_model_num_params(const dc_model *m);   /* float32 parameters in total */

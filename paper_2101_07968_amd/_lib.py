@@ -63,6 +63,10 @@ class Batch(ctypes.Structure):
     _fields_ = [("x_dev", c_vp), ("y_dev", c_vp), ("n", c_i32)]
 
 
+class GradContrib(ctypes.Structure):
+    _fields_ = [(n, c_i32) for n in ("tensor", "origin_op", "exec_op", "accumulate", "fused")]
+
+
 class ProfileT(ctypes.Structure):
     _fields_ = [("L", c_i32), ("pt_ns", ctypes.POINTER(c_i64)), ("fc_ns", ctypes.POINTER(c_i64)),
                 ("bc_ns", ctypes.POINTER(c_i64)), ("gt_ns", ctypes.POINTER(c_i64)), ("dt_ns", c_i64)]
@@ -90,6 +94,8 @@ _SIGS = {
     "dc_model_create": (ctypes.c_int, [_P(OpDesc), ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
                                        ctypes.c_int, ctypes.c_int, _P(c_vp)]),
     "dc_model_destroy": (None, [c_vp]),
+    "dc_backward_schedule": (ctypes.c_int, [_P(OpDesc), ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                            ctypes.c_int, ctypes.c_int, _P(GradContrib), ctypes.c_int, _P(c_i32)]),
     "dc_model_num_layers": (ctypes.c_int, [c_vp]),
     "dc_model_num_params": (c_sz, [c_vp]),
     "dc_workspace_bytes": (c_sz, [c_vp]),
@@ -286,6 +292,20 @@ def conv_set_plan(shape, pas, mt, nt=0, splits=0):
     """Pin a pass's plan for this process (mt = 0 unpins, mt = -1 pins the cost model's choice)."""
     sh = ConvShape(*shape)
     call("dc_conv2d_set_plan", ctypes.byref(sh), pas, mt, nt, splits)
+
+
+def backward_schedule(ops, batch, hwc, classes):
+    """dc_backward_schedule: the backward pass's gradient contributions in launch order, as
+    dicts with keys tensor, origin_op, exec_op, accumulate, fused."""
+    arr = (OpDesc * len(ops))(*[OpDesc(*o) for o in ops])
+    n = c_i32()
+    st = lib().dc_backward_schedule(arr, len(ops), batch, hwc[0], hwc[1], hwc[2], classes, None, 0, ctypes.byref(n))
+    if st != DC_OK and n.value == 0:
+        check(st, "dc_backward_schedule")
+    out = (GradContrib * max(n.value, 1))()
+    call("dc_backward_schedule", arr, len(ops), batch, hwc[0], hwc[1], hwc[2], classes, out, n.value,
+         ctypes.byref(n))
+    return [{k: getattr(out[i], k) for k, _ in GradContrib._fields_} for i in range(n.value)]
 
 
 def link(bytes_per_s=1e9, dt_emul_ns=0, paced=True):

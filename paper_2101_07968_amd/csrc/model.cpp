@@ -37,6 +37,13 @@ int check_desc(const dc_op_desc *ops, int n_ops, int batch, int in_h, int in_w, 
             if (d.in2 < -1 || d.in2 > i || d.in3 < -1 || d.in3 > i || (d.in2 < 0 && d.in3 >= 0))
                 return fail(DC_EINVAL, "op %d: concat inputs in2 / in3 must be earlier tensors or -1", i);
         }
+        // The input batch (tensor 0) has no activation or gradient buffer of
+        // its own: only a CONV / FC reads it, and its backward skips dgrad.
+        const bool weighted_op = d.kind == DC_OP_CONV || d.kind == DC_OP_FC;
+        const bool multi = d.kind == DC_OP_ADD || d.kind == DC_OP_CONCAT;
+        if ((!weighted_op && d.in0 == 0) || (multi && d.in1 == 0) ||
+            (d.kind == DC_OP_CONCAT && (d.in2 == 0 || d.in3 == 0)))
+            return fail(DC_EINVAL, "op %d: only a CONV or FC may read the input batch (tensor 0)", i);
         if (d.layer != prev_layer && d.layer != prev_layer + 1)
             return fail(DC_EINVAL, "op %d: layers must be contiguous and non-decreasing", i);
         bool weighted = d.kind == DC_OP_CONV || d.kind == DC_OP_FC;
@@ -227,6 +234,14 @@ static int build_model(dc_model *m, const dc_op_desc *ops, int n_ops) {
             c.dgrad_relu_from = i;
             r.bwd_folded = true;
         } else if (c.d.kind == DC_OP_CONCAT) {
+            // The concatenation hands its slices back in slot order, so a slot
+            // that reads the ReLU's input directly would receive its term on
+            // the wrong side of the ReLU's: no fold then.
+            bool direct = false;
+            for (int k = 0; k < c.n_in; ++k)
+                direct |= c.in[k] == r.d.in0;
+            if (direct)
+                continue;
             for (int k = 0; k < c.n_in; ++k)
                 if (c.in[k] == r.out && c.grad_in[k]) {
                     c.concat_relu_from[k] = i;
@@ -329,11 +344,18 @@ int run_forward_layer(dc_model *m, int l, const float *x, const int32_t *y, hipS
     return DC_OK;
 }
 
-int run_backward_layer(dc_model *m, int l, const float *x, hipStream_t s) {
+int run_backward_layer(dc_model *m, int l, const float *x, hipStream_t s, BwdRecorder *rec) {
     const float *P = m->dparams();
     float *G = m->dgrads();
     for (int i = m->layer_last[l]; i >= m->layer_first[l]; --i) {
         OpInfo &o = m->ops[i];
+        // With rec set, each launch below is replaced by the records of the
+        // tensor-gradient contributions it makes, in the order it makes them:
+        // (tensor, op whose chain-rule term it is, accumulate, fused).
+        auto note = [&](int t, int origin, int acc, int fused) {
+            if (rec)
+                rec->v.push_back(dc_grad_contrib{t, origin, i, acc, fused});
+        };
         const float *in = o.d.in0 == 0 ? x : m->act(o.d.in0);
         const float *dy = m->grad(o.out);
         float *dx = o.grad_in[0] ? m->grad(o.d.in0) : nullptr;
@@ -342,54 +364,85 @@ int run_backward_layer(dc_model *m, int l, const float *x, hipStream_t s) {
         switch (o.d.kind) {
         case DC_OP_CONV:
         case DC_OP_FC:
-            DC_TRY(conv_wgrad(o.geom, o.wgrad, in, dy, G + o.w_off, m->scratch(), s));
-            if (o.b_off != NONE)
-                DC_TRY(colsum((int64_t)to.n * to.h * to.w, to.c, dy, G + o.b_off, m->scratch(), s));
+            if (!rec) {
+                DC_TRY(conv_wgrad(o.geom, o.wgrad, in, dy, G + o.w_off, m->scratch(), s));
+                if (o.b_off != NONE)
+                    DC_TRY(colsum((int64_t)to.n * to.h * to.w, to.c, dy, G + o.b_off, m->scratch(), s));
+            }
             if (o.dgrad_relu_from >= 0) { // through the folded ReLU into its input's gradient
                 const OpInfo &r = m->ops[o.dgrad_relu_from];
-                DC_TRY(conv_dgrad(o.geom, o.dgrad, dy, P + o.w_off, r.acc_in[0], m->grad(r.d.in0), m->scratch(), s,
-                                  m->act(r.out)));
+                note(r.out, i, o.acc_in[0], 1);
+                note(r.d.in0, o.dgrad_relu_from, r.acc_in[0], 0);
+                if (!rec)
+                    DC_TRY(conv_dgrad(o.geom, o.dgrad, dy, P + o.w_off, r.acc_in[0], m->grad(r.d.in0), m->scratch(),
+                                      s, m->act(r.out)));
             } else if (dx) {
-                DC_TRY(conv_dgrad(o.geom, o.dgrad, dy, P + o.w_off, o.acc_in[0], dx, m->scratch(), s));
+                note(o.d.in0, i, o.acc_in[0], 0);
+                if (!rec)
+                    DC_TRY(conv_dgrad(o.geom, o.dgrad, dy, P + o.w_off, o.acc_in[0], dx, m->scratch(), s));
             }
             break;
         case DC_OP_BN: {
             const float *mean = reinterpret_cast<const float *>(m->ws + o.aux);
             // a folded ReLU: take its output gradient and mask it on the way in
             const bool fold = o.relu_into >= 0 && m->ops[i + 1].bwd_folded;
-            DC_TRY(bn_backward((int64_t)ti.n * ti.h * ti.w, ti.c, fold ? m->grad(o.relu_into) : dy, in, P + o.w_off,
-                               mean, mean + ti.c, o.acc_in[0], dx, G + o.w_off, G + o.b_off, m->scratch(), s,
-                               fold ? m->act(o.relu_into) : nullptr));
+            if (fold)
+                note(o.out, i + 1, m->ops[i + 1].acc_in[0], 1);
+            note(o.d.in0, i, o.acc_in[0], 0);
+            if (!rec)
+                DC_TRY(bn_backward((int64_t)ti.n * ti.h * ti.w, ti.c, fold ? m->grad(o.relu_into) : dy, in,
+                                   P + o.w_off, mean, mean + ti.c, o.acc_in[0], dx, G + o.w_off, G + o.b_off,
+                                   m->scratch(), s, fold ? m->act(o.relu_into) : nullptr));
             break;
         }
         case DC_OP_RELU:
             if (o.bwd_folded)
                 break; // done by the BN / add that produced its input, or by the op that reads its output
-            DC_TRY(relu_backward(dy, m->act(o.out), o.acc_in[0], dx, ti.size(), s));
+            note(o.d.in0, i, o.acc_in[0], 0);
+            if (!rec)
+                DC_TRY(relu_backward(dy, m->act(o.out), o.acc_in[0], dx, ti.size(), s));
             break;
         case DC_OP_MAXPOOL:
             if (o.relu_bwd_from >= 0) { // through the folded ReLU into its input's gradient
                 const OpInfo &r = m->ops[o.relu_bwd_from];
-                DC_TRY(maxpool_backward(o.pool, dy, reinterpret_cast<const uint8_t *>(m->ws + o.aux), r.acc_in[0],
-                                        m->grad(r.d.in0), s, m->act(o.out)));
+                note(r.out, i, o.acc_in[0], 1);
+                note(r.d.in0, o.relu_bwd_from, r.acc_in[0], 0);
+                if (!rec)
+                    DC_TRY(maxpool_backward(o.pool, dy, reinterpret_cast<const uint8_t *>(m->ws + o.aux),
+                                            r.acc_in[0], m->grad(r.d.in0), s, m->act(o.out)));
             } else {
-                DC_TRY(maxpool_backward(o.pool, dy, reinterpret_cast<const uint8_t *>(m->ws + o.aux), o.acc_in[0], dx,
-                                        s));
+                note(o.d.in0, i, o.acc_in[0], 0);
+                if (!rec)
+                    DC_TRY(maxpool_backward(o.pool, dy, reinterpret_cast<const uint8_t *>(m->ws + o.aux),
+                                            o.acc_in[0], dx, s));
             }
             break;
         case DC_OP_AVGPOOL:
-            DC_TRY(avgpool_backward(o.pool, dy, o.acc_in[0], dx, s));
+            note(o.d.in0, i, o.acc_in[0], 0);
+            if (!rec)
+                DC_TRY(avgpool_backward(o.pool, dy, o.acc_in[0], dx, s));
             break;
         case DC_OP_GAP:
-            DC_TRY(gap_backward(ti.n, ti.h * ti.w, ti.c, dy, o.acc_in[0], dx, s));
+            note(o.d.in0, i, o.acc_in[0], 0);
+            if (!rec)
+                DC_TRY(gap_backward(ti.n, ti.h * ti.w, ti.c, dy, o.acc_in[0], dx, s));
             break;
         case DC_OP_ADD:
             if (o.relu_into >= 0 && m->ops[i + 1].bwd_folded) { // the folded ReLU's gradient, masked, into both inputs
-                DC_TRY(add_relu_backward(m->grad(o.relu_into), m->act(o.relu_into), o.acc_in[0], dx, o.acc_in[1],
-                                         o.grad_in[1] ? m->grad(o.d.in1) : nullptr, ti.size(), s));
+                note(o.out, i + 1, m->ops[i + 1].acc_in[0], 1);
+                note(o.d.in0, i, o.acc_in[0], 0);
+                if (o.grad_in[1])
+                    note(o.d.in1, i, o.acc_in[1], 0);
+                if (!rec)
+                    DC_TRY(add_relu_backward(m->grad(o.relu_into), m->act(o.relu_into), o.acc_in[0], dx,
+                                             o.acc_in[1], o.grad_in[1] ? m->grad(o.d.in1) : nullptr, ti.size(), s));
             } else {
-                DC_TRY(copy_grad(dy, o.acc_in[0], dx, ti.size(), s));
-                DC_TRY(copy_grad(dy, o.acc_in[1], m->grad(o.d.in1), ti.size(), s));
+                note(o.d.in0, i, o.acc_in[0], 0);
+                note(o.d.in1, i, o.acc_in[1], 0);
+                if (!rec) {
+                    DC_TRY(copy_grad(dy, o.acc_in[0], dx, ti.size(), s));
+                    DC_TRY(copy_grad(dy, o.acc_in[1], m->grad(o.d.in1), ti.size(), s));
+                }
             }
             break;
         case DC_OP_CONCAT:
@@ -399,11 +452,16 @@ int run_backward_layer(dc_model *m, int l, const float *x, hipStream_t s) {
                 const TensorInfo &tk = m->tensors[o.in[k]];
                 if (o.concat_relu_from[k] >= 0) { // through the folded ReLU into its input's gradient
                     const OpInfo &r = m->ops[o.concat_relu_from[k]];
-                    DC_TRY(concat_backward((int64_t)tk.n * tk.h * tk.w, tk.c, to.c, o.ch_off[k], dy, r.acc_in[0],
-                                           m->grad(r.d.in0), s, m->act(r.out)));
+                    note(r.out, i, o.acc_in[k], 1);
+                    note(r.d.in0, o.concat_relu_from[k], r.acc_in[0], 0);
+                    if (!rec)
+                        DC_TRY(concat_backward((int64_t)tk.n * tk.h * tk.w, tk.c, to.c, o.ch_off[k], dy, r.acc_in[0],
+                                               m->grad(r.d.in0), s, m->act(r.out)));
                 } else {
-                    DC_TRY(concat_backward((int64_t)tk.n * tk.h * tk.w, tk.c, to.c, o.ch_off[k], dy, o.acc_in[k],
-                                           m->grad(o.in[k]), s));
+                    note(o.in[k], i, o.acc_in[k], 0);
+                    if (!rec)
+                        DC_TRY(concat_backward((int64_t)tk.n * tk.h * tk.w, tk.c, to.c, o.ch_off[k], dy,
+                                               o.acc_in[k], m->grad(o.in[k]), s));
                 }
             }
             break;
@@ -600,6 +658,30 @@ extern "C" void dc_model_destroy(dc_model *m) {
         (void)hipHostFree(m->probe_host);
     delete m->pool;
     delete m;
+}
+
+extern "C" int dc_backward_schedule(const dc_op_desc *ops, int n_ops, int batch, int in_h, int in_w, int in_c,
+                                    int classes, dc_grad_contrib *out, int cap, int *n_out) {
+    clear_error();
+    if (!n_out || cap < 0 || (cap > 0 && !out))
+        return fail(DC_EINVAL, "n_out is NULL, or out is NULL with cap > 0");
+    *n_out = 0;
+    DC_TRY(check_desc(ops, n_ops, batch, in_h, in_w, in_c, classes));
+    dc_model m;
+    m.batch = batch;
+    m.in_h = in_h;
+    m.in_w = in_w;
+    m.in_c = in_c;
+    m.classes = classes;
+    DC_TRY(build_model(&m, ops, n_ops));
+    BwdRecorder rec;
+    for (int l = m.L; l >= 1; --l)
+        DC_TRY(run_backward_layer(&m, l, nullptr, nullptr, &rec));
+    *n_out = (int)rec.v.size();
+    if ((size_t)cap < rec.v.size())
+        return fail(DC_EINVAL, "the schedule has %zu entries, cap is %d", rec.v.size(), cap);
+    std::copy(rec.v.begin(), rec.v.end(), out);
+    return DC_OK;
 }
 
 extern "C" int dc_model_num_layers(const dc_model *m) { return m ? m->L : 0; }

@@ -129,11 +129,18 @@ struct dc_model {
 };
 
 namespace dc {
+// The tensor-gradient contributions of the backward pass in launch order
+// (dc_backward_schedule).
+struct BwdRecorder {
+    std::vector<dc_grad_contrib> v;
+};
 // Enqueue the forward mini-procedures of layer l (and the loss after layer L)
 // on stream s; x is the input batch, y its labels.
 int run_forward_layer(dc_model *m, int l, const float *x, const int32_t *y, hipStream_t s);
-// Enqueue the backward mini-procedures of layer l (x: the input batch).
-int run_backward_layer(dc_model *m, int l, const float *x, hipStream_t s);
+// Enqueue the backward mini-procedures of layer l (x: the input batch).  With
+// rec set, nothing is launched: the contributions the launches would make are
+// appended to rec instead.
+int run_backward_layer(dc_model *m, int l, const float *x, hipStream_t s, BwdRecorder *rec = nullptr);
 // The same work through the layer's HIP graph when DC_OPT_GRAPHS is on (the
 // graphs are captured at the first call for a workspace and batch).
 int launch_forward_layer(dc_model *m, int l, const float *x, const int32_t *y, hipStream_t s);

@@ -141,9 +141,18 @@ def test_model_validation_rejects_bad_descriptions():
     # an output nobody reads
     assert _create([conv, (D.DC_OP_RELU, 1, 1, -1, 0, 0, 0, 0, 0, 0),
                     (D.DC_OP_FC, 2, 1, -1, 10, 0, 0, 0, 0, 1)])[0] == D.DC_EINVAL
-    # ADD of different shapes
-    assert _create([conv, (D.DC_OP_ADD, 1, 1, 0, 0, 0, 0, 0, 0, 0)])[0] == D.DC_EINVAL
+    # ADD of different shapes (4 and 6 channels)
+    conv6 = (D.DC_OP_CONV, 1, 1, -1, 6, 3, 3, 1, 1, 1)
+    assert _create([conv, conv6, (D.DC_OP_ADD, 1, 2, 1, 0, 0, 0, 0, 0, 0)])[0] == D.DC_EINVAL
     assert b"ADD" in D.lib().dc_last_error()
+    # only a CONV / FC reads the input batch, which has no gradient buffer:
+    # a conv followed by add(conv output, input batch), and a ReLU of the batch
+    assert _create([(D.DC_OP_CONV, 1, 0, -1, 3, 3, 3, 1, 1, 1), (D.DC_OP_ADD, 1, 1, 0, 0, 0, 0, 0, 0, 0),
+                    (D.DC_OP_FC, 2, 2, -1, 10, 0, 0, 0, 0, 1)])[0] == D.DC_EINVAL
+    assert b"input batch" in D.lib().dc_last_error()
+    assert _create([conv, (D.DC_OP_RELU, 1, 0, -1, 0, 0, 0, 0, 0, 0), (D.DC_OP_FC, 2, 2, -1, 10, 0, 0, 0, 0, 1)])[0] \
+        == D.DC_EINVAL
+    assert b"input batch" in D.lib().dc_last_error()
     # column padding as large as the filter's width (1 x 3 filter padded by 3 columns)
     wide = (D.DC_OP_CONV, 1, 0, -1, 4, 1, 3, 1, 0, 1, -1, -1, 3)
     assert _create([wide, (D.DC_OP_FC, 2, 1, -1, 10, 0, 0, 0, 0, 1)])[0] == D.DC_EINVAL

@@ -412,7 +412,9 @@ def test_relu_folds_on_odd_graphs():
       accumulates into a gradient the fused add-ReLU wrote through two aliased outputs;
     * a ReLU whose only consumer is a concatenation three ops later (non-adjacent fold);
     * a ReLU -> conv whose input is also read by a residual add: the masked data-gradient
-      epilogue accumulates."""
+      epilogue accumulates;
+    * concat(relu(t), t) and concat(t, relu(t)): a concatenation that reads a ReLU's input
+      as well as its output (the ReLU's backward is then not folded into it)."""
     C, R, MP, A, CAT, F = D.DC_OP_CONV, D.DC_OP_RELU, D.DC_OP_MAXPOOL, D.DC_OP_ADD, D.DC_OP_CONCAT, D.DC_OP_FC
     conv = lambda i, l, k, r, pad: {"op": "conv", "in": i, "layer": l, "k": k, "r": r, "s": r, "stride": 1,
                                     "pad": pad, "bias": True}
@@ -440,6 +442,14 @@ def test_relu_folds_on_odd_graphs():
          [(C, 1, 0, -1, 8, 3, 3, 1, 1, 1, -1, -1, 1), (R, 1, 1, -1, 0, 0, 0, 0, 0, 0, -1, -1, 0),
           (C, 2, 2, -1, 8, 3, 3, 1, 1, 1, -1, -1, 1), (A, 2, 3, 1, 0, 0, 0, 0, 0, 0, -1, -1, 0),
           (R, 2, 4, -1, 0, 0, 0, 0, 0, 0, -1, -1, 0), (F, 3, 5, -1, 5, 0, 0, 0, 0, 1, -1, -1, 0)]),
+        ({"name": "folds3", "hwc": (6, 6, 4), "classes": 5, "ops": [
+            conv(0, 1, 8, 3, 1), relu(1, 1), {"op": "concat", "in": 2, "others": [1], "layer": 1},
+            conv(3, 2, 8, 3, 1), relu(4, 2), {"op": "concat", "in": 4, "others": [5], "layer": 2},
+            {"op": "fc", "in": 6, "layer": 3, "out": 5, "bias": True}]},
+         [(C, 1, 0, -1, 8, 3, 3, 1, 1, 1, -1, -1, 1), (R, 1, 1, -1, 0, 0, 0, 0, 0, 0, -1, -1, 0),
+          (CAT, 1, 2, 1, 0, 0, 0, 0, 0, 0, -1, -1, 0),
+          (C, 2, 3, -1, 8, 3, 3, 1, 1, 1, -1, -1, 1), (R, 2, 4, -1, 0, 0, 0, 0, 0, 0, -1, -1, 0),
+          (CAT, 2, 4, 5, 0, 0, 0, 0, 0, 0, -1, -1, 0), (F, 3, 6, -1, 5, 0, 0, 0, 0, 1, -1, -1, 0)]),
     ]
     for spec, ops in cases:
         for batch in (1, 3):
