@@ -42,6 +42,15 @@ int dc_conv2d_forward(const dc_conv_shape *sh, const float *x, const float *w, c
 int dc_conv2d_backward_data(const dc_conv_shape *sh, const float *dy, const float *w,
                             int accumulate, float *dx, void *ws, size_t ws_bytes, void *stream);
 
+/* The data gradient through a ReLU that feeds this convolution (its output
+ * relu_y is the conv's input x): dx (+)= (relu_y > 0 ? the data gradient
+ * above : 0), the ReLU's input gradient in one pass (chain rule of
+ * Sec. III-A's backward procedure through both ops).  relu_y is laid out like
+ * dx.  This is the launch a model makes when a ReLU's only reader is a conv or
+ * FC. */
+int dc_conv2d_backward_data_relu(const dc_conv_shape *sh, const float *dy, const float *w, const float *relu_y,
+                                 int accumulate, float *dx, void *ws, size_t ws_bytes, void *stream);
+
 /* dw[k,r,s,c] = sum over n, p, q of dy[n,p,q,k] * x[n, p*stride+r-pad, q*stride+s-pad_w, c];
  * dbias[k] = sum over n, p, q of dy[n,p,q,k] if dbias != NULL.  Deterministic
  * (fixed-order split-K). */
@@ -90,6 +99,14 @@ int dc_maxpool_forward(const dc_pool_shape *sh, const float *x, float *y, uint8_
 int dc_maxpool_backward(const dc_pool_shape *sh, const float *dy, const uint8_t *arg,
                         int accumulate, float *dx, void *stream);
 
+/* The same through a ReLU that feeds the pool (x = relu(u)): du (+)= the sum
+ * of dy over the windows whose argmax is this element, where that window's
+ * maximum y (this pool's output) is positive.  The maximum is the ReLU's
+ * output at the argmax, so this is the ReLU's mask.  The launch a model makes
+ * when a ReLU's only reader is the max-pool after it. */
+int dc_maxpool_backward_relu(const dc_pool_shape *sh, const float *dy, const uint8_t *arg, const float *y,
+                             int accumulate, float *dx, void *stream);
+
 /* Average pooling: y = the mean of x over the window positions that lie
  * inside the input (padded positions are not counted).  Backward: dx (+)=
  * the sum, over the windows containing each element, of dy / that window's
@@ -107,6 +124,13 @@ int dc_add_forward(const float *a, const float *b, int relu, float *y, int64_t n
 /* dx (+)= dy over n floats. */
 int dc_copy_grad(const float *dy, int accumulate, float *dx, int64_t n, void *stream);
 
+/* Backward of relu(a + b) over n floats: with m = (y > 0 ? dy : 0), y the
+ * ReLU's output and dy its gradient, dx0 (+)= m and dx1 (+)= m (acc0 / acc1
+ * choose add or write for each); either dx may be NULL (skipped).  The launch
+ * a model makes for a residual add followed by a ReLU. */
+int dc_add_relu_backward(const float *dy, const float *y, int acc0, float *dx0, int acc1, float *dx1, int64_t n,
+                         void *stream);
+
 /* Channel concatenation of NHWC tensors viewed as [rows][channels]:
  * forward y[m][off + c] = x[m][c] for c < c_in, y having c_out channels;
  * backward dx[m][c] (+)= dy[m][off + c]. */
@@ -114,6 +138,13 @@ int dc_concat_forward(int64_t rows, int32_t c_in, int32_t c_out, int32_t off, co
                       void *stream);
 int dc_concat_backward(int64_t rows, int32_t c_in, int32_t c_out, int32_t off, const float *dy,
                        int accumulate, float *dx, void *stream);
+
+/* The concatenation's backward into the input of a ReLU whose output is this
+ * input (relu_y, laid out like dx): dx[m][c] (+)= (relu_y[m][c] > 0 ?
+ * dy[m][off + c] : 0).  The launch a model makes when a ReLU's only reader is
+ * a concatenation. */
+int dc_concat_backward_relu(int64_t rows, int32_t c_in, int32_t c_out, int32_t off, const float *dy,
+                            const float *relu_y, int accumulate, float *dx, void *stream);
 
 /* BatchNorm over rows = n*h*w rows of c channels (NHWC viewed as [rows][c]). */
 size_t dc_batchnorm_workspace_bytes(int64_t rows, int32_t c);
@@ -128,6 +159,14 @@ int dc_batchnorm_backward(int64_t rows, int32_t c, const float *dy, const float 
                           const float *gamma, const float *mean, const float *invstd,
                           int accumulate, float *dx, float *dgamma, float *dbeta, void *ws,
                           size_t ws_bytes, void *stream);
+
+/* BatchNorm backward through the ReLU applied to its output: dy is the
+ * ReLU's output gradient and relu_y = relu(y) the ReLU's output; the
+ * backward above runs on (relu_y > 0 ? dy : 0).  The launch a model makes for
+ * a BatchNorm followed by a ReLU.  dx may be NULL (no data gradient). */
+int dc_batchnorm_backward_relu(int64_t rows, int32_t c, const float *dy, const float *relu_y, const float *x,
+                               const float *gamma, const float *mean, const float *invstd, int accumulate,
+                               float *dx, float *dgamma, float *dbeta, void *ws, size_t ws_bytes, void *stream);
 
 /* loss[0] = mean over n of (logsumexp(z_i) - z_i[y_i]); dz = (softmax(z) - onehot(y)) / n.
  * logits n x classes.  Labels are not range-checked: a label outside

@@ -119,24 +119,31 @@ _SIGS = {
     "dc_conv2d_set_plan": (ctypes.c_int, [_P(ConvShape), ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int]),
     "dc_conv2d_forward": (ctypes.c_int, [_P(ConvShape), c_vp, c_vp, c_vp, ctypes.c_int, c_vp, c_vp, c_sz, c_vp]),
     "dc_conv2d_backward_data": (ctypes.c_int, [_P(ConvShape), c_vp, c_vp, ctypes.c_int, c_vp, c_vp, c_sz, c_vp]),
+    "dc_conv2d_backward_data_relu": (ctypes.c_int, [_P(ConvShape), c_vp, c_vp, c_vp, ctypes.c_int, c_vp, c_vp,
+                                                    c_sz, c_vp]),
     "dc_conv2d_backward_filter": (ctypes.c_int, [_P(ConvShape), c_vp, c_vp, c_vp, c_vp, c_vp, c_sz, c_vp]),
     "dc_relu_forward": (ctypes.c_int, [c_vp, c_vp, c_i64, c_vp]),
     "dc_relu_backward": (ctypes.c_int, [c_vp, c_vp, ctypes.c_int, c_vp, c_i64, c_vp]),
     "dc_maxpool_forward": (ctypes.c_int, [_P(PoolShape), c_vp, c_vp, c_vp, c_vp]),
     "dc_maxpool_backward": (ctypes.c_int, [_P(PoolShape), c_vp, c_vp, ctypes.c_int, c_vp, c_vp]),
+    "dc_maxpool_backward_relu": (ctypes.c_int, [_P(PoolShape), c_vp, c_vp, c_vp, ctypes.c_int, c_vp, c_vp]),
     "dc_avgpool_forward": (ctypes.c_int, [_P(PoolShape), c_vp, c_vp, c_vp]),
     "dc_avgpool_backward": (ctypes.c_int, [_P(PoolShape), c_vp, ctypes.c_int, c_vp, c_vp]),
     "dc_gap_forward": (ctypes.c_int, [c_i32, c_i32, c_i32, c_vp, c_vp, c_vp]),
     "dc_gap_backward": (ctypes.c_int, [c_i32, c_i32, c_i32, c_vp, ctypes.c_int, c_vp, c_vp]),
     "dc_add_forward": (ctypes.c_int, [c_vp, c_vp, ctypes.c_int, c_vp, c_i64, c_vp]),
     "dc_copy_grad": (ctypes.c_int, [c_vp, ctypes.c_int, c_vp, c_i64, c_vp]),
+    "dc_add_relu_backward": (ctypes.c_int, [c_vp, c_vp, ctypes.c_int, c_vp, ctypes.c_int, c_vp, c_i64, c_vp]),
     "dc_concat_forward": (ctypes.c_int, [c_i64, c_i32, c_i32, c_i32, c_vp, c_vp, c_vp]),
     "dc_concat_backward": (ctypes.c_int, [c_i64, c_i32, c_i32, c_i32, c_vp, ctypes.c_int, c_vp, c_vp]),
+    "dc_concat_backward_relu": (ctypes.c_int, [c_i64, c_i32, c_i32, c_i32, c_vp, c_vp, ctypes.c_int, c_vp, c_vp]),
     "dc_batchnorm_workspace_bytes": (c_sz, [c_i64, c_i32]),
     "dc_batchnorm_forward": (ctypes.c_int, [c_i64, c_i32, c_vp, c_vp, c_vp, c_f32, c_vp, c_vp, c_vp, c_vp, c_sz,
                                             c_vp]),
     "dc_batchnorm_backward": (ctypes.c_int, [c_i64, c_i32, c_vp, c_vp, c_vp, c_vp, c_vp, ctypes.c_int, c_vp, c_vp,
                                              c_vp, c_vp, c_sz, c_vp]),
+    "dc_batchnorm_backward_relu": (ctypes.c_int, [c_i64, c_i32, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, ctypes.c_int,
+                                                  c_vp, c_vp, c_vp, c_vp, c_sz, c_vp]),
     "dc_softmax_xent_workspace_bytes": (c_sz, [c_i32]),
     "dc_softmax_xent": (ctypes.c_int, [c_i32, c_i32, c_vp, c_vp, c_vp, c_vp, c_vp, c_sz, c_vp]),
 }

@@ -213,6 +213,21 @@ extern "C" int dc_conv2d_backward_data(const dc_conv_shape *sh, const float *dy,
     return conv_dgrad(g, pl, dy, w, accumulate, dx, ws, static_cast<hipStream_t>(stream));
 }
 
+extern "C" int dc_conv2d_backward_data_relu(const dc_conv_shape *sh, const float *dy, const float *w,
+                                            const float *relu_y, int accumulate, float *dx, void *ws, size_t ws_bytes,
+                                            void *stream) {
+    clear_error();
+    ConvGeom g;
+    DC_TRY(conv_setup(sh, &g));
+    if (g.N == 0)
+        return DC_OK;
+    if (!dy || !w || !relu_y || !dx)
+        return fail(DC_EINVAL, "NULL tensor");
+    GemmPlan pl = plan_gemm(g, PASS_DGRAD);
+    DC_TRY(need_ws(pl.ws_bytes, ws, ws_bytes));
+    return conv_dgrad(g, pl, dy, w, accumulate, dx, ws, static_cast<hipStream_t>(stream), relu_y);
+}
+
 extern "C" int dc_conv2d_backward_filter(const dc_conv_shape *sh, const float *x, const float *dy, float *dw,
                                          float *dbias, void *ws, size_t ws_bytes, void *stream) {
     clear_error();
@@ -275,6 +290,15 @@ extern "C" int dc_maxpool_backward(const dc_pool_shape *sh, const float *dy, con
     return maxpool_backward(*sh, dy, arg, accumulate, dx, static_cast<hipStream_t>(stream));
 }
 
+extern "C" int dc_maxpool_backward_relu(const dc_pool_shape *sh, const float *dy, const uint8_t *arg,
+                                        const float *y, int accumulate, float *dx, void *stream) {
+    clear_error();
+    DC_TRY(pool_check(sh));
+    if (sh->n > 0 && (!dy || !arg || !y || !dx))
+        return fail(DC_EINVAL, "NULL tensor");
+    return maxpool_backward(*sh, dy, arg, accumulate, dx, static_cast<hipStream_t>(stream), y);
+}
+
 extern "C" int dc_avgpool_forward(const dc_pool_shape *sh, const float *x, float *y, void *stream) {
     clear_error();
     DC_TRY(pool_check(sh));
@@ -321,6 +345,14 @@ extern "C" int dc_copy_grad(const float *dy, int accumulate, float *dx, int64_t 
     return copy_grad(dy, accumulate, dx, n, static_cast<hipStream_t>(stream));
 }
 
+extern "C" int dc_add_relu_backward(const float *dy, const float *y, int acc0, float *dx0, int acc1, float *dx1,
+                                    int64_t n, void *stream) {
+    clear_error();
+    if (n < 0 || (n > 0 && (!dy || !y || (!dx0 && !dx1))))
+        return fail(DC_EINVAL, "bad add arguments");
+    return add_relu_backward(dy, y, acc0, dx0, acc1, dx1, n, static_cast<hipStream_t>(stream));
+}
+
 extern "C" int dc_concat_forward(int64_t rows, int32_t c_in, int32_t c_out, int32_t off, const float *x, float *y,
                                  void *stream) {
     clear_error();
@@ -335,6 +367,14 @@ extern "C" int dc_concat_backward(int64_t rows, int32_t c_in, int32_t c_out, int
     if (rows < 0 || c_in < 1 || off < 0 || off + c_in > c_out || (rows > 0 && (!dy || !dx)))
         return fail(DC_EINVAL, "bad concat arguments");
     return concat_backward(rows, c_in, c_out, off, dy, accumulate, dx, static_cast<hipStream_t>(stream));
+}
+
+extern "C" int dc_concat_backward_relu(int64_t rows, int32_t c_in, int32_t c_out, int32_t off, const float *dy,
+                                       const float *relu_y, int accumulate, float *dx, void *stream) {
+    clear_error();
+    if (rows < 0 || c_in < 1 || off < 0 || off + c_in > c_out || (rows > 0 && (!dy || !relu_y || !dx)))
+        return fail(DC_EINVAL, "bad concat arguments");
+    return concat_backward(rows, c_in, c_out, off, dy, accumulate, dx, static_cast<hipStream_t>(stream), relu_y);
 }
 
 extern "C" size_t dc_batchnorm_workspace_bytes(int64_t rows, int32_t c) {
@@ -368,6 +408,22 @@ extern "C" int dc_batchnorm_backward(int64_t rows, int32_t c, const float *dy, c
     DC_TRY(need_ws(bn_ws_bytes(rows, c), ws, ws_bytes));
     return bn_backward(rows, c, dy, x, gamma, mean, invstd, accumulate, dx, dgamma, dbeta, ws,
                        static_cast<hipStream_t>(stream));
+}
+
+extern "C" int dc_batchnorm_backward_relu(int64_t rows, int32_t c, const float *dy, const float *relu_y,
+                                          const float *x, const float *gamma, const float *mean, const float *invstd,
+                                          int accumulate, float *dx, float *dgamma, float *dbeta, void *ws,
+                                          size_t ws_bytes, void *stream) {
+    clear_error();
+    if (rows < 0 || c < 1)
+        return fail(DC_EINVAL, "bad batchnorm arguments");
+    if (rows == 0)
+        return DC_OK;
+    if (!dy || !relu_y || !x || !gamma || !mean || !invstd || !dgamma || !dbeta)
+        return fail(DC_EINVAL, "NULL tensor");
+    DC_TRY(need_ws(bn_ws_bytes(rows, c), ws, ws_bytes));
+    return bn_backward(rows, c, dy, x, gamma, mean, invstd, accumulate, dx, dgamma, dbeta, ws,
+                       static_cast<hipStream_t>(stream), relu_y);
 }
 
 extern "C" size_t dc_softmax_xent_workspace_bytes(int32_t n) { return xent_ws_bytes(n); }

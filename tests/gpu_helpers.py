@@ -44,3 +44,13 @@ def rel_err(x, ref):
 
 def stream():
     return torch().cuda.current_stream().cuda_stream
+
+
+# Lines the GPU tests want in the session's output whether they pass or not
+# (tests/conftest.py prints them in the terminal summary).
+SUMMARY = []
+
+
+def report(line):
+    print(line, flush=True)
+    SUMMARY.append(line)

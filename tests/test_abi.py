@@ -184,3 +184,15 @@ def test_ibatch_hand_fixture_through_abi():
     plan = D.dc_plan_ibatch(D.Profile(f["pt"], f["fc"], b["bc"], b["gt"], 3))
     assert plan.decisions() == (f["p"], b["g"])
     assert (plan.t_fwd_ns, plan.t_bwd_ns) == (f["T"], b["T"])
+
+
+def test_ibatch_hand_worked_cases_through_abi():
+    d = json.load(open(os.path.join(ROOT, "tests", "golden", "ibatch_cases.json")))
+    for f in d["forward"]:
+        z = [0] * len(f["pt"])
+        plan = D.dc_plan_ibatch(D.Profile(f["pt"], f["fc"], z, z, f["dt"]))
+        assert plan.decisions()[0] == f["p"] and plan.t_fwd_ns == f["T"], f["name"]
+    for b in d["backward"]:
+        z = [0] * len(b["bc"])
+        plan = D.dc_plan_ibatch(D.Profile(z, z, b["bc"], b["gt"], b["dt"]))
+        assert plan.decisions()[1] == b["g"] and plan.t_bwd_ns == b["T"], b["name"]

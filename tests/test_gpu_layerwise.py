@@ -1,50 +1,26 @@
-"""Every op of the deep workloads on the GPU, fed the oracle's own tensors.
+"""Every op of the workloads on the GPU, fed the oracle's own tensors.
 
 The end-to-end iteration of a deep ReLU / BatchNorm network is chaotic under
 float32 rounding: float32 evaluations of it (torch's, or the oracle with its
 conv / BN outputs nudged by one float32 rounding) scatter by up to 50% on some
 gradient tensors, so the end-to-end parity test there can only hold the GPU
 to that scatter.  This test removes the chaos instead of widening the bar:
-the oracle runs the whole float64 iteration; then each op's GPU kernel is
-called through the C ABI on the oracle's input tensors (forward) and on the
-oracle's gradient of the op's output (backward), rounded to float32, and its
-output is compared with the oracle's output of that op at the kernel-level
-bars of test_gpu_kernels.py.  Nothing flows from the GPU into the oracle.
-
-Bars per tensor (max |gpu - oracle| / max |oracle|): conv / FC passes
-tol(sum length); BatchNorm tol(rows), 10x for its data gradient; pooling,
-GAP and residual add 1e-6; ReLU, max-pool forward and concatenation
-bit-exact against the oracle's value rounded to float32 (their decisions are
-taken in float32 on both sides); loss 1e-6 relative.
+each op's kernels, plain and as the model folds them, run on the oracle's
+own tensors at kernel-level bars (tests/layerwise.py).  These are reduced
+batches; tests/test_gpu_full_batch.py does the same at the benchmark
+configurations' own batches.
 """
-import ctypes
-import math
-
-import numpy as np
 import pytest
 
 import synth
 from oracle import cnn as OC
 from oracle import nets as ON
-from paper_2101_07968_amd import _lib as D
-from tests.gpu_helpers import dev, host, rel_err, scratch, stream, zeros
+from tests import layerwise
 
 pytestmark = pytest.mark.gpu
 
-
-def tol(k_terms):
-    return min(2e-4, 1e-5 * max(1.0, math.sqrt(k_terms / 256.0)))
-
-
-def f32(a):
-    return dev(np.ascontiguousarray(np.asarray(a, dtype=np.float32)))
-
-
-def exact(got, ref):
-    np.testing.assert_array_equal(got, np.asarray(ref, dtype=np.float32))
-
-
-CASES = [("resnet50", 2), ("resnet152", 2), ("inception_v4", 1), ("googlenet", 2), ("vgg16", 1), ("resnet18", 8)]
+CASES = [("resnet50", 2), ("resnet152", 2), ("inception_v4", 1), ("googlenet", 2), ("vgg16", 1), ("resnet18", 8),
+         ("alexnet", 2), ("tiny", 4)]
 
 
 @pytest.mark.parametrize("name,batch", CASES, ids=[f"{n}-b{b}" for n, b in CASES])
@@ -53,151 +29,7 @@ def test_each_op_on_oracle_tensors(name, batch):
     net = OC.Net(spec, batch)
     x, y, params = synth.cnn_inputs(30 + batch, batch, spec["hwc"], spec["classes"], net.param_specs)
     print(f"layerwise {name} batch {batch}", flush=True)
-    loss_ref, grads_ref, t, cache, g = net.loss_and_grads(x, y, params, keep=True)
-    p64 = np.asarray(params, dtype=np.float64)
-    worst = {}
-
-    def check(kind, err, bar):
-        assert err <= bar, (kind, err, bar)
-        worst[kind] = max(worst.get(kind, 0.0), err / bar)
-
-    def prm(i, key):
-        off, shape = net.pslots[i][key]
-        return p64[off:off + int(np.prod(shape))].reshape(shape)
-
-    s = stream()
-    for i, op in enumerate(net.ops):
-        kind = op["op"]
-        a = t[op["in"]]
-        out_ref = t[i + 1]
-        dy = g[i + 1]
-        n, h, w, c = a.shape
-        if kind in ("conv", "fc"):
-            if kind == "conv":
-                r, ss, st = op["r"], op["s"], op["stride"]
-                ph, pw = op["pad"], op.get("pad_w", op["pad"])
-                geom = (n, h, w, c, op["k"], r, ss, st, ph, pw)
-                wt = prm(i, "w")
-            else:
-                geom = (n, 1, 1, h * w * c, op["out"], 1, 1, 1, 0, 0)
-                wt = prm(i, "w").reshape(op["out"], 1, 1, h * w * c)
-                r = ss = 1
-            sh = D.ConvShape(*geom)
-            K = geom[4]
-            P, Q = out_ref.shape[1], out_ref.shape[2]
-            _ws_t, ws, wsb = scratch(D.lib().dc_conv2d_workspace_bytes(ctypes.byref(sh)))
-            xd, wd, dyd = f32(a), f32(wt), f32(dy)
-            bias = f32(prm(i, "b")) if op["bias"] else None
-            yo = zeros((n, P, Q, K))
-            D.call("dc_conv2d_forward", ctypes.byref(sh), xd.data_ptr(), wd.data_ptr(),
-                   bias.data_ptr() if bias is not None else None, 0, yo.data_ptr(), ws, wsb, s)
-            check(kind + " fwd", rel_err(host(yo).reshape(out_ref.shape), out_ref), tol(r * ss * geom[3]))
-            dw = zeros(wt.shape)
-            db = zeros((K,))
-            D.call("dc_conv2d_backward_filter", ctypes.byref(sh), xd.data_ptr(), dyd.data_ptr(), dw.data_ptr(),
-                   db.data_ptr() if op["bias"] else None, ws, wsb, s)
-            off, shape = net.pslots[i]["w"]
-            check(kind + " wgrad", rel_err(host(dw).reshape(-1), grads_ref[off:off + int(np.prod(shape))]),
-                  tol(n * P * Q))
-            if op["bias"]:
-                off, shape = net.pslots[i]["b"]
-                check(kind + " bias grad", rel_err(host(db), grads_ref[off:off + shape[0]]), tol(n * P * Q))
-            if op["in"] != 0:
-                dx = zeros(a.shape)
-                D.call("dc_conv2d_backward_data", ctypes.byref(sh), dyd.data_ptr(), wd.data_ptr(), 0,
-                       dx.data_ptr(), ws, wsb, s)
-                if kind == "conv":
-                    dx_ref = OC.conv2d_backward_data(dy, wt, (h, w), st, (ph, pw))
-                else:
-                    dx_ref = (dy.reshape(n, -1) @ prm(i, "w")).reshape(a.shape)
-                check(kind + " dgrad", rel_err(host(dx), dx_ref), tol(r * ss * K))
-        elif kind == "bn":
-            rows = n * h * w
-            gamma, beta = prm(i, "gamma"), prm(i, "beta")
-            _ws_t, ws, wsb = scratch(D.lib().dc_batchnorm_workspace_bytes(rows, c))
-            xd, gd, bd, dyd = f32(a), f32(gamma), f32(beta), f32(dy)
-            yo, mean, invstd = zeros(a.shape), zeros((c,)), zeros((c,))
-            D.call("dc_batchnorm_forward", rows, c, xd.data_ptr(), gd.data_ptr(), bd.data_ptr(),
-                   ctypes.c_float(OC.BN_EPS), yo.data_ptr(), mean.data_ptr(), invstd.data_ptr(), ws, wsb, s)
-            check("bn fwd", rel_err(host(yo), out_ref), tol(rows))
-            dx, dg, dbeta = zeros(a.shape), zeros((c,)), zeros((c,))
-            D.call("dc_batchnorm_backward", rows, c, dyd.data_ptr(), xd.data_ptr(), gd.data_ptr(), mean.data_ptr(),
-                   invstd.data_ptr(), 0, dx.data_ptr(), dg.data_ptr(), dbeta.data_ptr(), ws, wsb, s)
-            xhat, inv_ref = cache[i]
-            dx_ref, dg_ref, db_ref = OC.batchnorm_backward(dy, xhat, inv_ref, gamma)
-            check("bn dgamma", rel_err(host(dg), dg_ref), tol(rows))
-            check("bn dbeta", rel_err(host(dbeta), db_ref), tol(rows))
-            check("bn dgrad", rel_err(host(dx), dx_ref), 10 * tol(rows))
-        elif kind == "relu":
-            nel = a.size
-            xd, dyd = f32(a), f32(dy)
-            yo = zeros(a.shape)
-            D.call("dc_relu_forward", xd.data_ptr(), yo.data_ptr(), nel, s)
-            yh = host(yo)
-            exact(yh, out_ref)
-            dx = zeros(a.shape)
-            D.call("dc_relu_backward", dyd.data_ptr(), yo.data_ptr(), 0, dx.data_ptr(), nel, s)
-            exact(host(dx), np.where(OC.relu_mask(a), dy, 0.0))
-            worst["relu"] = 0.0
-        elif kind in ("maxpool", "avgpool"):
-            r, st, pad = op["r"], op["stride"], op["pad"]
-            psh = D.PoolShape(n, h, w, c, r, op["s"], st, pad)
-            xd, dyd = f32(a), f32(dy)
-            yo = zeros(out_ref.shape)
-            dx = zeros(a.shape)
-            if kind == "maxpool":
-                arg = zeros(out_ref.shape, "uint8")
-                D.call("dc_maxpool_forward", ctypes.byref(psh), xd.data_ptr(), yo.data_ptr(), arg.data_ptr(), s)
-                exact(host(yo), out_ref)
-                np.testing.assert_array_equal(host(arg).astype(np.int32), cache[i])
-                D.call("dc_maxpool_backward", ctypes.byref(psh), dyd.data_ptr(), arg.data_ptr(), 0, dx.data_ptr(), s)
-                check("maxpool bwd", rel_err(host(dx), OC.maxpool_backward(dy, cache[i], a.shape, r, op["s"], st, pad)),
-                      1e-6)
-            else:
-                D.call("dc_avgpool_forward", ctypes.byref(psh), xd.data_ptr(), yo.data_ptr(), s)
-                check("avgpool fwd", rel_err(host(yo), out_ref), 1e-6)
-                D.call("dc_avgpool_backward", ctypes.byref(psh), dyd.data_ptr(), 0, dx.data_ptr(), s)
-                check("avgpool bwd", rel_err(host(dx), OC.avgpool_backward(dy, a.shape, r, op["s"], st, pad)), 1e-6)
-        elif kind == "gap":
-            xd, dyd = f32(a), f32(dy)
-            yo, dx = zeros(out_ref.shape), zeros(a.shape)
-            D.call("dc_gap_forward", n, h * w, c, xd.data_ptr(), yo.data_ptr(), s)
-            check("gap fwd", rel_err(host(yo), out_ref), 1e-6)
-            D.call("dc_gap_backward", n, h * w, c, dyd.data_ptr(), 0, dx.data_ptr(), s)
-            check("gap bwd", rel_err(host(dx), np.broadcast_to(dy / (h * w), a.shape)), 1e-6)
-        elif kind == "add":
-            ad, bd = f32(a), f32(t[op["other"]])
-            yo = zeros(a.shape)
-            D.call("dc_add_forward", ad.data_ptr(), bd.data_ptr(), 0, yo.data_ptr(), a.size, s)
-            check("add fwd", rel_err(host(yo), out_ref), 1e-6)
-        elif kind == "concat":
-            parts = [op["in"]] + list(op["others"])
-            ct = out_ref.shape[3]
-            rows = n * h * w
-            yo = zeros(out_ref.shape)
-            dyd = f32(dy)
-            lo = 0
-            for tid in parts:
-                ci = t[tid].shape[3]
-                xd = f32(t[tid])
-                D.call("dc_concat_forward", rows, ci, ct, lo, xd.data_ptr(), yo.data_ptr(), s)
-                dx = zeros(t[tid].shape)
-                D.call("dc_concat_backward", rows, ci, ct, lo, dyd.data_ptr(), 0, dx.data_ptr(), s)
-                exact(host(dx), dy[..., lo:lo + ci])
-                lo += ci
-            exact(host(yo), out_ref)
-            worst["concat"] = 0.0
-        else:
-            raise AssertionError(kind)
-    # the loss on the oracle's logits
-    z = t[-1].reshape(batch, -1)
-    classes = z.shape[1]
-    _ws_t, ws, wsb = scratch(D.lib().dc_softmax_xent_workspace_bytes(batch))
-    zd, yd = f32(z), dev(np.asarray(y, dtype=np.int32))
-    loss, dz = zeros((1,)), zeros((batch, classes))
-    D.call("dc_softmax_xent", batch, classes, zd.data_ptr(), yd.data_ptr(), loss.data_ptr(), dz.data_ptr(), ws, wsb, s)
-    l_ref, dz_ref = OC.softmax_xent(z, np.asarray(y))
-    check("loss", abs(float(host(loss)[0]) - l_ref) / abs(l_ref), 1e-6)
-    check("dlogits", rel_err(host(dz), dz_ref), 1e-6)
+    res = net.loss_and_grads(x, y, params, keep=True)
+    worst = layerwise.check_ops(name, net, y, params, res)
     print(f"{name}: worst error / bar per op kind: "
           + ", ".join(f"{k} {v:.3f}" for k, v in sorted(worst.items())), flush=True)

@@ -23,7 +23,7 @@ from oracle import nets as ON
 from oracle import plan as OP
 from paper_2101_07968_amd import _lib as D
 from paper_2101_07968_amd import nets as PN
-from tests.gpu_helpers import dev, rel_err
+from tests.gpu_helpers import dev, rel_err, report
 
 pytestmark = pytest.mark.gpu
 
@@ -212,16 +212,19 @@ def test_profile_plan_timeline_and_model(name, batch, rate):
         assert abs(st["t_iter_ns"] - t_model) <= 0.10 * t_model, (key, st["t_iter_ns"], t_model)
 
 
-CONFIG_RATES = [("vgg16", 32, 3, 100e9 / 8), ("vgg16", 32, 3, 10e9 / 8), ("resnet50", 64, 4, 10e9 / 8),
+CONFIG_RATES = [("vgg16", 32, 3, 100e9 / 8), ("vgg16", 32, 3, 10e9 / 8), ("vgg16", 32, 3, 1e9 / 8),
+                ("vgg16", 32, 3, None), ("resnet50", 64, 4, 10e9 / 8), ("resnet50", 64, 4, None),
                 ("resnet18", 128, 2, 1e9 / 8)]
 
 
 @pytest.mark.parametrize("name,batch,seed,rate", CONFIG_RATES,
-                         ids=[f"{n}-b{b}-{r * 8 / 1e9:g}Gbps" for n, b, _, r in CONFIG_RATES])
+                         ids=[f"{n}-b{b}-" + (f"{r * 8 / 1e9:g}Gbps" if r else "unpaced") for n, b, _, r in CONFIG_RATES])
 def test_time_model_at_config_rates(name, batch, seed, rate):
-    """The benchmark configurations at their own paced link rates: the plan is
-    the oracle DP's on the measured profile, and the measured iteration time of
-    the DP and of the sequential plan is within 10% of f_m (Eq. 8 / 9)."""
+    """The benchmark configurations at their own link rates, paced, and on the
+    unpaced host interface (rate None): the plan is the oracle DP's on the
+    measured profile, and the measured iteration time of the DP and of the
+    sequential plan is within 10% of f_m (Eq. 8 / 9).  AlexNet at 0.1 Gb/s and
+    VGG-16 at 0.1 Gb/s take 40-90 s per iteration and are left to the report."""
     ops, hwc, classes = PN.build(name)
     specs = PN.param_specs(ops, hwc)
     x, y, params = synth.cnn_inputs(seed, batch, hwc, classes, specs)
@@ -229,19 +232,24 @@ def test_time_model_at_config_rates(name, batch, seed, rate):
     model.set_option(D.DC_OPT_LR, PN.WORKLOADS[name]["lr"])  # the workload's own rate: VGG diverges at 1e-2
     model.ps_write(params)
     xd, yd = dev(x), dev(y)
-    lnk = D.link(rate, 0, paced=True)
-    print(f"time model {name} batch {batch} at {rate * 8 / 1e9:g} Gb/s", flush=True)
+    lnk = D.link(rate, 0, paced=True) if rate else UNPACED
+    label = f"{rate * 8 / 1e9:g} Gb/s" if rate else "unpaced"
+    print(f"time model {name} batch {batch} at {label}", flush=True)
     prof = model.profile(xd, yd, lnk, reps=3)
     plan = D.dc_plan(prof)
     p_ref, tf, _, _ = OP.forward_dp(prof.pt.tolist(), prof.fc.tolist(), prof.dt)
     g_ref, tb, _, _ = OP.backward_dp(prof.bc.tolist(), prof.gt.tolist(), prof.dt)
     assert plan.decisions() == (p_ref, g_ref) and (plan.t_fwd_ns, plan.t_bwd_ns) == (tf, tb)
+    errs = {}
     for key, pl in {"dp": plan, "sequential": D.dc_plan_eval(prof, *D.Plan(model.L).decisions())}.items():
         model.step(xd, yd, pl, lnk)  # warm
         st = model.step(xd, yd, pl, lnk)
         t_model = pl.t_fwd_ns + pl.t_bwd_ns
+        errs[key] = (st["t_iter_ns"] - t_model) / t_model
         assert abs(st["t_iter_ns"] - t_model) <= 0.10 * t_model, (key, st["t_iter_ns"], t_model)
         assert np.isfinite(st["loss"])
+    report(f"time model {name} b{batch} {label}: (measured - f_m) / f_m = DP {errs['dp']:+.2%}, "
+           f"sequential {errs['sequential']:+.2%}; DP p={p_ref} g={g_ref}")
 
 
 def test_argument_errors():
@@ -356,29 +364,49 @@ def test_layer_graphs_replay_the_eager_iteration(name, batch):
 
 
 def test_dynamic_step_plans_in_idle_windows():
-    """dc_step_dynamic (idle-event trigger, Sec. IV-C): same decisions as dc_plan,
-    same numbers as dc_step, and planning finished while a transfer was in flight."""
+    """dc_step_dynamic (idle-event trigger, Sec. IV-C) against the oracle: the
+    backward decision it plans on the fly and the forward decision it plans for
+    the next call are the oracle DP's (Eq. 8 / 9, Algorithms 3 / 4) on the
+    profile it was given, with the same f_m; its loss, gradients and post-step
+    weights are the oracle iteration's (the bars of test_step_matches_oracle);
+    planning finished while a transfer was in flight.  A second call runs on the
+    forward decision the first one planned, from the same parameters, and gives
+    bit-identical results; both equal a plain dc_step under the oracle's plan."""
     model, onet, xd, yd, x, y, params = setup_model("resnet18", 16, seed=5)
     lnk = D.link(5e8, 0, paced=True)
     prof = model.profile(xd, yd, lnk, reps=2)
-    ref = D.dc_plan(prof)
+    p_or, tf, _, _ = OP.forward_dp(prof.pt.tolist(), prof.fc.tolist(), prof.dt)
+    g_or, tb, _, _ = OP.backward_dp(prof.bc.tolist(), prof.gt.tolist(), prof.dt)
+    loss_ref, g_ref, w_ref = onet.step(x, y, params)
+    spread, spread_w = fp32_spread(ON.get("resnet18"), onet, x, y, params, g_ref)
+    plan = D.Plan(model.L)
+    plan.p[:] = p_or            # first call: the forward decision given, the backward one planned on the fly
+    outs = []
+    for call in range(2):
+        model.ps_write(params)
+        st = model.step_dynamic(xd, yd, prof, plan, lnk)
+        p_new, g = model.ps_read()
+        outs.append((st["loss"], p_new, g))
+        assert plan.decisions() == (p_or, g_or), call
+        assert (plan.t_fwd_ns, plan.t_bwd_ns) == (tf, tb), call
+        assert st["plan_hidden"] == 3, st
+        assert 0 < st["t_plan_bwd_ns"] and 0 < st["t_plan_fwd_ns"]
+        assert abs(st["loss"] - loss_ref) <= 1e-4 * abs(loss_ref)
+        for i, slots in enumerate(onet.pslots):
+            for pname, (off, shape) in slots.items():
+                sl = slice(off, off + int(np.prod(shape)))
+                assert rel_err(g[sl], g_ref[sl]) <= max(1e-3, 5.0 * spread[(i, pname)]), (call, i, pname)
+                assert rel_err(p_new[sl], w_ref[sl]) <= max(1e-3, 5.0 * spread_w[(i, pname)]), (call, i, pname)
+    assert outs[1][0] == outs[0][0]
+    np.testing.assert_array_equal(outs[1][1], outs[0][1])
+    np.testing.assert_array_equal(outs[1][2], outs[0][2])
+    # the same numbers as dc_step under the oracle's decisions
     model.ps_write(params)
-    st_ref = model.step(xd, yd, ref, lnk)
-    p_ref, g_ref = model.ps_read()
-    plan = D.Plan(model.L)                      # first call: sequential forward, backward planned on the fly
-    plan.p[:] = ref.p
-    model.ps_write(params)
-    st = model.step_dynamic(xd, yd, prof, plan, lnk)
-    p_dyn, g_dyn = model.ps_read()
-    assert plan.decisions() == ref.decisions()
-    assert st["loss"] == st_ref["loss"]
-    np.testing.assert_array_equal(g_dyn, g_ref)
-    np.testing.assert_array_equal(p_dyn, p_ref)
-    assert st["plan_hidden"] == 3, st
-    assert 0 < st["t_plan_bwd_ns"] and 0 < st["t_plan_fwd_ns"]
-    # a second call reuses the decision the first one planned for it
-    st2 = model.step_dynamic(xd, yd, prof, plan, lnk)
-    assert plan.decisions() == ref.decisions() and st2["n_pull"] == st["n_pull"]
+    st_ref = model.step(xd, yd, D.dc_plan_eval(prof, p_or, g_or), lnk)
+    p_s, g_s = model.ps_read()
+    assert st_ref["loss"] == outs[0][0]
+    np.testing.assert_array_equal(g_s, outs[0][2])
+    np.testing.assert_array_equal(p_s, outs[0][1])
 
 
 def test_replanning_follows_the_link():

@@ -11,6 +11,7 @@ checked against things that do not share their recurrences:
 * the special cases of Sec. III-B: one segment is the sequential default PS,
   and with no per-transmission overhead layer-by-layer is never worse than it.
 """
+import inspect
 import itertools
 import json
 import os
@@ -210,6 +211,52 @@ def test_ibatch_hand_worked():
     b = d["backward"]
     g, t = P.ibatch_backward(b["bc"], b["gt"], b["dt"])
     assert g == b["g"] and t == b["T"]
+
+
+def test_ibatch_hand_worked_cases():
+    """Algorithm 1's loop choosing among several positions in three iterations, and
+    finding none; Algorithm 2's winning candidate running to k = 3 with k * dt
+    deciding a step (tests/golden/ibatch_cases.json, derived by hand)."""
+    d = _load("ibatch_cases.json")
+    for f in d["forward"]:
+        p = P.ibatch_forward(f["pt"], f["fc"], f["dt"])
+        assert p == f["p"] and P.fm_forward(f["pt"], f["fc"], f["dt"], p) == f["T"], f["name"]
+        assert P.forward_dp(f["pt"], f["fc"], f["dt"])[1] <= f["T"]
+    for b in d["backward"]:
+        g, t = P.ibatch_backward(b["bc"], b["gt"], b["dt"])
+        assert g == b["g"] and t == b["T"], b["name"]
+        assert P.backward_dp(b["bc"], b["gt"], b["dt"])[1] <= b["T"]
+
+
+def _mutant(fn, old, new):
+    """fn with one source fragment replaced: a plausible slip, planted in a copy on the CPU."""
+    src = inspect.getsource(fn)
+    assert old in src, old
+    ns = dict(vars(P))
+    exec(src.replace(old, new), ns)
+    return ns[fn.__name__]
+
+
+SLIPS = [
+    ("forward", P.ibatch_forward, "j = min((dt + (PT[x] - PT[m])", "j = max((dt + (PT[x] - PT[m])"),
+    ("forward", P.ibatch_forward, "            j = L\n", "            j = m + 1\n"),
+    ("forward", P.ibatch_forward, "d2 = min((dt + (PT[b] - PT[a])", "d2 = max((dt + (PT[b] - PT[a])"),
+    ("backward", P.ibatch_backward, "pushed = k * dt +", "pushed = dt +"),
+    ("backward", P.ibatch_backward, "j = min((pushed - (BC[m - 1] - BC[x - 1]), x)",
+     "j = max((pushed - (BC[m - 1] - BC[x - 1]), x)"),
+    ("backward", P.ibatch_backward, "                j = m - 1\n", "                j = 1\n"),
+]
+
+
+@pytest.mark.parametrize("which,fn,old,new", SLIPS, ids=[f"{w}-{i}" for i, (w, *_rest) in enumerate(SLIPS)])
+def test_ibatch_fixtures_catch_slips(which, fn, old, new):
+    """Each slip, planted in a copy of the oracle, fails one of the hand-worked fixtures."""
+    bad = _mutant(fn, old, new)
+    cases = _load("ibatch_cases.json")[which] + [_load("ibatch_hand.json")[which]]
+    if which == "forward":
+        assert any(bad(c["pt"], c["fc"], c["dt"]) != c["p"] for c in cases)
+    else:
+        assert any(bad(c["bc"], c["gt"], c["dt"]) != (c["g"], c["T"]) for c in cases)
 
 
 @pytest.mark.parametrize("seed", range(150))

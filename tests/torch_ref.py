@@ -12,8 +12,11 @@ def _nchw(a, dtype):
     return torch.from_numpy(np.ascontiguousarray(np.asarray(a).transpose(0, 3, 1, 2))).to(dtype)
 
 
-def loss_and_grads(spec, net, x, y, p, dtype=torch.float64):
-    """(loss, flat gradient as float64) of one iteration in the given torch dtype on the CPU."""
+def loss_and_grads(spec, net, x, y, p, dtype=torch.float64, perturb=None):
+    """(loss, flat gradient as float64) of one iteration in the given torch dtype on the CPU.
+
+    perturb(i, o), if given, replaces the output o (NCHW) of every conv, FC and
+    BN op i in the forward pass, as the oracle's test hook does."""
     pt = torch.from_numpy(np.asarray(p, dtype=np.float64)).to(dtype).requires_grad_(True)
 
     def prm(i, name):
@@ -47,6 +50,8 @@ def loss_and_grads(spec, net, x, y, p, dtype=torch.float64):
             o = a + t[op["other"]]
         elif k == "concat":
             o = torch.cat([a] + [t[j] for j in op["others"]], dim=1)
+        if perturb is not None and k in ("conv", "fc", "bn"):
+            o = perturb(i, o)
         t.append(o)
     loss = F.cross_entropy(t[-1].reshape(net.batch, -1), torch.from_numpy(np.asarray(y, dtype=np.int64)))
     loss.backward()
