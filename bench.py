@@ -10,9 +10,12 @@ Prints one JSON line (rank 0, N = 1):
   value        images/s with the DynaComm plan (whole job = the one GPU)
   extra        the same for the sequential (no-overlap) and layer-by-layer plans,
                measured iteration times next to the time model f_m
-  roofline     conv / FC implicit-GEMM kernels against the fp32 MFMA peak,
-               timed live with HIP events on their launch stream
-  cpu_baseline the oracle (float64 loops) on a bounded sample, host cores
+  roofline     conv / FC implicit-GEMM passes against the fp32 MFMA peak, timed
+               inside the timed DP steps with HIP events on the compute stream
+               (DC_OPT_GEMM_TIMING); the same passes launched alone are reported
+               beside them
+  cpu_baseline the oracle (float64 loops) for one whole iteration of the same
+               workload and batch on the host cores (about a minute for VGG-16)
 """
 from __future__ import annotations
 
@@ -46,6 +49,8 @@ def parse():
     ap.add_argument("--compare", default="sequential,lbl,ibatch", help="other plans to time ('' for none)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-roofline", action="store_true")
+    ap.add_argument("--oracle-configs", action="store_true",
+                    help="time the oracle on every benchmark configuration and the planner oracle, then exit")
     ap.add_argument("--kernels-only", action="store_true",
                     help="run each conv / FC pass of the workload once plus a 256 MiB calibration copy "
                          "(for rocprofv3 --pmc), then exit")
@@ -128,24 +133,76 @@ def measure_convs(D, PN, ops, hwc, batch, reps=3):
     return flops, ms_total, per
 
 
-def cpu_baseline(name, batch_total):
-    """The oracle, untuned, on one image of the workload: forward, backward and SGD."""
-    import numpy as np
+def cpu_model():
+    """The host CPU's model string and the OpenMP threads the oracle runs with."""
+    model = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or os.cpu_count()
+    return model, threads
 
+
+def oracle_iteration(name, batch, seed):
+    """One full oracle iteration (float64 loops: forward, backward, server SGD) on the
+    workload's own seeded inputs; returns its wall time in seconds."""
     import synth
     from oracle import cnn as OC
     from oracle import nets as ON
     spec = ON.get(name)
-    n = 1
-    net = OC.Net(spec, n)
-    x, y, p = synth.cnn_inputs(0, n, spec["hwc"], spec["classes"], net.param_specs)
+    net = OC.Net(spec, batch)
+    x, y, p = synth.cnn_inputs(seed, batch, spec["hwc"], spec["classes"], net.param_specs)
     t0 = time.perf_counter()
     net.step(x, y, p)
-    dt = time.perf_counter() - t0
-    threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or os.cpu_count()
-    return {"value": round(n / dt, 4), "unit": "images/s", "cores": threads, "kind": "oracle",
-            "sample": f"{n} of the {batch_total} images of one {name} iteration (forward, backward, SGD), "
-                      f"{dt:.1f} s, float64 loops with OpenMP"}
+    return time.perf_counter() - t0
+
+
+def cpu_baseline(name, batch, seed):
+    """The oracle, untuned, for one whole iteration of the benchmarked workload and batch."""
+    dt = oracle_iteration(name, batch, seed)
+    model, threads = cpu_model()
+    return {"value": round(batch / dt, 4), "unit": "images/s", "cores": threads, "kind": "oracle",
+            "cpu": model, "seconds": round(dt, 2),
+            "sample": f"one whole {name} iteration at batch {batch} (the benchmark's own seeded inputs): "
+                      f"forward, backward and SGD in float64 loops with OpenMP on {threads} threads, {dt:.1f} s"}
+
+
+def oracle_configs():
+    """Oracle images/s for every benchmark configuration at its own batch and seed, and
+    the planner oracle (Eq. 8 / 9 in Python) next to dc_plan at L = 50.  Host only."""
+    from oracle import plan as OP
+    from paper_2101_07968_amd import _lib as D
+    from paper_2101_07968_amd import nets as PN
+    import synth
+    model, threads = cpu_model()
+    rows = []
+    for name in ("tiny", "alexnet", "resnet18", "vgg16", "resnet50"):
+        wl = PN.WORKLOADS[name]
+        dt = oracle_iteration(name, wl["batch"], wl["seed"])
+        rows.append({"workload": name, "batch": wl["batch"], "seconds": round(dt, 3),
+                     "images_per_s": round(wl["batch"] / dt, 4)})
+        log(f"[oracle] {name} batch {wl['batch']}: {dt:.2f} s, {wl['batch'] / dt:.3f} images/s")
+    plans = []
+    for L in (50, 76, 152):
+        pt, fc, bc, gt, dt = synth.random_profile(777 + L, L, hi=10 ** 7, dt_hi=10 ** 6)
+        t0 = time.perf_counter()
+        OP.forward_dp(pt, fc, dt)
+        OP.backward_dp(bc, gt, dt)
+        t_py = time.perf_counter() - t0
+        prof = D.Profile(pt, fc, bc, gt, dt)
+        D.dc_plan(prof)
+        t0 = time.perf_counter()
+        reps = 20
+        for _ in range(reps):
+            D.dc_plan(prof)
+        t_c = (time.perf_counter() - t0) / reps
+        plans.append({"L": L, "oracle_ms": round(t_py * 1e3, 2), "dc_plan_ms": round(t_c * 1e3, 4)})
+        log(f"[oracle] planner L={L}: oracle (Python) {t_py * 1e3:.1f} ms, dc_plan {t_c * 1e3:.3f} ms")
+    print(json.dumps({"cpu": model, "threads": threads, "oracle_iterations": rows, "planner": plans}), flush=True)
 
 
 def _finite(v):
@@ -166,6 +223,9 @@ def main():
         print(f"bench.py runs on one GPU only (the library has no multi-GPU path); got --gpus {args.gpus}",
               file=sys.stderr)
         sys.exit(2)
+    if args.oracle_configs:
+        oracle_configs()
+        return
     import numpy as np
     import torch
 
@@ -203,12 +263,16 @@ def main():
     t_plan_us = (time.perf_counter() - t0) * 1e6
     log(f"[bench] profiled in {t_profile:.2f} s; plan p={plan.decisions()[0]} g={plan.decisions()[1]}")
 
+    gemm = {"n": 0, "ns": 0, "flop": 0.0}
+
     def run(kind, steps, warmup):
         # every plan starts from the same initial parameters (outside the timed region)
         model.ps_write(params)
         for _ in range(warmup):
             pl = D.dc_plan(prof) if kind == "dp" else fixed[kind]
             model.step(xd, yd, pl, lnk)
+        # the DP steps time their own conv / FC GEMM passes with events on the compute stream
+        model.set_option(D.DC_OPT_GEMM_TIMING, 1 if kind == "dp" else 0)
         torch.cuda.synchronize()
         iters, losses = [], []
         t0 = time.perf_counter()
@@ -217,8 +281,13 @@ def main():
             st = model.step(xd, yd, pl, lnk)
             iters.append(st["t_iter_ns"])
             losses.append(st["loss"])
+            if kind == "dp":
+                gemm["n"] += st["n_gemm"]
+                gemm["ns"] += st["t_gemm_ns"]
+                gemm["flop"] += st["gemm_flop"]
         torch.cuda.synchronize()
         wall = time.perf_counter() - t0
+        model.set_option(D.DC_OPT_GEMM_TIMING, 0)
         pl = D.dc_plan(prof) if kind == "dp" else fixed[kind]
         res = {"images_per_s": batch * steps / wall, "ms_per_step": wall / steps * 1e3,
                "t_iter_ms": float(np.mean(iters)) / 1e6, "t_model_ms": (pl.t_fwd_ns + pl.t_bwd_ns) / 1e6,
@@ -235,25 +304,38 @@ def main():
         others[kind] = run(kind, max(2, args.steps // 2), 1)
 
     roof = None
-    if not args.no_roofline:
-        flops, ms, per = measure_convs(D, PN, ops, hwc, batch)
-        achieved = flops / (ms * 1e-3) / 1e12
-        roof = {"bound": "mfma", "kernel": "igemm_kernel (conv/FC forward, dgrad, wgrad; fp32 MFMA)",
+    if not args.no_roofline and gemm["n"]:
+        # the timed DP steps' own GEMM passes: algorithmic FLOPs per pass / mean pass duration
+        achieved = gemm["flop"] / (gemm["ns"] * 1e-9) / 1e12
+        per_step = gemm["n"] / args.steps
+        roof = {"bound": "mfma",
+                "kernel": "igemm_kernel: the conv / FC GEMM passes (forward, dgrad, wgrad; fp32 MFMA), each with "
+                          "its split-K reduction, as dispatched inside the timed steps",
                 "achieved": round(achieved, 2), "peak": FP32_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(achieved / FP32_MFMA_PEAK_TFLOPS, 4), "traffic": None,
-                "gflop_per_step": round(flops / 1e9, 1), "conv_ms_per_step": round(ms, 3)}
+                "launches_per_step": per_step, "gflop_per_launch": round(gemm["flop"] / gemm["n"] / 1e9, 3),
+                "ms_per_launch": round(gemm["ns"] / gemm["n"] / 1e6, 4),
+                "gemm_ms_per_step": round(gemm["ns"] / args.steps / 1e6, 3),
+                "gflop_per_step": round(gemm["flop"] / args.steps / 1e9, 1)}
         tr = traffic_from_profiles(name, batch)
         if tr is not None:
             roof["traffic"] = round(tr[0])
             roof["traffic_algorithmic"] = round(tr[1])
-        log(f"[bench] conv GEMMs: {achieved:.1f} TFLOP/s over {flops / 1e9:.0f} GFLOP in {ms:.2f} ms")
+        log(f"[bench] conv GEMMs in the steps: {achieved:.1f} TFLOP/s, {per_step:.0f} passes and "
+            f"{gemm['ns'] / args.steps / 1e6:.2f} ms per step")
+        # the same passes launched alone on random tensors, for comparison
+        flops, ms, per = measure_convs(D, PN, ops, hwc, batch)
+        iso = flops / (ms * 1e-3) / 1e12
+        roof["isolated"] = {"achieved": round(iso, 2), "frac": round(iso / FP32_MFMA_PEAK_TFLOPS, 4),
+                            "gemm_ms_per_step": round(ms, 3)}
+        log(f"[bench] conv GEMMs alone: {iso:.1f} TFLOP/s over {flops / 1e9:.0f} GFLOP in {ms:.2f} ms")
         for d in sorted(per, key=lambda d: -d["ms"]):
             log(f"[bench]   {d['pass']:5s} {str(d['shape']):42s} {d['ms']:8.3f} ms {d['tflops']:7.2f} TFLOP/s")
 
     cpu = None
     if not args.no_cpu_baseline:
         log("[bench] timing the oracle on the host ...")
-        cpu = cpu_baseline(name, batch)
+        cpu = cpu_baseline(name, batch, wl["seed"])
 
     out = {
         "metric": "images/s per SGD iteration with segment-overlapped pull/push; conv MFMA %",

@@ -165,11 +165,15 @@ enum {
     DC_OPT_TIMELINE = 2,    /* 1: dc_step records per-layer timestamps (default 0) */
     DC_OPT_TIMEOUT_S = 3,   /* watchdog for one dc_step / dc_profile in seconds (default 600) */
     DC_OPT_SGD_THREADS = 4, /* host threads of the server update (default: hardware threads, max 16) */
-    DC_OPT_GRAPHS = 5       /* 1: each layer's forward and backward kernels run as one captured HIP graph
+    DC_OPT_GRAPHS = 5,      /* 1: each layer's forward and backward kernels run as one captured HIP graph
                                launch (default 0: launched one by one).  The graphs are captured at the first
                                dc_step / dc_profile for a workspace and batch address (a one-time cost) and
                                recaptured when either changes; results are identical either way.  A graph
                                launch costs more than it saves unless a layer is many kernels of ~1 us */
+    DC_OPT_GEMM_TIMING = 6  /* 1: dc_step brackets every conv / FC GEMM pass it launches (forward, data and
+                               filter gradient, each with its split-K reduction) with a pair of HIP events on
+                               the compute stream and reports their summed durations and algorithmic FLOPs in
+                               dc_step_stats (default 0).  Ignored while DC_OPT_GRAPHS is on */
 };
 int dc_model_set_option(dc_model *m, int option, double value);
 
@@ -288,6 +292,9 @@ typedef struct dc_step_stats {
     int64_t t_plan_fwd_ns; /* dc_step_dynamic: host time of the next forward DP (0 otherwise) */
     int32_t plan_hidden;   /* dc_step_dynamic: bit 0 set if the backward DP ended before the forward
                               pass did, bit 1 if the next forward DP ended before the last push did */
+    int32_t n_gemm;        /* DC_OPT_GEMM_TIMING: conv / FC GEMM passes timed in this step (0 otherwise) */
+    int64_t t_gemm_ns;     /* DC_OPT_GEMM_TIMING: their summed durations, from events on the compute stream */
+    double gemm_flop;      /* DC_OPT_GEMM_TIMING: their algorithmic FLOPs, 2 per multiply-add */
 } dc_step_stats;
 
 /*

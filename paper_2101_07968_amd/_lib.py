@@ -17,7 +17,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libdc.so")
 
 DC_OK, DC_EINVAL, DC_EHIP, DC_ENOMEM, DC_ESTATE, DC_ETIMEOUT = range(6)
 DC_OP_CONV, DC_OP_FC, DC_OP_BN, DC_OP_RELU, DC_OP_MAXPOOL, DC_OP_GAP, DC_OP_ADD, DC_OP_CONCAT, DC_OP_AVGPOOL = range(1, 10)
-DC_OPT_LR, DC_OPT_TIMELINE, DC_OPT_TIMEOUT_S, DC_OPT_SGD_THREADS, DC_OPT_GRAPHS = range(1, 6)
+DC_OPT_LR, DC_OPT_TIMELINE, DC_OPT_TIMEOUT_S, DC_OPT_SGD_THREADS, DC_OPT_GRAPHS, DC_OPT_GEMM_TIMING = range(1, 7)
 
 c_i32, c_i64, c_f32, c_f64, c_sz, c_vp = (ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_double,
                                           ctypes.c_size_t, ctypes.c_void_p)
@@ -80,7 +80,8 @@ class PlanT(ctypes.Structure):
 class StepStats(ctypes.Structure):
     _fields_ = [("loss", c_f32), ("n_pull", c_i32), ("n_push", c_i32), ("t_iter_ns", c_i64), ("t_fwd_ns", c_i64),
                 ("t_bwd_ns", c_i64), ("t_compute_ns", c_i64), ("t_link_ns", c_i64), ("t_sgd_tail_ns", c_i64),
-                ("t_host_ns", c_i64), ("t_plan_bwd_ns", c_i64), ("t_plan_fwd_ns", c_i64), ("plan_hidden", c_i32)]
+                ("t_host_ns", c_i64), ("t_plan_bwd_ns", c_i64), ("t_plan_fwd_ns", c_i64), ("plan_hidden", c_i32),
+                ("n_gemm", c_i32), ("t_gemm_ns", c_i64), ("gemm_flop", c_f64)]
 
     def as_dict(self):
         return {name: getattr(self, name) for name, _ in self._fields_}

@@ -178,6 +178,7 @@ int step_impl(dc_model *m, const dc_batch *b, dc_plan_t *plan, const dc_profile_
     const auto pulls = pull_segs(plan, L);
     const Clock::time_point deadline = t_host0 + std::chrono::microseconds((int64_t)(m->timeout_s * 1e6));
     m->timeline_valid = false;
+    m->gemm_n = 0;
     int64_t t_plan_bwd = 0, t_plan_fwd = 0;
     int32_t hidden = 0;
 
@@ -281,6 +282,12 @@ int step_impl(dc_model *m, const dc_batch *b, dc_plan_t *plan, const dc_profile_
         out->t_plan_bwd_ns = t_plan_bwd;
         out->t_plan_fwd_ns = t_plan_fwd;
         out->plan_hidden = hidden;
+        for (size_t i = 0; i < m->gemm_n; ++i) {
+            DC_TRY(elapsed_ns(m->gemm_ev[2 * i], m->gemm_ev[2 * i + 1], &d));
+            out->t_gemm_ns += d;
+            out->gemm_flop += m->gemm_flop[i];
+        }
+        out->n_gemm = (int32_t)m->gemm_n;
     }
     if (m->timeline) {
         m->timeline_ns.assign(8 * (size_t)L, 0);
@@ -444,6 +451,13 @@ extern "C" int dc_profile(dc_model *m, const dc_batch *b, const dc_link *link, i
         return fail(DC_EINVAL, "profile arrays must hold L=%d entries", m->L);
     const int L = m->L;
     hipStream_t cs = static_cast<hipStream_t>(stream);
+    // the profile times whole layers; GEMM pass events are for dc_step only
+    struct GemmTimingOff {
+        dc_model *m;
+        int saved;
+        ~GemmTimingOff() { m->gemm_timing = saved; }
+    } timing_off{m, m->gemm_timing};
+    m->gemm_timing = 0;
     // every parameter on the device, then one untimed pass
     DC_HIP(hipMemcpyAsync(m->dparams(), m->ps_params, m->n_params * sizeof(float), hipMemcpyHostToDevice, cs));
     for (int l = 1; l <= L; ++l)

@@ -289,6 +289,41 @@ static int build_model(dc_model *m, const dc_op_desc *ops, int n_ops) {
 
 // ---------------------------------------------------------------- mini-procedures
 
+// Algorithmic FLOPs of one GEMM pass (forward, data or filter gradient):
+// 2 per multiply-add, N*P*Q*K*R*S*C multiply-adds.
+static double gemm_flop(const ConvGeom &g) {
+    return 2.0 * g.N * g.P * g.Q * (double)g.K * g.R * g.S * g.C;
+}
+
+int gemm_mark(dc_model *m, bool start, double flop, hipStream_t s) {
+    if (!m->gemm_timing || m->use_graphs)
+        return DC_OK;
+    const size_t i = 2 * m->gemm_n + (start ? 0 : 1);
+    while (m->gemm_ev.size() <= i) {
+        hipEvent_t e = nullptr;
+        DC_HIP(hipEventCreate(&e));
+        m->gemm_ev.push_back(e);
+    }
+    if (start) {
+        if (m->gemm_flop.size() <= m->gemm_n)
+            m->gemm_flop.resize(m->gemm_n + 1);
+        m->gemm_flop[m->gemm_n] = flop;
+    }
+    DC_HIP(hipEventRecord(m->gemm_ev[i], s));
+    if (!start)
+        ++m->gemm_n;
+    return DC_OK;
+}
+
+void free_gemm_events(dc_model *m) {
+    for (hipEvent_t e : m->gemm_ev)
+        if (e)
+            (void)hipEventDestroy(e);
+    m->gemm_ev.clear();
+    m->gemm_flop.clear();
+    m->gemm_n = 0;
+}
+
 int run_forward_layer(dc_model *m, int l, const float *x, const int32_t *y, hipStream_t s) {
     const float *P = m->dparams();
     for (int i = m->layer_first[l]; i <= m->layer_last[l]; ++i) {
@@ -302,8 +337,10 @@ int run_forward_layer(dc_model *m, int l, const float *x, const int32_t *y, hipS
         switch (o.d.kind) {
         case DC_OP_CONV:
         case DC_OP_FC:
+            DC_TRY(gemm_mark(m, true, gemm_flop(o.geom), s));
             DC_TRY(conv_forward(o.geom, o.fwd, in, P + o.w_off, o.b_off != NONE ? P + o.b_off : nullptr, relu, out,
                                 m->scratch(), s));
+            DC_TRY(gemm_mark(m, false, 0, s));
             break;
         case DC_OP_BN: {
             float *mean = reinterpret_cast<float *>(m->ws + o.aux);
@@ -365,7 +402,9 @@ int run_backward_layer(dc_model *m, int l, const float *x, hipStream_t s, BwdRec
         case DC_OP_CONV:
         case DC_OP_FC:
             if (!rec) {
+                DC_TRY(gemm_mark(m, true, gemm_flop(o.geom), s));
                 DC_TRY(conv_wgrad(o.geom, o.wgrad, in, dy, G + o.w_off, m->scratch(), s));
+                DC_TRY(gemm_mark(m, false, 0, s));
                 if (o.b_off != NONE)
                     DC_TRY(colsum((int64_t)to.n * to.h * to.w, to.c, dy, G + o.b_off, m->scratch(), s));
             }
@@ -373,13 +412,19 @@ int run_backward_layer(dc_model *m, int l, const float *x, hipStream_t s, BwdRec
                 const OpInfo &r = m->ops[o.dgrad_relu_from];
                 note(r.out, i, o.acc_in[0], 1);
                 note(r.d.in0, o.dgrad_relu_from, r.acc_in[0], 0);
-                if (!rec)
+                if (!rec) {
+                    DC_TRY(gemm_mark(m, true, gemm_flop(o.geom), s));
                     DC_TRY(conv_dgrad(o.geom, o.dgrad, dy, P + o.w_off, r.acc_in[0], m->grad(r.d.in0), m->scratch(),
                                       s, m->act(r.out)));
+                    DC_TRY(gemm_mark(m, false, 0, s));
+                }
             } else if (dx) {
                 note(o.d.in0, i, o.acc_in[0], 0);
-                if (!rec)
+                if (!rec) {
+                    DC_TRY(gemm_mark(m, true, gemm_flop(o.geom), s));
                     DC_TRY(conv_dgrad(o.geom, o.dgrad, dy, P + o.w_off, o.acc_in[0], dx, m->scratch(), s));
+                    DC_TRY(gemm_mark(m, false, 0, s));
+                }
             }
             break;
         case DC_OP_BN: {
@@ -644,6 +689,7 @@ extern "C" void dc_model_destroy(dc_model *m) {
     if (m->ev_cs_done)
         (void)hipEventDestroy(m->ev_cs_done);
     drop_graphs(m);
+    free_gemm_events(m);
     if (m->cap_s)
         (void)hipStreamDestroy(m->cap_s);
     if (m->pull_s)
@@ -731,6 +777,9 @@ extern "C" int dc_model_set_option(dc_model *m, int option, double value) {
         return DC_OK;
     case DC_OPT_GRAPHS:
         m->use_graphs = value != 0.0;
+        return DC_OK;
+    case DC_OPT_GEMM_TIMING:
+        m->gemm_timing = value != 0.0;
         return DC_OK;
     case DC_OPT_SGD_THREADS: {
         int t = (int)value;

@@ -119,6 +119,12 @@ struct dc_model {
     const float *g_x = nullptr;
     const int32_t *g_y = nullptr;
 
+    // DC_OPT_GEMM_TIMING: an event before and after every GEMM pass of a step
+    int gemm_timing = 0;
+    std::vector<hipEvent_t> gemm_ev;  // 2 per pass, grown on demand
+    std::vector<double> gemm_flop;    // algorithmic FLOPs of each timed pass
+    size_t gemm_n = 0;                // passes timed in the current step
+
     float *dparams() const { return reinterpret_cast<float *>(ws + off_params); }
     float *dgrads() const { return reinterpret_cast<float *>(ws + off_grads); }
     float *act(int t) const { return reinterpret_cast<float *>(ws + tensors[t].act); }
@@ -146,4 +152,9 @@ int run_backward_layer(dc_model *m, int l, const float *x, hipStream_t s, BwdRec
 int launch_forward_layer(dc_model *m, int l, const float *x, const int32_t *y, hipStream_t s);
 int launch_backward_layer(dc_model *m, int l, const float *x, hipStream_t s);
 void drop_graphs(dc_model *m);
+// DC_OPT_GEMM_TIMING: record the event opening (start = true) or closing a
+// GEMM pass of `flop` algorithmic FLOPs on stream s; a no-op when the option is
+// off or the layer is being captured into a graph.
+int gemm_mark(dc_model *m, bool start, double flop, hipStream_t s);
+void free_gemm_events(dc_model *m);
 } // namespace dc

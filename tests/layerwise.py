@@ -218,15 +218,44 @@ def check_ops(name, net, y, params, res):
     return worst
 
 
+KIND_NAME = {D.DC_OP_CONV: "conv", D.DC_OP_FC: "fc", D.DC_OP_BN: "bn", D.DC_OP_RELU: "relu",
+             D.DC_OP_MAXPOOL: "maxpool", D.DC_OP_GAP: "gap", D.DC_OP_ADD: "add", D.DC_OP_CONCAT: "concat",
+             D.DC_OP_AVGPOOL: "avgpool"}
+
+
+def op_map(ops, net):
+    """Product op index -> oracle op index.  The two sides describe each network
+    separately, in the same order, except that the product nests a concatenation of
+    more than four parts (its inner concatenation maps to None)."""
+    tmap, parts, out = {0: 0}, {}, {}
+    j = 0
+    for i, o in enumerate(ops):
+        ins = []
+        for tid in [o[2]] + ([o[3]] if o[0] in (D.DC_OP_ADD, D.DC_OP_CONCAT) else []) + \
+                [x for x in (o[10], o[11]) if o[0] == D.DC_OP_CONCAT and x >= 0]:
+            ins += parts[tid] if tid in parts else [tmap[tid]]
+        oo = net.ops[j]
+        o_ins = [oo["in"]] + ([oo["other"]] if oo["op"] == "add" else []) + list(oo.get("others", []))
+        if KIND_NAME[o[0]] == oo["op"] and ins == o_ins:
+            out[i], tmap[i + 1] = j, j + 1
+            j += 1
+        else:
+            assert o[0] == D.DC_OP_CONCAT and oo["op"] == "concat" and ins == o_ins[:len(ins)], (i, j)
+            out[i], parts[i + 1] = None, ins
+    assert j == len(net.ops)
+    return out
+
+
 def _check_folds(name, net, t, cache, g, prm, weight, check, worst, s):
     """The launches that carry a ReLU's backward in a model, on the oracle's tensors.
     A folded ReLU's output has one reader, so its gradient g[r + 1] is that reader's
     term alone, and the expected result is the ReLU's mask applied to it."""
     ops, hwc, classes = PN.build(name)
     sched = D.backward_schedule(ops, net.batch, hwc, classes)
-    folds = sorted({(e["origin_op"], e["exec_op"]) for e in sched
-                    if net.ops[e["origin_op"]]["op"] == "relu" and e["exec_op"] != e["origin_op"]})
-    assert folds, name
+    omap = op_map(ops, net)
+    folds = sorted({(omap[e["origin_op"]], omap[e["exec_op"]]) for e in sched
+                    if ops[e["origin_op"]][0] == D.DC_OP_RELU and e["exec_op"] != e["origin_op"]})
+    assert folds and all(r is not None and j is not None for r, j in folds), (name, folds)
     for r, j in folds:
         r_in = net.ops[r]["in"]
         mask = OC.relu_mask(t[r_in])

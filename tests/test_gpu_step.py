@@ -536,3 +536,37 @@ def test_degenerate_models():
         assert rel_err(g, g_ref) <= 1e-3
         assert rel_err(p_new, p_ref) <= 1e-3
         model.close()
+
+
+def test_gemm_timing_counts_every_pass():
+    """DC_OPT_GEMM_TIMING: every conv / FC pass of the step is timed (forward, filter gradient,
+    and data gradient unless the op reads the input batch), with its algorithmic FLOPs; the
+    events change no number."""
+    model, onet, xd, yd, x, y, params = setup_model("resnet18", 4, seed=9)
+    plan = plans_for(model.L, seed=3)["random"]
+    st0 = model.step(xd, yd, plan, UNPACED)
+    p0, g0 = model.ps_read()
+    assert st0["n_gemm"] == 0 and st0["t_gemm_ns"] == 0
+    n_exp, flop_exp = 0, 0.0
+    for i, op in enumerate(onet.ops):
+        if op["op"] in ("conv", "fc"):
+            n, P, Q, K = onet.shapes[i + 1]
+            _, h, w, c = onet.shapes[op["in"]]
+            mac = n * P * Q * K * (op["r"] * op["s"] * c if op["op"] == "conv" else h * w * c)
+            passes = 2 if op["in"] == 0 else 3
+            n_exp += passes
+            flop_exp += passes * 2.0 * mac
+    model.set_option(D.DC_OPT_GEMM_TIMING, 1)
+    for _ in range(2):
+        model.ps_write(params)
+        st = model.step(xd, yd, plan, UNPACED)
+        p1, g1 = model.ps_read()
+        assert st["n_gemm"] == n_exp and st["gemm_flop"] == flop_exp
+        assert 0 < st["t_gemm_ns"] < st["t_iter_ns"]
+        assert st["loss"] == st0["loss"]
+        np.testing.assert_array_equal(g1, g0)
+        np.testing.assert_array_equal(p1, p0)
+    # a profile in between neither times passes nor disturbs the next step's count
+    model.profile(xd, yd, UNPACED, reps=1)
+    model.ps_write(params)
+    assert model.step(xd, yd, plan, UNPACED)["n_gemm"] == n_exp
