@@ -37,6 +37,23 @@ size_t dc_conv2d_workspace_bytes(const dc_conv_shape *sh);
 int dc_conv2d_forward(const dc_conv_shape *sh, const float *x, const float *w, const float *bias,
                       int relu, float *y, void *ws, size_t ws_bytes, void *stream);
 
+/* For callers that cannot allocate (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc): dc_conv2d_forward with no
+ * workspace argument.  Its scratch (split-K partial sums, the channel-padded
+ * copies of a C % 4 != 0 input) lives in a static device array of 64 MiB
+ * (67,108,864 bytes) that each device holds until the process ends.  The call
+ * allocates nothing (no hipMalloc, hipFree or allocating library routine) and
+ * gives the same result as dc_conv2d_forward under the same launch plan.  A
+ * shape whose forward pass needs more scratch than that (at most
+ * dc_conv2d_workspace_bytes) is refused with DC_EINVAL before anything is
+ * launched.  Every call on one device shares its array and leaves its own
+ * contents there: calls that overlap on a device (other streams, other host
+ * threads) race; order them on one stream or synchronise between them.  The
+ * first call on a device looks up that device's array address
+ * (hipGetSymbolAddress) with the device current. */
+int dc_conv2d_forward_noalloc(const dc_conv_shape *sh, const float *x, const float *w, const float *bias,
+                              int relu, float *y, void *stream);
+
 /* dx[n,h,w,c] (+)= sum over the (r, s, k) that reach (h, w) of dy[n,p,q,k] * w[k,r,s,c];
  * strided convolutions are split into stride^2 phase GEMMs with only the taps that hit. */
 int dc_conv2d_backward_data(const dc_conv_shape *sh, const float *dy, const float *w,

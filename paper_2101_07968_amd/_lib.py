@@ -120,6 +120,7 @@ _SIGS = {
     "dc_conv2d_set_plan": (ctypes.c_int, [_P(ConvShape), ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int]),
     "dc_conv2d_forward": (ctypes.c_int, [_P(ConvShape), c_vp, c_vp, c_vp, ctypes.c_int, c_vp, c_vp, c_sz, c_vp]),
     "dc_conv2d_backward_data": (ctypes.c_int, [_P(ConvShape), c_vp, c_vp, ctypes.c_int, c_vp, c_vp, c_sz, c_vp]),
+    "dc_conv2d_forward_noalloc": (ctypes.c_int, [_P(ConvShape), c_vp, c_vp, c_vp, ctypes.c_int, c_vp, c_vp]),
     "dc_conv2d_backward_data_relu": (ctypes.c_int, [_P(ConvShape), c_vp, c_vp, c_vp, ctypes.c_int, c_vp, c_vp,
                                                     c_sz, c_vp]),
     "dc_conv2d_backward_filter": (ctypes.c_int, [_P(ConvShape), c_vp, c_vp, c_vp, c_vp, c_vp, c_sz, c_vp]),

@@ -5,6 +5,7 @@
 #include <algorithm>
 #include <cstdarg>
 #include <cstdio>
+#include <mutex>
 #include <vector>
 
 namespace dc {
@@ -196,6 +197,60 @@ extern "C" int dc_conv2d_forward(const dc_conv_shape *sh, const float *x, const 
         return fail(DC_EINVAL, "NULL tensor");
     GemmPlan pl = plan_gemm(g, PASS_FWD);
     DC_TRY(need_ws(pl.ws_bytes, ws, ws_bytes));
+    return conv_forward(g, pl, x, w, bias, relu, y, ws, static_cast<hipStream_t>(stream));
+}
+
+// ---------------------------------------------------------------- forward conv without allocation
+//
+// dc_conv2d_forward_noalloc keeps the pass's scratch (split-K partial sums,
+// channel-padded operand copies) in this file-scope device array instead of
+// a caller workspace.  Each device holds its own copy for the life of the
+// process.  In host code `noalloc_scratch` only names the array: its device
+// address comes from hipGetSymbolAddress, taken once per device (with that
+// device current) at the first call there, and only that address is handed
+// to kernels.
+namespace {
+constexpr size_t NOALLOC_SCRATCH_BYTES = size_t(64) << 20;
+constexpr int NOALLOC_MAX_DEVICES = 64;
+static __device__ __align__(256) unsigned char noalloc_scratch[NOALLOC_SCRATCH_BYTES];
+std::mutex g_noalloc_mu;
+void *g_noalloc_ptr[NOALLOC_MAX_DEVICES] = {};
+
+int noalloc_scratch_ptr(void **out) {
+    int dev = -1;
+    DC_HIP(hipGetDevice(&dev));
+    if (dev < 0 || dev >= NOALLOC_MAX_DEVICES)
+        return fail(DC_EINVAL, "device %d is beyond the %d devices the static scratch serves", dev,
+                    NOALLOC_MAX_DEVICES);
+    std::lock_guard<std::mutex> lock(g_noalloc_mu);
+    if (!g_noalloc_ptr[dev]) {
+        void *p = nullptr;
+        DC_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(noalloc_scratch)));
+        if (!p)
+            return fail(DC_EHIP, "hipGetSymbolAddress gave no address for the static scratch");
+        g_noalloc_ptr[dev] = p;
+    }
+    *out = g_noalloc_ptr[dev];
+    return DC_OK;
+}
+} // namespace
+
+extern "C" int dc_conv2d_forward_noalloc(const dc_conv_shape *sh, const float *x, const float *w, const float *bias,
+                                         int relu, float *y, void *stream) {
+    clear_error();
+    ConvGeom g;
+    DC_TRY(conv_setup(sh, &g));
+    if (g.N == 0)
+        return DC_OK;
+    if (!x || !w || !y)
+        return fail(DC_EINVAL, "NULL tensor");
+    GemmPlan pl = plan_gemm(g, PASS_FWD);
+    if (pl.ws_bytes > NOALLOC_SCRATCH_BYTES)
+        return fail(DC_EINVAL, "this shape's forward pass needs %zu bytes of scratch; the static scratch holds %zu",
+                    pl.ws_bytes, NOALLOC_SCRATCH_BYTES);
+    void *ws = nullptr;
+    if (pl.ws_bytes > 0)
+        DC_TRY(noalloc_scratch_ptr(&ws));
     return conv_forward(g, pl, x, w, bias, relu, y, ws, static_cast<hipStream_t>(stream));
 }
 

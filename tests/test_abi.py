@@ -196,3 +196,14 @@ def test_ibatch_hand_worked_cases_through_abi():
         z = [0] * len(b["bc"])
         plan = D.dc_plan_ibatch(D.Profile(z, z, b["bc"], b["gt"], b["dt"]))
         assert plan.decisions()[1] == b["g"] and plan.t_bwd_ns == b["T"], b["name"]
+
+
+def test_noalloc_forward_refuses_shapes_beyond_its_scratch():
+    """dc_conv2d_forward_noalloc checks the plan's scratch against its 64 MiB static array
+    on the host, before any HIP call: a 128 x 224 x 224 x 3 input (a 103 MB channel-padded
+    copy) is refused.  The pointers are never dereferenced on that path."""
+    sh = D.ConvShape(128, 224, 224, 3, 64, 3, 3, 1, 1, 1)
+    fake = 1 << 20
+    st = D.lib().dc_conv2d_forward_noalloc(ctypes.byref(sh), fake, fake, None, 0, fake, None)
+    assert st == D.DC_EINVAL
+    assert b"static scratch" in D.lib().dc_last_error()
