@@ -78,8 +78,11 @@ int dc_conv2d_backward_filter(const dc_conv_shape *sh, const float *x, const flo
  * gradient, 2 filter gradient).  out[0..7] = workgroup tile M, tile N, split-K
  * factor, GEMM M, GEMM N, GEMM K, stride phases, and where the plan came from
  * (0 the occupancy cost model, 1 the library's table of measured plans, 2 a
- * plan pinned with dc_conv2d_set_plan).  out holds at least 8 int32.  Host
- * only; for inspection and tuning. */
+ * plan pinned with dc_conv2d_set_plan, 3 the weight-streaming FC kernel, which
+ * takes the data gradient of an FC shape (h = w = r = s = 1) of at most 32
+ * rows, c % 4 == 0 and at least 4,000,000 weights unless a plan is pinned; its
+ * tiles read as 0 and the split as its reduction splits).  out holds at least 8 int32.  Host only; for inspection and
+ * tuning. */
 int dc_conv2d_plan_info(const dc_conv_shape *sh, int pass, int32_t *out);
 
 /* Every plan the pass can be launched with for this shape, as (tile M, tile N,

@@ -149,7 +149,8 @@ extern "C" int dc_conv2d_plan_info(const dc_conv_shape *sh, int pass, int32_t *o
     if (pass < 0 || pass > 2 || !out)
         return fail(DC_EINVAL, "pass must be 0, 1 or 2 and out non-NULL");
     GemmPlan pl = plan_gemm(g, pass);
-    const int32_t v[8] = {pl.mt, pl.nt, pl.splits, pl.M, pl.Ng, pl.Kg, pl.phases, pl.source};
+    const int32_t v[8] = {pl.fc ? 0 : pl.mt, pl.fc ? 0 : pl.nt, pl.fc ? pl.fc_splits : pl.splits, pl.M, pl.Ng, pl.Kg,
+                          pl.phases, pl.source};
     for (int i = 0; i < 8; ++i)
         out[i] = v[i];
     return DC_OK;

@@ -53,10 +53,16 @@ struct GemmPlan {
     size_t pad_x_off;     // workspace offsets of the padded x and of the padded w (FWD) or dw (WGRAD)
     size_t pad_w_off;
     size_t ws_bytes;      // split-K partial sums, then the padded copies
-    int source;           // PLAN_MODEL, PLAN_TABLE or PLAN_PINNED
+    int source;           // PLAN_MODEL, PLAN_TABLE, PLAN_PINNED or PLAN_FC
+    // PLAN_FC: the pass (an FC data gradient) runs on the weight-streaming
+    // kernel (fc.hip) with fc_splits reduction splits of fc_chunk rows each;
+    // the implicit-GEMM fields above still hold the plan used when an operand
+    // is not 16-byte aligned, and ws_bytes covers both.
+    bool fc;
+    int fc_splits, fc_chunk;
 };
 
-enum PlanSource { PLAN_MODEL = 0, PLAN_TABLE = 1, PLAN_PINNED = 2 };
+enum PlanSource { PLAN_MODEL = 0, PLAN_TABLE = 1, PLAN_PINNED = 2, PLAN_FC = 3 };
 
 bool conv_geom_from_shape(const dc_conv_shape &sh, ConvGeom *g);
 GemmPlan plan_gemm(const ConvGeom &g, int pass);
@@ -73,6 +79,14 @@ int lookup_plan(const ConvGeom &g, int pass, int out[3]);
 // mt > 0 pins (mt, nt, splits); mt == 0 removes the pin; mt == -1 pins the
 // cost model's choice (the built-in table is then skipped for this shape).
 void pin_plan(const ConvGeom &g, int pass, int mt, int nt, int splits);
+
+// The data gradient of a large FC layer with at most 32 rows (fc.hip):
+// whether the weight-streaming kernel takes the pass, its split of the
+// reduction and scratch, and the pass (relu_mask as for conv_dgrad).
+bool fc_streaming(const ConvGeom &g, int pass);
+void fc_plan(const ConvGeom &g, int splits_out[1], int *chunk, size_t *ws_bytes);
+int fc_dgrad(const ConvGeom &g, int splits, int chunk, const float *dy, const float *w, int accumulate, float *dx,
+             void *ws, hipStream_t s, const float *relu_mask);
 
 int conv_forward(const ConvGeom &g, const GemmPlan &pl, const float *x, const float *w,
                  const float *bias, int relu, float *y, void *ws, hipStream_t s);

@@ -1,0 +1,212 @@
+// The data gradient of a large FC layer with few rows: a weight-streaming
+// GEMM on gfx950 fp32 matrix cores.
+//
+// For an FC layer with weights W [O][I] and M <= 32 rows (the batch), the
+// backward compute mini-procedure's data gradient (Sec. III-A)
+//
+//   dX[m][i] = sum_o dY[m][o] W[o][i]
+//
+// moves the O x I weights once and little else: 2 M flops per 4 weight
+// bytes, near the balance point of HBM and the fp32 matrix cores.  This
+// kernel streams W straight from HBM into registers, in rows of 512
+// contiguous bytes per half-wave, with no LDS staging and no barriers:
+//
+// * v_mfma_f32_32x32x2f32 takes, per lane l, one element of a 32 x 2 block
+//   of A (row l % 32, k = l / 32) and of a 2 x 32 block of B (k = l / 32,
+//   column l % 32).
+// * Lane (j = l % 32, h = l / 32) holds dY[m = j][o + 4h .. +3] and
+//   W[o + 4h + u][i + 4j .. +3] for u = 0..3.  Product (u, e) takes element u
+//   of the dY quad and element e of the u-th W quad, so it adds row pair
+//   (o + u, o + 4 + u) into the column set {i + 4j + e}: four accumulators
+//   cover 128 contiguous columns, written back as float4.
+// * Three register buffers form a ring, so the loads of the next two steps
+//   are in flight while a step multiplies; operands are read with raw buffer
+//   loads whose out-of-range offsets read as zero, which masks the ragged
+//   edges without a branch around a load.
+//
+// The reduction over o is split over waves: fixed-slot partial sums, then a
+// fixed-order reduction that applies a folded ReLU's mask and the
+// accumulate flag, so results are deterministic.  The implicit GEMM keeps
+// the other FC passes, which it runs faster.
+#include "dc_internal.h"
+
+#include <algorithm>
+#include <climits>
+
+namespace dc {
+namespace {
+
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+constexpr int WAVES = 4;              // waves per workgroup
+constexpr int TARGET_WAVES = 2048;    // 2 per SIMD on 256 CUs, each with two steps of loads in flight
+constexpr unsigned OOB = 0x80000000u; // a byte offset that reads as zero
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const float *p, int64_t elems) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<float *>(p), (short)0, (int)(4 * elems), 0x00020000);
+}
+
+__device__ __forceinline__ float4 ld4_sel(__amdgpu_buffer_rsrc_t r, int64_t elem, bool ok) {
+    return __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(r, ok ? (unsigned)(4 * elem) : OOB, 0, 0));
+}
+
+__device__ __forceinline__ float ld_sel(__amdgpu_buffer_rsrc_t r, int64_t elem, bool ok) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, ok ? (unsigned)(4 * elem) : OOB, 0, 0));
+}
+
+__device__ __forceinline__ float el(const float4 &v, int e) {
+    return e == 0 ? v.x : (e == 1 ? v.y : (e == 2 ? v.z : v.w));
+}
+
+// One wave: columns i0 .. i0+127 for rows 0 .. M-1 (M <= 32), over the o
+// range of split `sp` (ochunk rows, a multiple of 24); partial[sp][m][i].
+__global__ __launch_bounds__(64 * WAVES) void fc_dgrad_kernel(const float *__restrict__ dY,
+                                                              const float *__restrict__ W,
+                                                              float *__restrict__ partial, int M, int I, int O,
+                                                              int tiles_i, int splits, int ochunk) {
+    const int wave = blockIdx.x * WAVES + (threadIdx.x >> 6);
+    if (wave >= tiles_i * splits)
+        return;
+    const int lane = threadIdx.x & 63, j = lane & 31, h = lane >> 5;
+    const int tile = wave % tiles_i, sp = wave / tiles_i;
+    const int i = tile * 128 + 4 * j;
+    const bool iok = i < I;
+    const int ob = sp * ochunk, oe = min(O, ob + ochunk);
+    f32x16 acc[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+        acc[e] = f32x16{};
+    const __amdgpu_buffer_rsrc_t rw = rsrc(W, (int64_t)O * I), ra = rsrc(dY, (int64_t)M * O);
+    const bool aok = j < M;
+    const int64_t arow = (int64_t)j * O;
+    // dY rows are read as float4 only when O % 4 == 0; else element by element
+    const bool a4 = O % 4 == 0;
+    struct Buf {
+        float4 w[4], a;
+    };
+    auto load = [&](Buf &b, int o0) {
+        const int oa = o0 + 4 * h;
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+            b.w[u] = ld4_sel(rw, (int64_t)(oa + u) * I + i, iok && oa + u < oe);
+        if (a4) {
+            b.a = ld4_sel(ra, arow + oa, aok && oa < oe);
+        } else {
+            float t[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+                t[u] = ld_sel(ra, arow + oa + u, aok && oa + u < oe);
+            b.a = make_float4(t[0], t[1], t[2], t[3]);
+        }
+    };
+    auto step = [&](const Buf &b) {
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                acc[e] = __builtin_amdgcn_mfma_f32_32x32x2f32(el(b.a, u), el(b.w[u], e), acc[e], 0, 0, 0);
+    };
+    // steps past oe load zeros and add nothing
+    Buf b0, b1, b2;
+    load(b0, ob);
+    load(b1, ob + 8);
+    for (int o0 = ob; o0 < oe; o0 += 24) {
+        load(b2, o0 + 16);
+        step(b0);
+        load(b0, o0 + 24);
+        step(b1);
+        load(b1, o0 + 32);
+        step(b2);
+    }
+    if (!iok)
+        return;
+    // element v of lane l is row 8*(v/4) + 4*(l/32) + v%4 of a 32 x 32 block
+    float *dst = partial + (size_t)sp * M * I;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+        const int m = 8 * (v >> 2) + 4 * h + (v & 3);
+        if (m < M)
+            *reinterpret_cast<float4 *>(dst + (size_t)m * I + i) =
+                make_float4(acc[0][v], acc[1][v], acc[2][v], acc[3][v]);
+    }
+}
+
+// dX[m][i] (+)= (mask?) sum over splits in order of partial[s][m][i]; a
+// float4 of columns per thread (I % 4 == 0).
+__global__ __launch_bounds__(256) void fc_dgrad_reduce_kernel(const float4 *__restrict__ partial, int splits,
+                                                              int64_t n4, const float4 *__restrict__ relu_mask,
+                                                              int accumulate, float4 *__restrict__ dX) {
+    for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < n4;
+         idx += (int64_t)gridDim.x * blockDim.x) {
+        float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+        for (int s = 0; s < splits; ++s) {
+            const float4 p = partial[(size_t)s * n4 + idx];
+            v.x += p.x; v.y += p.y; v.z += p.z; v.w += p.w;
+        }
+        if (relu_mask) {
+            const float4 r = relu_mask[idx];
+            if (!(r.x > 0.f)) v.x = 0.f;
+            if (!(r.y > 0.f)) v.y = 0.f;
+            if (!(r.z > 0.f)) v.z = 0.f;
+            if (!(r.w > 0.f)) v.w = 0.f;
+        }
+        if (accumulate) {
+            const float4 d = dX[idx];
+            v.x += d.x; v.y += d.y; v.z += d.z; v.w += d.w;
+        }
+        dX[idx] = v;
+    }
+}
+
+} // namespace
+
+bool fc_streaming(const ConvGeom &g, int pass) {
+    const bool fc = g.H == 1 && g.W == 1 && g.R == 1 && g.S == 1 && g.st == 1 && g.pad == 0 && g.pad_w == 0;
+    // Measured on MI355X against the implicit GEMM's plans: the streaming data
+    // gradient wins from about 4 M weights at 32 rows (VGG-16's 25088 -> 4096:
+    // 106 against 133 us); below that, or with more rows, it does not.
+    if (pass != PASS_DGRAD || !fc || g.N < 1 || g.N > 32 || g.C % 4 != 0 || (int64_t)g.K * g.C < 4000000)
+        return false;
+    // every operand is read through 32-bit byte offsets, offsets from 2^31 up
+    // reading as zero: each below 2^31 bytes (with the ring's 32 rows past the
+    // end), as are the partial sums
+    const int64_t lim = (int64_t)1 << 31;
+    return 4 * ((int64_t)g.K + 32) * g.C < lim && 4 * (int64_t)g.N * std::max(g.C, g.K) * 64 < lim;
+}
+
+// Splits of the reduction over o: about TARGET_WAVES waves, in chunks of 24
+// rows (the ring's three steps), while the partial sums (splits x M x I) stay
+// within a quarter of the weight bytes.
+void fc_plan(const ConvGeom &g, int splits_out[1], int *chunk, size_t *ws_bytes) {
+    const int64_t M = g.N, I = g.C, O = g.K;
+    const int64_t tiles = (I + 127) / 128;
+    const int64_t steps = (O + 23) / 24;
+    int64_t s = std::max<int64_t>(1, (TARGET_WAVES + tiles - 1) / tiles);
+    s = std::min<int64_t>(s, std::max<int64_t>(1, O / (4 * M)));
+    s = std::min<int64_t>(s, steps);
+    const int64_t per = (steps + s - 1) / s;
+    *chunk = (int)(per * 24);
+    splits_out[0] = (int)((steps + per - 1) / per);
+    *ws_bytes = (size_t)splits_out[0] * M * I * sizeof(float);
+}
+
+int fc_dgrad(const ConvGeom &g, int splits, int chunk, const float *dy, const float *w, int accumulate, float *dx,
+             void *ws, hipStream_t s, const float *relu_mask) {
+    const int M = g.N, I = g.C, O = g.K;
+    if (!ws)
+        return fail(DC_EINVAL, "FC dgrad needs a workspace");
+    float *partial = static_cast<float *>(ws);
+    const int tiles = (I + 127) / 128;
+    const int grid = (int)(((int64_t)tiles * splits + WAVES - 1) / WAVES);
+    hipLaunchKernelGGL(fc_dgrad_kernel, dim3(grid), dim3(64 * WAVES), 0, s, dy, w, partial, M, I, O, tiles, splits,
+                       chunk);
+    DC_HIP(hipGetLastError());
+    const int64_t n4 = (int64_t)M * I / 4;
+    hipLaunchKernelGGL(fc_dgrad_reduce_kernel, dim3((int)std::min<int64_t>((n4 + 255) / 256, 4096)), dim3(256), 0,
+                       s, reinterpret_cast<const float4 *>(partial), splits, n4,
+                       reinterpret_cast<const float4 *>(relu_mask), accumulate, reinterpret_cast<float4 *>(dx));
+    DC_HIP(hipGetLastError());
+    return DC_OK;
+}
+
+} // namespace dc

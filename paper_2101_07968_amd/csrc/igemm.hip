@@ -1142,6 +1142,13 @@ GemmPlan plan_gemm(const ConvGeom &g, int pass) {
         pl = plan_core(gp, pass, nullptr);
         pl.source = PLAN_MODEL;
     }
+    if (src != PLAN_PINNED && src != -1 && fc_streaming(g, pass)) {
+        size_t fws = 0;
+        fc_plan(g, &pl.fc_splits, &pl.fc_chunk, &fws);
+        pl.fc = true;
+        pl.source = PLAN_FC;
+        pl.ws_bytes = std::max(pl.ws_bytes, fws);
+    }
     if (!pads)
         return pl;
     pl.cpad = gp.C;
@@ -1150,6 +1157,8 @@ GemmPlan plan_gemm(const ConvGeom &g, int pass) {
     pl.ws_bytes = pl.pad_w_off + round256((size_t)g.K * g.R * g.S * gp.C * sizeof(float));
     return pl;
 }
+
+static bool al16(const void *p) { return (uintptr_t)p % 16 == 0; }
 
 int conv_forward(const ConvGeom &g, const GemmPlan &pl, const float *x, const float *w,
                  const float *bias, int relu, float *y, void *ws, hipStream_t s) {
@@ -1172,6 +1181,8 @@ int conv_forward(const ConvGeom &g, const GemmPlan &pl, const float *x, const fl
 
 int conv_dgrad(const ConvGeom &g, const GemmPlan &pl, const float *dy, const float *w,
                int accumulate, float *dx, void *ws, hipStream_t s, const float *relu_mask) {
+    if (pl.fc && al16(dy) && al16(w) && al16(dx) && al16(ws) && al16(relu_mask))
+        return fc_dgrad(g, pl.fc_splits, pl.fc_chunk, dy, w, accumulate, dx, ws, s, relu_mask);
     Args a = make_args(g, pl);
     a.A = dy; a.B = w; a.out = dx; a.accumulate = accumulate; a.relu_mask = relu_mask;
     return run(g, pl, a, ws, s);

@@ -1,14 +1,13 @@
 """Summarise rocprofv3 CSV output into the short text reports kept under profiles/.
 
-  python -m paper_2101_07968_amd.profsum stats <kernel_trace.csv> <kernel_stats.csv> --passes-per-conv 4 \
+  python -m paper_2101_07968_amd.profsum stats <kernel_trace.csv> <kernel_stats.csv> --steps 10 --flops 2964.7 \
       --cmd "<command>" > profiles/igemm_<workload>_kernel_stats.md
   python -m paper_2101_07968_amd.profsum traffic <fetch counter_collection.csv> <write counter_collection.csv> \
       --workload vgg16 --batch 32 --cmd "<commands>" > profiles/igemm_<workload>_b<batch>_traffic.txt
 
-stats: per-kernel totals from --stats, and the implicit-GEMM window that bench.py
-times live (every igemm / split-K / channel-padding dispatch after the last pacing kernel,
-i.e. the per-pass timing loop: 1 warm-up + 3 timed launches per pass) reduced
-to one iteration's worth, for comparison with the bench's conv_ms_per_step.
+stats: per-kernel totals from --stats, and the conv/FC GEMM passes of bench.py's
+timed DP steps (the dispatches between the two relu_fwd_kernel marks it launches
+around them), per step and per pass, for comparison with the bench's roofline.
 
 traffic: FETCH_SIZE / WRITE_SIZE (KiB per dispatch) of the igemm dispatches of a
 `bench.py --kernels-only` run, scaled by what the same counters read for the
@@ -34,7 +33,7 @@ import re
 HERE = os.path.dirname(os.path.abspath(__file__))
 
 
-GEMM_SOURCES = ("igemm.hip", "plan_table.cpp", "plan_table.inc")
+GEMM_SOURCES = ("igemm.hip", "fc.hip", "plan_table.cpp", "plan_table.inc")
 
 
 def gemm_sources_sha256():
@@ -54,7 +53,13 @@ def short(name):
 
 def is_gemm(name):
     """A dispatch of a conv/FC pass: the GEMM, its split-K reduction or its channel padding."""
-    return any(k in name for k in ("igemm_kernel", "splitk_reduce_kernel", "pad_channels_kernel"))
+    return any(k in name for k in ("igemm_kernel", "splitk_reduce_kernel", "pad_channels_kernel",
+                                   "fc_dgrad_kernel", "fc_dgrad_reduce_kernel"))
+
+
+def is_pass(name):
+    """The one dispatch of each conv/FC pass that does its multiply-adds."""
+    return "igemm_kernel" in name or ("fc_dgrad_kernel" in name and "reduce" not in name)
 
 
 def cmd_stats(a):
@@ -70,17 +75,25 @@ def cmd_stats(a):
             f"{gemm_total / 1e6:.2f} ms."]
     trace = list(csv.DictReader(open(a.trace)))
     trace.sort(key=lambda r: int(r["Start_Timestamp"]))
-    last_pace = max((i for i, r in enumerate(trace) if "pace_" in r["Kernel_Name"]), default=-1)
-    win = [r for r in trace[last_pace + 1:] if is_gemm(r["Kernel_Name"])]
+    marks = [i for i, r in enumerate(trace) if "relu_fwd_kernel" in r["Kernel_Name"]]
+    if len(marks) < 2:
+        raise SystemExit("no pair of relu_fwd_kernel marks around the timed steps in the trace")
+    win = [r for r in trace[marks[0] + 1:marks[1]] if is_gemm(r["Kernel_Name"])]
     dur = sum(int(r["End_Timestamp"]) - int(r["Start_Timestamp"]) for r in win)
-    per_iter = dur / a.passes_per_conv / 1e6
-    out += ["", "Roofline window (the per-pass timing loop of bench.py, after the last pacing kernel):",
-            f"{len(win)} conv-pass dispatches, {dur / 1e6:.2f} ms in all, {per_iter:.3f} ms per iteration "
-            f"({a.passes_per_conv} launches per pass).",
-            f"Mean duration per launch: {dur / max(len(win), 1) / 1e3:.1f} us."]
+    passes = sum(1 for r in win if is_pass(r["Kernel_Name"]))
+    gemm_only = sum(int(r["End_Timestamp"]) - int(r["Start_Timestamp"]) for r in win if "igemm_kernel" in r["Kernel_Name"])
+    n_igemm = sum(1 for r in win if "igemm_kernel" in r["Kernel_Name"])
+    per_step = dur / a.steps / 1e6
+    out += ["", "Timed steps (the dispatches between the two relu_fwd_kernel marks bench.py places around them):",
+            f"{passes} conv/FC passes ({passes // a.steps} per step), {len(win)} dispatches (implicit GEMM, "
+            f"split-K reduce, channel padding, FC data-gradient kernel), {dur / 1e6:.2f} ms in all, "
+            f"{per_step:.3f} ms per step.",
+            f"Mean duration per pass: {dur / max(passes, 1) / 1e3:.1f} us; igemm_kernel alone: "
+            f"{n_igemm} dispatches, mean {gemm_only / max(n_igemm, 1) / 1e3:.1f} us."]
     if a.flops:
-        out.append(f"Algorithmic GEMM work per iteration {a.flops:.1f} GFLOP -> "
-                   f"{a.flops / per_iter:.1f} TFLOP/s from these durations.")
+        out.append(f"Algorithmic GEMM work per step {a.flops:.1f} GFLOP -> "
+                   f"{a.flops / per_step:.1f} TFLOP/s from these durations "
+                   f"({100 * a.flops / per_step / 157.3:.1f}% of the 157.3 TFLOP/s fp32 matrix peak).")
     print("\n".join(out))
 
 
@@ -112,8 +125,8 @@ def cmd_traffic(a):
     cal_w = [float(r["Counter_Value"]) for r in write if "copy_grad_kernel" in r["Kernel_Name"]]
     known_kib = a.cal_bytes / 1024.0
     sf, sw = known_kib / cal_f[0], known_kib / cal_w[0]
-    gf = [float(r["Counter_Value"]) for r in fetch if "igemm_kernel" in r["Kernel_Name"]]
-    gw = [float(r["Counter_Value"]) for r in write if "igemm_kernel" in r["Kernel_Name"]]
+    gf = [float(r["Counter_Value"]) for r in fetch if is_pass(r["Kernel_Name"])]
+    gw = [float(r["Counter_Value"]) for r in write if is_pass(r["Kernel_Name"])]
     n = len(gf)
     hbm = (sum(gf) * sf + sum(gw) * sw) * 1024.0 / n
     ops, hwc, _ = PN.build(a.workload)
@@ -123,7 +136,8 @@ def cmd_traffic(a):
     print(f"# HBM traffic of the implicit-GEMM kernel, {a.workload} batch {a.batch}")
     print(f"# commands: {a.cmd}")
     print(f"# calibration: {a.cal_bytes} B copy read as FETCH_SIZE {cal_f[0]:.1f} KiB, WRITE_SIZE {cal_w[0]:.1f} KiB")
-    print(f"# igemm dispatches: {n} ({len(passes)} conv/FC passes, each launched twice)")
+    print(f"# pass dispatches (igemm_kernel, and fc_dgrad_kernel for the FC data gradients it takes): {n} "
+          f"({len(passes)} conv/FC passes, each launched twice)")
     print(f"# raw FETCH_SIZE {sum(gf):.0f} KiB, WRITE_SIZE {sum(gw):.0f} KiB over those dispatches")
     print(f"fetch_scale={sf:.4f}")
     print(f"write_scale={sw:.4f}")
@@ -228,7 +242,7 @@ def main():
     s = sub.add_parser("stats")
     s.add_argument("trace")
     s.add_argument("stats")
-    s.add_argument("--passes-per-conv", type=int, default=4)
+    s.add_argument("--steps", type=int, default=10, help="timed DP steps between the two marks")
     s.add_argument("--flops", type=float, default=0.0, help="GFLOP of one iteration's GEMM passes")
     s.add_argument("--top", type=int, default=25)
     s.add_argument("--cmd", default="")

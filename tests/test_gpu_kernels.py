@@ -131,6 +131,45 @@ def test_conv_small(shape, variant):
     assert rel_err(db, db_ref) <= tol(n * P * Q)
 
 
+FC_SHAPES = [(1, 4000, 1003), (5, 1004, 3999), (31, 2052, 2001), (32, 4096, 1000), (32, 25088, 4096),
+             (33, 4096, 1000), (32, 3996, 1000), (4, 1024, 64), (3, 300, 130)]
+
+
+@pytest.mark.parametrize("n,fin,fout", FC_SHAPES, ids=[f"{n}x{i}->{o}" for n, i, o in FC_SHAPES])
+def test_fc_streaming(n, fin, fout):
+    """The data gradient of an FC layer of at most 32 rows and at least 4 M weights runs on
+    the weight-streaming kernel (plan source 3), other FC passes on the implicit GEMM;
+    ragged rows, features and outputs, bias + ReLU, an accumulating data gradient and the
+    ReLU-masked data gradient, against the oracle."""
+    shape = (n, 1, 1, fin, fout, 1, 1, 1, 0, 0)
+    src = [D.conv_plan_info(shape, p)[7] for p in range(3)]
+    streams = n <= 32 and fin % 4 == 0 and fin * fout >= 4000000
+    assert (src[1] == 3) == streams and src[0] != 3 and src[2] != 3, src
+    seed = n * 1000 + fin + fout
+    x = synth.random_tensor(seed, (n, 1, 1, fin))
+    wt = synth.random_tensor(seed + 1, (fout, 1, 1, fin), scale=math.sqrt(2.0 / fin))
+    b = synth.random_tensor(seed + 2, (fout,))
+    dy = synth.random_tensor(seed + 3, (n, 1, 1, fout))
+    acc0 = synth.random_tensor(seed + 4, (n, 1, 1, fin))
+    y, dx, dw, db = run_conv(shape, x, wt, b, dy, 1, acc0)
+    assert rel_err(y, np.maximum(OC.conv2d_forward(x, wt, b, 1, 0), 0)) <= tol(fin)
+    dx_ref = OC.conv2d_backward_data(dy, wt, (1, 1), 1, 0)
+    assert rel_err(dx, dx_ref + acc0) <= tol(fout)
+    assert rel_err(dw, OC.conv2d_backward_filter(x, dy, (1, 1), 1, 0)) <= tol(n)
+    assert rel_err(db, dy.astype(np.float64).sum(axis=(0, 1, 2))) <= tol(n)
+    # the data gradient through a ReLU whose output is x (the model's folded launch)
+    sh = conv_shape(*shape)
+    ws_t, ws, wsb = scratch(D.lib().dc_conv2d_workspace_bytes(ctypes.byref(sh)))
+    relu_y = np.maximum(x, 0)
+    dxm = zeros((n, 1, 1, fin))
+    dyd, wd, yd = dev(dy), dev(wt), dev(relu_y)   # held: a freed tensor's memory is reused at once
+    D.call("dc_conv2d_backward_data_relu", ctypes.byref(sh), dyd.data_ptr(), wd.data_ptr(), yd.data_ptr(), 0,
+           dxm.data_ptr(), ws, wsb, stream())
+    exp = np.where(relu_y.astype(np.float32) > 0, dx_ref, 0.0)
+    assert rel_err(host(dxm), exp) <= tol(fout)
+    assert (host(dxm)[relu_y <= 0] == 0).all()
+
+
 PLAN_SHAPES = [
     (4, 14, 14, 64, 96, 3, 3, 1, 1, 1),    # K = 576: split-K up to 8 in forward and dgrad
     (3, 15, 15, 32, 48, 3, 3, 2, 1, 1),    # strided: four dgrad phases
