@@ -81,8 +81,11 @@ int dc_conv2d_backward_filter(const dc_conv_shape *sh, const float *x, const flo
  * plan pinned with dc_conv2d_set_plan, 3 the weight-streaming FC kernel, which
  * takes the data gradient of an FC shape (h = w = r = s = 1) of at most 32
  * rows, c % 4 == 0 and at least 4,000,000 weights unless a plan is pinned; its
- * tiles read as 0 and the split as its reduction splits).  out holds at least 8 int32.  Host only; for inspection and
- * tuning. */
+ * tiles read as 0 and the split as its reduction splits; 4 the direct kernels
+ * of the RGB input layer, which take the forward pass and filter gradient of
+ * c = 3, r = s = 3, k a multiple of 32 from 32 to 128 unless a plan is
+ * pinned; tiles 0, split 1).  out holds at least 8 int32.  Host only; for
+ * inspection and tuning. */
 int dc_conv2d_plan_info(const dc_conv_shape *sh, int pass, int32_t *out);
 
 /* Every plan the pass can be launched with for this shape, as (tile M, tile N,

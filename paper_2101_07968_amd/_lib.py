@@ -281,7 +281,8 @@ def dc_plan_eval(prof, p, g):
 def conv_plan_info(shape, pas):
     """(tile M, tile N, splits, GEMM M, GEMM N, GEMM K, phases, source) of one conv pass;
     source 0 = cost model, 1 = table of measured plans, 2 = pinned, 3 = the weight-streaming
-    FC data-gradient kernel (tiles 0, splits = its reduction splits)."""
+    FC data-gradient kernel (tiles 0, splits = its reduction splits), 4 = the direct kernels of
+    the RGB input layer (tiles 0, split 1)."""
     out = (c_i32 * 8)()
     sh = ConvShape(*shape)
     call("dc_conv2d_plan_info", ctypes.byref(sh), pas, out)

@@ -149,8 +149,9 @@ extern "C" int dc_conv2d_plan_info(const dc_conv_shape *sh, int pass, int32_t *o
     if (pass < 0 || pass > 2 || !out)
         return fail(DC_EINVAL, "pass must be 0, 1 or 2 and out non-NULL");
     GemmPlan pl = plan_gemm(g, pass);
-    const int32_t v[8] = {pl.fc ? 0 : pl.mt, pl.fc ? 0 : pl.nt, pl.fc ? pl.fc_splits : pl.splits, pl.M, pl.Ng, pl.Kg,
-                          pl.phases, pl.source};
+    const bool own = pl.fc || pl.direct; // kernels outside the implicit GEMM
+    const int32_t v[8] = {own ? 0 : pl.mt, own ? 0 : pl.nt, pl.fc ? pl.fc_splits : (pl.direct ? 1 : pl.splits),
+                          pl.M, pl.Ng, pl.Kg, pl.phases, pl.source};
     for (int i = 0; i < 8; ++i)
         out[i] = v[i];
     return DC_OK;
@@ -301,8 +302,9 @@ extern "C" int dc_conv2d_backward_filter(const dc_conv_shape *sh, const float *x
             DC_HIP(hipMemsetAsync(dbias, 0, sizeof(float) * g.K, s));
         return DC_OK;
     }
-    DC_TRY(conv_wgrad(g, pl, x, dy, dw, ws, s));
-    if (dbias)
+    bool bias_done = false;
+    DC_TRY(conv_wgrad(g, pl, x, dy, dw, ws, s, dbias, &bias_done));
+    if (dbias && !bias_done)
         DC_TRY(colsum((int64_t)g.N * g.P * g.Q, g.K, dy, dbias, ws, s));
     return DC_OK;
 }

@@ -60,9 +60,13 @@ struct GemmPlan {
     // is not 16-byte aligned, and ws_bytes covers both.
     bool fc;
     int fc_splits, fc_chunk;
+    // PLAN_DIRECT: a forward or filter-gradient pass of the RGB input layer
+    // runs on the direct kernels (conv3.hip); the fields above still hold the
+    // implicit-GEMM plan used when an operand is not 16-byte aligned.
+    bool direct;
 };
 
-enum PlanSource { PLAN_MODEL = 0, PLAN_TABLE = 1, PLAN_PINNED = 2, PLAN_FC = 3 };
+enum PlanSource { PLAN_MODEL = 0, PLAN_TABLE = 1, PLAN_PINNED = 2, PLAN_FC = 3, PLAN_DIRECT = 4 };
 
 bool conv_geom_from_shape(const dc_conv_shape &sh, ConvGeom *g);
 GemmPlan plan_gemm(const ConvGeom &g, int pass);
@@ -83,6 +87,14 @@ void pin_plan(const ConvGeom &g, int pass, int mt, int nt, int splits);
 // The data gradient of a large FC layer with at most 32 rows (fc.hip):
 // whether the weight-streaming kernel takes the pass, its split of the
 // reduction and scratch, and the pass (relu_mask as for conv_dgrad).
+// Direct kernels for the RGB input layer (C = 3, a 3 x 3 filter; conv3.hip):
+// forward pass and filter gradient, the latter with the bias gradient.
+bool conv3_direct(const ConvGeom &g, int pass);
+size_t conv3_ws_bytes(const ConvGeom &g, int pass);
+int conv3_forward(const ConvGeom &g, const float *x, const float *w, const float *bias, int relu, float *y,
+                  hipStream_t s);
+int conv3_wgrad(const ConvGeom &g, const float *x, const float *dy, float *dw, float *dbias, void *ws,
+                hipStream_t s);
 bool fc_streaming(const ConvGeom &g, int pass);
 void fc_plan(const ConvGeom &g, int splits_out[1], int *chunk, size_t *ws_bytes);
 int fc_dgrad(const ConvGeom &g, int splits, int chunk, const float *dy, const float *w, int accumulate, float *dx,
@@ -94,8 +106,11 @@ int conv_forward(const ConvGeom &g, const GemmPlan &pl, const float *x, const fl
 // dx (+)= (relu_mask > 0 ? dgrad : 0), laid out like dx.
 int conv_dgrad(const ConvGeom &g, const GemmPlan &pl, const float *dy, const float *w,
                int accumulate, float *dx, void *ws, hipStream_t s, const float *relu_mask = nullptr);
+// Filter gradient.  When the pass's kernel also forms the bias gradient (the
+// direct RGB-layer kernel, given bias_done), it writes dbias (if not NULL)
+// and sets *bias_done; otherwise the caller computes the bias gradient.
 int conv_wgrad(const ConvGeom &g, const GemmPlan &pl, const float *x, const float *dy, float *dw,
-               void *ws, hipStream_t s);
+               void *ws, hipStream_t s, float *dbias = nullptr, bool *bias_done = nullptr);
 
 // ---------------------------------------------------------------- elementwise and reductions
 size_t colsum_ws_bytes(int64_t rows, int c);

@@ -1149,6 +1149,11 @@ GemmPlan plan_gemm(const ConvGeom &g, int pass) {
         pl.source = PLAN_FC;
         pl.ws_bytes = std::max(pl.ws_bytes, fws);
     }
+    if (src != PLAN_PINNED && src != -1 && conv3_direct(g, pass)) {
+        pl.direct = true;
+        pl.source = PLAN_DIRECT;
+        pl.ws_bytes = std::max(pl.ws_bytes, conv3_ws_bytes(g, pass));
+    }
     if (!pads)
         return pl;
     pl.cpad = gp.C;
@@ -1162,6 +1167,8 @@ static bool al16(const void *p) { return (uintptr_t)p % 16 == 0; }
 
 int conv_forward(const ConvGeom &g, const GemmPlan &pl, const float *x, const float *w,
                  const float *bias, int relu, float *y, void *ws, hipStream_t s) {
+    if (pl.direct && al16(y))
+        return conv3_forward(g, x, w, bias, relu, y, s);
     if (pl.cpad) {
         if (!ws)
             return fail(DC_EINVAL, "conv forward needs %zu bytes of workspace", pl.ws_bytes);
@@ -1189,7 +1196,13 @@ int conv_dgrad(const ConvGeom &g, const GemmPlan &pl, const float *dy, const flo
 }
 
 int conv_wgrad(const ConvGeom &g, const GemmPlan &pl, const float *x, const float *dy, float *dw,
-               void *ws, hipStream_t s) {
+               void *ws, hipStream_t s, float *dbias, bool *bias_done) {
+    if (bias_done)
+        *bias_done = false;
+    if (pl.direct && ws && bias_done && al16(dy)) {
+        *bias_done = true;
+        return conv3_wgrad(g, x, dy, dw, dbias, ws, s);
+    }
     if (pl.cpad) {
         if (!ws)
             return fail(DC_EINVAL, "conv wgrad needs %zu bytes of workspace", pl.ws_bytes);

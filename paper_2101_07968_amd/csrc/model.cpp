@@ -403,9 +403,11 @@ int run_backward_layer(dc_model *m, int l, const float *x, hipStream_t s, BwdRec
         case DC_OP_FC:
             if (!rec) {
                 DC_TRY(gemm_mark(m, true, gemm_flop(o.geom), s));
-                DC_TRY(conv_wgrad(o.geom, o.wgrad, in, dy, G + o.w_off, m->scratch(), s));
+                bool bias_done = false;
+                DC_TRY(conv_wgrad(o.geom, o.wgrad, in, dy, G + o.w_off, m->scratch(), s,
+                                  o.b_off != NONE ? G + o.b_off : nullptr, &bias_done));
                 DC_TRY(gemm_mark(m, false, 0, s));
-                if (o.b_off != NONE)
+                if (o.b_off != NONE && !bias_done)
                     DC_TRY(colsum((int64_t)to.n * to.h * to.w, to.c, dy, G + o.b_off, m->scratch(), s));
             }
             if (o.dgrad_relu_from >= 0) { // through the folded ReLU into its input's gradient

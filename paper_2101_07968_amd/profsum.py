@@ -33,7 +33,7 @@ import re
 HERE = os.path.dirname(os.path.abspath(__file__))
 
 
-GEMM_SOURCES = ("igemm.hip", "fc.hip", "plan_table.cpp", "plan_table.inc")
+GEMM_SOURCES = ("igemm.hip", "fc.hip", "conv3.hip", "plan_table.cpp", "plan_table.inc")
 
 
 def gemm_sources_sha256():
@@ -52,14 +52,16 @@ def short(name):
 
 
 def is_gemm(name):
-    """A dispatch of a conv/FC pass: the GEMM, its split-K reduction or its channel padding."""
+    """A dispatch of a conv/FC pass: the GEMM, its split-K reduction or its channel padding, the FC
+    data-gradient kernels, or the RGB layer's direct kernels."""
     return any(k in name for k in ("igemm_kernel", "splitk_reduce_kernel", "pad_channels_kernel",
-                                   "fc_dgrad_kernel", "fc_dgrad_reduce_kernel"))
+                                   "fc_dgrad_kernel", "fc_dgrad_reduce_kernel", "conv3_"))
 
 
 def is_pass(name):
     """The one dispatch of each conv/FC pass that does its multiply-adds."""
-    return "igemm_kernel" in name or ("fc_dgrad_kernel" in name and "reduce" not in name)
+    return ("igemm_kernel" in name or ("fc_dgrad_kernel" in name and "reduce" not in name)
+            or "conv3_fwd_kernel" in name or "conv3_wgrad_kernel" in name)
 
 
 def cmd_stats(a):

@@ -9,7 +9,8 @@ The three fastest and the cost model's own choice are then timed again in
 interleaved rounds; the median decides.  A shape enters the table only when
 its winner beats the cost model's choice by more than --margin, so timing
 noise does not churn plans.  A pass that runs on the weight-streaming FC
-data-gradient kernel (plan source 3) is skipped.  Needs a GPU; run from the repository root:
+data-gradient kernel (plan source 3) or on the direct RGB-layer kernels (source 4) is
+skipped.  Needs a GPU; run from the repository root:
 
     python -m paper_2101_07968_amd.tune --out plan_table.inc
 
@@ -74,8 +75,9 @@ def main(argv=None):
         for pas in (0, 1, 2):
             if pas == 1 and rec["first"]:
                 continue
-            if D.conv_plan_info(g, pas)[7] == 3:   # the weight-streaming FC data-gradient kernel
-                line.append(f"{PASS_NAMES[pas]} FC streaming kernel")
+            src = D.conv_plan_info(g, pas)[7]
+            if src in (3, 4):   # the FC streaming kernel, the RGB layer's direct kernels
+                line.append(f"{PASS_NAMES[pas]} {'FC streaming' if src == 3 else 'direct RGB-layer'} kernel")
                 continue
 
             def run(ws, wsb, pas=pas):

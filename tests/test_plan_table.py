@@ -102,3 +102,28 @@ def test_table_covers_only_workload_shapes():
             known.add(tuple(g))
     for pas, g, _plan in _table():
         assert g in known, g
+
+
+RGB = [((32, 224, 224, 3, 64, 3, 3, 1, 1, 1), True), ((32, 299, 299, 3, 32, 3, 3, 2, 0, 0), True),
+       ((128, 32, 32, 3, 64, 3, 3, 1, 1, 1), True), ((2, 9, 9, 3, 128, 3, 3, 1, 1, 1), True),
+       ((2, 9, 9, 3, 70, 3, 3, 1, 1, 1), False), ((2, 9, 9, 3, 160, 3, 3, 1, 1, 1), False),
+       ((2, 9, 9, 3, 16, 3, 3, 1, 1, 1), False), ((32, 224, 224, 3, 64, 7, 7, 2, 3, 3), False),
+       ((2, 9, 9, 4, 64, 3, 3, 1, 1, 1), False), ((2, 9, 1, 3, 64, 3, 3, 1, 1, 1), False)]
+
+
+@pytest.mark.parametrize("shape,direct", RGB, ids=[str(s) for s, _ in RGB])
+def test_rgb_layer_takes_the_direct_kernels(shape, direct):
+    """Three input channels, a 3 x 3 filter and 32 to 128 output channels in blocks of 32
+    (and output rows of at least two pixels): forward and filter gradient report plan source 4,
+    the data gradient stays on the implicit GEMM; a pinned plan overrides the direct kernels."""
+    src = [D.conv_plan_info(shape, p)[7] for p in range(3)]
+    assert (src[0] == 4, src[2] == 4) == (direct, direct), src
+    assert src[1] != 4
+    if direct:
+        mt, nt, sp = D.conv_plan_candidates(shape, 0)[0]
+        D.conv_set_plan(shape, 0, mt, nt, sp)
+        try:
+            assert D.conv_plan_info(shape, 0)[7] == 2
+        finally:
+            D.conv_set_plan(shape, 0, 0)
+        assert D.conv_plan_info(shape, 0)[7] == 4
