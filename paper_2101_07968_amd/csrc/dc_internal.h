@@ -96,7 +96,9 @@ int conv3_forward(const ConvGeom &g, const float *x, const float *w, const float
 int conv3_wgrad(const ConvGeom &g, const float *x, const float *dy, float *dw, float *dbias, void *ws,
                 hipStream_t s);
 bool fc_streaming(const ConvGeom &g, int pass);
-void fc_plan(const ConvGeom &g, int splits_out[1], int *chunk, size_t *ws_bytes);
+void fc_plan(const ConvGeom &g, int pass, int splits_out[1], int *chunk, size_t *ws_bytes);
+int fc_forward(const ConvGeom &g, int splits, int chunk, const float *x, const float *w, const float *bias, int relu,
+               float *y, void *ws, hipStream_t s);
 int fc_dgrad(const ConvGeom &g, int splits, int chunk, const float *dy, const float *w, int accumulate, float *dx,
              void *ws, hipStream_t s, const float *relu_mask);
 

@@ -1144,7 +1144,7 @@ GemmPlan plan_gemm(const ConvGeom &g, int pass) {
     }
     if (src != PLAN_PINNED && src != -1 && fc_streaming(g, pass)) {
         size_t fws = 0;
-        fc_plan(g, &pl.fc_splits, &pl.fc_chunk, &fws);
+        fc_plan(g, pass, &pl.fc_splits, &pl.fc_chunk, &fws);
         pl.fc = true;
         pl.source = PLAN_FC;
         pl.ws_bytes = std::max(pl.ws_bytes, fws);
@@ -1169,6 +1169,8 @@ int conv_forward(const ConvGeom &g, const GemmPlan &pl, const float *x, const fl
                  const float *bias, int relu, float *y, void *ws, hipStream_t s) {
     if (pl.direct && al16(y))
         return conv3_forward(g, x, w, bias, relu, y, s);
+    if (pl.fc && ws && al16(x) && al16(w) && al16(y) && al16(bias) && al16(ws))
+        return fc_forward(g, pl.fc_splits, pl.fc_chunk, x, w, bias, relu, y, ws, s);
     if (pl.cpad) {
         if (!ws)
             return fail(DC_EINVAL, "conv forward needs %zu bytes of workspace", pl.ws_bytes);

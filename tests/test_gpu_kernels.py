@@ -170,19 +170,22 @@ def test_conv_rgb_direct(shape):
 
 
 FC_SHAPES = [(1, 4000, 1003), (5, 1004, 3999), (31, 2052, 2001), (32, 4096, 1000), (32, 25088, 4096),
-             (33, 4096, 1000), (32, 3996, 1000), (4, 1024, 64), (3, 300, 130)]
+             (33, 4096, 1000), (32, 3996, 1000), (4, 1024, 64), (3, 300, 130), (7, 4100, 4000),
+             (32, 16000, 1004), (1, 9216, 4096)]
 
 
 @pytest.mark.parametrize("n,fin,fout", FC_SHAPES, ids=[f"{n}x{i}->{o}" for n, i, o in FC_SHAPES])
 def test_fc_streaming(n, fin, fout):
-    """The data gradient of an FC layer of at most 32 rows and at least 4 M weights runs on
-    the weight-streaming kernel (plan source 3), other FC passes on the implicit GEMM;
-    ragged rows, features and outputs, bias + ReLU, an accumulating data gradient and the
-    ReLU-masked data gradient, against the oracle."""
+    """FC layers of at most 32 rows run on the FC kernels (plan source 3): the forward from 16 M
+    weights (outputs a multiple of 4), the data gradient from 4 M weights; the filter gradient
+    and smaller layers on the implicit GEMM.  Ragged rows, features and
+    outputs, bias + ReLU, an accumulating data gradient and the ReLU-masked data gradient,
+    against the oracle."""
     shape = (n, 1, 1, fin, fout, 1, 1, 1, 0, 0)
     src = [D.conv_plan_info(shape, p)[7] for p in range(3)]
-    streams = n <= 32 and fin % 4 == 0 and fin * fout >= 4000000
-    assert (src[1] == 3) == streams and src[0] != 3 and src[2] != 3, src
+    small = n <= 32 and fin % 4 == 0
+    want = [small and fout % 4 == 0 and fin * fout >= 16000000, small and fin * fout >= 4000000, False]
+    assert [s == 3 for s in src] == want, (src, want)
     seed = n * 1000 + fin + fout
     x = synth.random_tensor(seed, (n, 1, 1, fin))
     wt = synth.random_tensor(seed + 1, (fout, 1, 1, fin), scale=math.sqrt(2.0 / fin))
