@@ -53,14 +53,15 @@ def short(name):
 
 def is_gemm(name):
     """A dispatch of a conv/FC pass: the GEMM, its split-K reduction or its channel padding, the FC
-    data-gradient kernels, or the RGB layer's direct kernels."""
+    forward and data-gradient kernels, or the RGB layer's direct kernels."""
     return any(k in name for k in ("igemm_kernel", "splitk_reduce_kernel", "pad_channels_kernel",
-                                   "fc_dgrad_kernel", "fc_dgrad_reduce_kernel", "conv3_"))
+                                   "fc_dgrad_kernel", "fc_dgrad_reduce_kernel", "fc_fwd_kernel", "fc_fwd_reduce_kernel",
+                                   "conv3_"))
 
 
 def is_pass(name):
     """The one dispatch of each conv/FC pass that does its multiply-adds."""
-    return ("igemm_kernel" in name or ("fc_dgrad_kernel" in name and "reduce" not in name)
+    return ("igemm_kernel" in name or any(k in name and "reduce" not in name for k in ("fc_dgrad_kernel", "fc_fwd_kernel"))
             or "conv3_fwd_kernel" in name or "conv3_wgrad_kernel" in name)
 
 
@@ -88,7 +89,7 @@ def cmd_stats(a):
     per_step = dur / a.steps / 1e6
     out += ["", "Timed steps (the dispatches between the two relu_fwd_kernel marks bench.py places around them):",
             f"{passes} conv/FC passes ({passes // a.steps} per step), {len(win)} dispatches (implicit GEMM, "
-            f"split-K reduce, channel padding, FC data-gradient kernel), {dur / 1e6:.2f} ms in all, "
+            f"split-K reduce, channel padding, FC and RGB-layer kernels), {dur / 1e6:.2f} ms in all, "
             f"{per_step:.3f} ms per step.",
             f"Mean duration per pass: {dur / max(passes, 1) / 1e3:.1f} us; igemm_kernel alone: "
             f"{n_igemm} dispatches, mean {gemm_only / max(n_igemm, 1) / 1e3:.1f} us."]
@@ -138,7 +139,8 @@ def cmd_traffic(a):
     print(f"# HBM traffic of the implicit-GEMM kernel, {a.workload} batch {a.batch}")
     print(f"# commands: {a.cmd}")
     print(f"# calibration: {a.cal_bytes} B copy read as FETCH_SIZE {cal_f[0]:.1f} KiB, WRITE_SIZE {cal_w[0]:.1f} KiB")
-    print(f"# pass dispatches (igemm_kernel, and fc_dgrad_kernel for the FC data gradients it takes): {n} "
+    print(f"# pass dispatches (igemm_kernel, fc_fwd_kernel / fc_dgrad_kernel for the FC passes they take, "
+          f"conv3_fwd_kernel / conv3_wgrad_kernel for the RGB layer): {n} "
           f"({len(passes)} conv/FC passes, each launched twice)")
     print(f"# raw FETCH_SIZE {sum(gf):.0f} KiB, WRITE_SIZE {sum(gw):.0f} KiB over those dispatches")
     print(f"fetch_scale={sf:.4f}")
@@ -168,13 +170,14 @@ def _counters(path, names):
 
 
 def cmd_mfma(a):
-    """MFMA work and busy fraction of the implicit-GEMM dispatches of a `bench.py --kernels-only` run."""
+    """MFMA work and busy fraction of the pass dispatches (implicit GEMM, FC and RGB-layer kernels, all on
+    fp32 MFMA) of a `bench.py --kernels-only` run."""
     from . import nets as PN
     cnt = _counters(a.counters, {"SQ_INSTS_VALU_MFMA_MOPS_F32", "SQ_VALU_MFMA_BUSY_CYCLES", "GRBM_GUI_ACTIVE"})
-    gem = [(k, v) for k, v in cnt.values() if "igemm_kernel" in k]
-    dur = [d for _, d in _trace_durations(a.trace, lambda n: "igemm_kernel" in n)]
+    gem = [(k, v) for k, v in cnt.values() if is_pass(k)]
+    dur = [d for _, d in _trace_durations(a.trace, is_pass)]
     if len(dur) != len(gem):
-        raise SystemExit(f"{len(gem)} counted igemm dispatches but {len(dur)} in the trace")
+        raise SystemExit(f"{len(gem)} counted pass dispatches but {len(dur)} in the trace")
     mops = sum(v.get("SQ_INSTS_VALU_MFMA_MOPS_F32", 0) for _, v in gem)
     busy = sum(v.get("SQ_VALU_MFMA_BUSY_CYCLES", 0) for _, v in gem)
     active = sum(v.get("GRBM_GUI_ACTIVE", 0) for _, v in gem)
@@ -188,9 +191,9 @@ def cmd_mfma(a):
                                                                           PN.conv_geoms(ops, hwc, a.batch) if f))
     flops = mops * 512.0
     simds = a.cus * 4
-    print(f"# fp32 MFMA counters of the implicit-GEMM kernel, {a.workload} batch {a.batch}")
+    print(f"# fp32 MFMA counters of the conv/FC pass kernels, {a.workload} batch {a.batch}")
     print(f"# commands: {a.cmd}")
-    print(f"# igemm dispatches: {len(gem)} ({launches:g} launches of each conv/FC pass)")
+    print(f"# pass dispatches: {len(gem)} ({launches:g} launches of each conv/FC pass)")
     print(f"mfma_flops_per_iteration={flops / launches:.4e}")
     print(f"algorithmic_flops_per_iteration={algo:.4e}")
     print(f"mfma_over_algorithmic={flops / launches / algo:.3f}")
