@@ -208,6 +208,54 @@ def cmd_mfma(a):
     print(f"gemm_sources_sha256={gemm_sources_sha256()}")
 
 
+def cmd_stalls(a):
+    """Where the wave cycles of the implicit-GEMM dispatches go, from two counter passes of a
+    `bench.py --kernels-only` run: fractions of SQ_WAVE_CYCLES per pass kind, LDS counters, MFMA busy."""
+    pa = _counters(a.a, {"SQ_WAVE_CYCLES", "SQ_WAIT_ANY", "SQ_WAIT_INST_ANY", "SQ_WAIT_INST_LDS", "SQ_ACTIVE_INST_LDS",
+                         "SQ_ACTIVE_INST_VALU", "SQ_ACTIVE_INST_VMEM", "SQ_ACTIVE_INST_MISC"})
+    pb = _counters(a.b, {"SQ_INSTS_LDS", "SQ_LDS_BANK_CONFLICT", "SQ_LDS_DATA_FIFO_FULL", "SQ_VALU_MFMA_BUSY_CYCLES",
+                         "GRBM_GUI_ACTIVE"})
+
+    def total(cnt, pred):
+        s = {}
+        for k, v in cnt.values():
+            if pred(k):
+                for n, x in v.items():
+                    s[n] = s.get(n, 0.0) + x
+        return s
+
+    print("# wave-cycle attribution of the implicit-GEMM kernel, vgg16 batch 32")
+    print(f"# commands: {a.cmd}")
+    print("# fractions of SQ_WAVE_CYCLES: wait_any = s_waitcnt / barrier waits, wait_inst_any = waiting to issue "
+          "(the SIMD's MFMA pipe or a dependency), active_* = issuing that instruction type")
+    for label, pas in (("all", None), ("forward", "<0,"), ("data gradient", "<1,"), ("filter gradient", "<2,")):
+        def pred(n, pas=pas):
+            return "igemm_kernel" in n and (pas is None or pas in n.replace(" ", ""))
+        x, y = total(pa, pred), total(pb, pred)
+        wc = x.get("SQ_WAVE_CYCLES", 0.0) or 1.0
+        simd_cycles = y.get("GRBM_GUI_ACTIVE", 0.0) / a.xcds * a.cus * 4
+        print(f"{label}: wait_any={x.get('SQ_WAIT_ANY', 0) / wc:.3f} wait_inst_any={x.get('SQ_WAIT_INST_ANY', 0) / wc:.3f} "
+              f"wait_inst_lds={x.get('SQ_WAIT_INST_LDS', 0) / wc:.3f} active_lds={x.get('SQ_ACTIVE_INST_LDS', 0) / wc:.3f} "
+              f"active_valu={x.get('SQ_ACTIVE_INST_VALU', 0) / wc:.3f} active_vmem={x.get('SQ_ACTIVE_INST_VMEM', 0) / wc:.3f} "
+              f"active_misc={x.get('SQ_ACTIVE_INST_MISC', 0) / wc:.3f} "
+              f"lds_bank_conflicts_per_lds_inst={y.get('SQ_LDS_BANK_CONFLICT', 0) / max(y.get('SQ_INSTS_LDS', 0), 1):.3f} "
+              f"lds_data_fifo_full_per_lds_inst={y.get('SQ_LDS_DATA_FIFO_FULL', 0) / max(y.get('SQ_INSTS_LDS', 0), 1):.3f} "
+              f"mfma_busy={y.get('SQ_VALU_MFMA_BUSY_CYCLES', 0) / max(simd_cycles, 1):.3f}")
+    print(f"gemm_sources_sha256={gemm_sources_sha256()}")
+
+
+def cmd_table(a):
+    """Calls and per-dispatch durations of the kernels whose names contain one of the patterns."""
+    rows = [r for r in csv.DictReader(open(a.stats)) if any(p in r["Name"] for p in a.patterns.split(","))]
+    print(f"# rocprofv3 kernel statistics: {a.title}")
+    print(f"\nCommand: `{a.cmd}`\n")
+    print("| kernel | calls | total ms | avg us | min us | max us |")
+    print("|---|---|---|---|---|---|")
+    for r in rows:
+        print(f"| `{short(r['Name'])}` | {r['Calls']} | {float(r['TotalDurationNs']) / 1e6:.2f} | "
+              f"{float(r['AverageNs']) / 1e3:.1f} | {float(r['MinNs']) / 1e3:.1f} | {float(r['MaxNs']) / 1e3:.1f} |")
+
+
 def cmd_hbm(a):
     """HBM GB/s of the bandwidth-bound kernels: calibrated FETCH_SIZE + WRITE_SIZE per dispatch over the
     dispatch's duration from a kernel-trace run of the same command."""
@@ -266,6 +314,17 @@ def main():
     m.add_argument("--cus", type=int, default=256)
     m.add_argument("--xcds", type=int, default=8)
     m.add_argument("--cmd", default="")
+    tb = sub.add_parser("table")
+    tb.add_argument("stats")
+    tb.add_argument("--patterns", required=True, help="comma-separated substrings of kernel names")
+    tb.add_argument("--title", default="")
+    tb.add_argument("--cmd", default="")
+    w = sub.add_parser("stalls")
+    w.add_argument("a")
+    w.add_argument("b")
+    w.add_argument("--cus", type=int, default=256)
+    w.add_argument("--xcds", type=int, default=8)
+    w.add_argument("--cmd", default="")
     h = sub.add_parser("hbm")
     h.add_argument("fetch")
     h.add_argument("write")
@@ -274,7 +333,7 @@ def main():
     h.add_argument("--what-ran", default="")
     h.add_argument("--cmd", default="")
     a = ap.parse_args()
-    {"stats": cmd_stats, "traffic": cmd_traffic, "mfma": cmd_mfma, "hbm": cmd_hbm}[a.what](a)
+    {"stats": cmd_stats, "traffic": cmd_traffic, "mfma": cmd_mfma, "hbm": cmd_hbm, "stalls": cmd_stalls, "table": cmd_table}[a.what](a)
 
 
 if __name__ == "__main__":
