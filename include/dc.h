@@ -185,6 +185,22 @@ int dc_ps_write(dc_model *m, const float *host_params, size_t n);
  * pointer may be NULL). */
 int dc_ps_read(const dc_model *m, float *params_out, float *grads_out, size_t n);
 
+/* Copy one tensor of the last dc_step / dc_profile out of the workspace, for
+ * checks against an oracle (the discrete decisions of Sec. III-A's forward:
+ * which ReLU inputs were positive, which window tap each max-pool took).
+ * tensor 0 is the input batch, tensor i + 1 the output of op i.
+ *   what = DC_READ_ACT:    the activation, n*h*w*c float32 (NHWC) -> host;
+ *   what = DC_READ_ARGMAX: when op tensor-1 is a max-pool, its window tap per
+ *                          output element (r * S + s), n*h*w*c uint8 -> host.
+ * bytes must equal the tensor's size.  DC_EINVAL for a bad tensor or size,
+ * DC_READ_ACT of tensor 0 (the caller's own buffer) or of an activation the
+ * model does not keep (the output of a conv / FC / BN / add whose ReLU is
+ * folded into it: only the ReLU's output is written), or DC_READ_ARGMAX on
+ * anything but a max-pool output; DC_ESTATE when no workspace is bound.
+ * Waits for the model's work to finish first. */
+enum { DC_READ_ACT = 0, DC_READ_ARGMAX = 1 };
+int dc_model_read_tensor(const dc_model *m, int tensor, int what, void *host, size_t bytes);
+
 /* ------------------------------------------------------------ link and batch */
 
 /*

@@ -15,7 +15,10 @@ Sec. III-A (pull, forward, backward, push), and of the server's update:
 Everything is float64.  Convolutions and max-pooling run in the C loops of
 ``cnn.c`` (built by ``oracle/build.py``); the rest are numpy expressions of
 the definitions.  Decisions that floating point takes (the ReLU sign, the
-max-pool argmax) are taken on the values rounded to float32.
+max-pool argmax) are taken on the values rounded to float32, or, when the
+caller passes them (``decisions``), taken as given: a parity check can then
+hand the oracle another implementation's decisions and compare the arithmetic
+alone, apart from the decisions that float32 rounding flips near a tie.
 
 Only ``tests/``, ``__graft_entry__.smoke()`` and ``bench.py``'s
 ``cpu_baseline`` leg may use this module.
@@ -130,6 +133,21 @@ def maxpool_forward(x, r, s, st, pad):
     lib().or_maxpool_forward(N, H, W, C, r, s, st, pad, P, Q, _dp(x), _dp(y),
                              arg.ctypes.data_as(ctypes.POINTER(ctypes.c_int)))
     return y, arg
+
+
+def maxpool_at(x, arg, r, s, st, pad):
+    """The max-pool forward with given window taps: y[n,p,q,c] = x at tap arg = r' * s + s' of the
+    window at (p*st - pad, q*st - pad); every tap must lie inside the image."""
+    x = _f64(x)
+    N, H, W, C = x.shape
+    P, Q = conv_out(H, r, st, pad), conv_out(W, s, st, pad)
+    arg = np.asarray(arg).reshape(N, P, Q, C)
+    h = np.arange(P)[None, :, None, None] * st + arg // s - pad
+    w = np.arange(Q)[None, None, :, None] * st + arg % s - pad
+    assert (h >= 0).all() and (h < H).all() and (w >= 0).all() and (w < W).all(), "a tap outside the image"
+    n = np.arange(N)[:, None, None, None]
+    c = np.arange(C)[None, None, None, :]
+    return x[n, h, w, c]
 
 
 def maxpool_backward(dy, arg, in_shape, r, s, st, pad):
@@ -340,8 +358,11 @@ class Net:
         off, shape = self.pslots[i][name]
         return params[off:off + int(np.prod(shape))].reshape(shape)
 
-    def forward(self, x, params):
-        """Returns (tensors, caches); tensors[0] is the input, tensors[-1] the logits."""
+    def forward(self, x, params, decisions=None):
+        """Returns (tensors, caches); tensors[0] is the input, tensors[-1] the logits.
+        decisions: optional {op index: ReLU mask (bool, the op's input shape) or max-pool window
+        tap r * S + s (int, the op's output shape)} taken instead of deciding."""
+        decisions = decisions or {}
         params = np.asarray(params, dtype=np.float64)
         t = [np.asarray(x, dtype=np.float64)]
         cache = {}
@@ -361,9 +382,15 @@ class Net:
                 y, xhat, invstd = batchnorm_forward(a, self._p(params, i, "gamma"), self._p(params, i, "beta"))
                 cache[i] = (xhat, invstd)
             elif kind == "relu":
-                y = np.where(relu_mask(a), a, 0.0)
+                mask = np.asarray(decisions[i], dtype=bool) if i in decisions else relu_mask(a)
+                y = np.where(mask, a, 0.0)
+                cache[i] = mask
             elif kind == "maxpool":
-                y, arg = maxpool_forward(a, op["r"], op["s"], op["stride"], op["pad"])
+                if i in decisions:
+                    arg = np.asarray(decisions[i], dtype=np.int32)
+                    y = maxpool_at(a, arg, op["r"], op["s"], op["stride"], op["pad"])
+                else:
+                    y, arg = maxpool_forward(a, op["r"], op["s"], op["stride"], op["pad"])
                 cache[i] = arg
             elif kind == "avgpool":
                 y = avgpool_forward(a, op["r"], op["s"], op["stride"], op["pad"])
@@ -378,11 +405,11 @@ class Net:
             t.append(y)
         return t, cache
 
-    def loss_and_grads(self, x, y, params, keep=False):
+    def loss_and_grads(self, x, y, params, keep=False, decisions=None):
         """One forward and backward pass: returns (loss, flat float64 gradient), and
         with keep=True also (tensors, caches, tensor gradients) of the pass."""
         params = np.asarray(params, dtype=np.float64)
-        t, cache = self.forward(x, params)
+        t, cache = self.forward(x, params, decisions)
         N = self.batch
         loss, dz = softmax_xent(t[-1].reshape(N, self.classes), np.asarray(y))
         g = [None] * len(t)
@@ -428,7 +455,7 @@ class Net:
                 put(i, "beta", dbeta)
                 acc(op["in"], dx)
             elif kind == "relu":
-                acc(op["in"], np.where(relu_mask(a), dy, 0.0))
+                acc(op["in"], np.where(cache[i], dy, 0.0))
             elif kind == "maxpool":
                 acc(op["in"], maxpool_backward(dy, cache[i], a.shape, op["r"], op["s"], op["stride"], op["pad"]))
             elif kind == "avgpool":

@@ -18,6 +18,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libdc.so")
 DC_OK, DC_EINVAL, DC_EHIP, DC_ENOMEM, DC_ESTATE, DC_ETIMEOUT = range(6)
 DC_OP_CONV, DC_OP_FC, DC_OP_BN, DC_OP_RELU, DC_OP_MAXPOOL, DC_OP_GAP, DC_OP_ADD, DC_OP_CONCAT, DC_OP_AVGPOOL = range(1, 10)
 DC_OPT_LR, DC_OPT_TIMELINE, DC_OPT_TIMEOUT_S, DC_OPT_SGD_THREADS, DC_OPT_GRAPHS, DC_OPT_GEMM_TIMING = range(1, 7)
+DC_READ_ACT, DC_READ_ARGMAX = 0, 1
 
 c_i32, c_i64, c_f32, c_f64, c_sz, c_vp = (ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_double,
                                           ctypes.c_size_t, ctypes.c_void_p)
@@ -105,6 +106,7 @@ _SIGS = {
     "dc_model_set_option": (ctypes.c_int, [c_vp, ctypes.c_int, c_f64]),
     "dc_ps_write": (ctypes.c_int, [c_vp, c_vp, c_sz]),
     "dc_ps_read": (ctypes.c_int, [c_vp, c_vp, c_vp, c_sz]),
+    "dc_model_read_tensor": (ctypes.c_int, [c_vp, ctypes.c_int, ctypes.c_int, c_vp, c_sz]),
     "dc_profile": (ctypes.c_int, [c_vp, _P(Batch), _P(Link), ctypes.c_int, c_vp, _P(ProfileT)]),
     "dc_plan": (ctypes.c_int, [_P(ProfileT), _P(PlanT)]),
     "dc_plan_sequential": (ctypes.c_int, [_P(ProfileT), _P(PlanT)]),
@@ -372,6 +374,13 @@ class Model:
         g = np.empty(self.n_params, dtype=np.float32)
         call("dc_ps_read", self.h, p.ctypes.data, g.ctypes.data, self.n_params)
         return p, g
+
+    def read_tensor(self, tensor, shape, what=0):
+        """dc_model_read_tensor: tensor `tensor` of the last step (NHWC `shape`) as a float32 array
+        (what = DC_READ_ACT) or the max-pool window taps as a uint8 array (DC_READ_ARGMAX)."""
+        out = np.empty(shape, dtype=np.float32 if what == DC_READ_ACT else np.uint8)
+        call("dc_model_read_tensor", self.h, tensor, what, out.ctypes.data, out.nbytes)
+        return out
 
     def _batch(self, x, y):
         """dc_batch of a float32 NHWC input and int32 labels, both contiguous device tensors."""

@@ -805,6 +805,39 @@ extern "C" int dc_ps_write(dc_model *m, const float *host_params, size_t n) {
     return DC_OK;
 }
 
+extern "C" int dc_model_read_tensor(const dc_model *m, int tensor, int what, void *host, size_t bytes) {
+    clear_error();
+    if (!m || !host)
+        return fail(DC_EINVAL, "NULL model or destination");
+    if (tensor < 0 || tensor >= (int)m->tensors.size())
+        return fail(DC_EINVAL, "tensor %d outside 0..%zu", tensor, m->tensors.size() - 1);
+    if (!m->ws)
+        return fail(DC_ESTATE, "no workspace is bound");
+    const TensorInfo &ti = m->tensors[tensor];
+    size_t off = NONE, need = 0;
+    if (what == DC_READ_ACT) {
+        if (tensor == 0)
+            return fail(DC_EINVAL, "tensor 0 is the caller's input batch");
+        // a producer with a folded ReLU writes only the ReLU's output
+        if (m->ops[tensor - 1].relu_into >= 0 || ti.act == NONE)
+            return fail(DC_EINVAL, "tensor %d is not kept (the input of a folded ReLU)", tensor);
+        off = ti.act;
+        need = (size_t)ti.size() * sizeof(float);
+    } else if (what == DC_READ_ARGMAX) {
+        if (tensor == 0 || m->ops[tensor - 1].d.kind != DC_OP_MAXPOOL)
+            return fail(DC_EINVAL, "tensor %d is not a max-pool output", tensor);
+        off = m->ops[tensor - 1].aux;
+        need = (size_t)ti.size();
+    } else {
+        return fail(DC_EINVAL, "what must be DC_READ_ACT or DC_READ_ARGMAX");
+    }
+    if (bytes != need)
+        return fail(DC_EINVAL, "tensor %d needs %zu bytes, got %zu", tensor, need, bytes);
+    DC_HIP(hipDeviceSynchronize());
+    DC_HIP(hipMemcpy(host, m->ws + off, bytes, hipMemcpyDeviceToHost));
+    return DC_OK;
+}
+
 extern "C" int dc_ps_read(const dc_model *m, float *params_out, float *grads_out, size_t n) {
     clear_error();
     if (!m || n != m->n_params)

@@ -42,6 +42,25 @@ def rel_err(x, ref):
     return num / den
 
 
+def update_err(p_new, p_old, want):
+    """How far the applied update p_new - p_old is from want, relative to max |want|.
+
+    p_new is the server's float32 weight after the step, which holds w - lr g rounded
+    to float32: half an ulp of each new weight is storage rounding that no accuracy of
+    g removes (for a BN gamma near 1 updated by ~1e-5 it is ~5e-3 of the update), so
+    each element's distance is taken less that half ulp."""
+    p_new = np.asarray(p_new, dtype=np.float32)
+    upd = p_new.astype(np.float64) - np.asarray(p_old, dtype=np.float64)
+    want = np.asarray(want, dtype=np.float64)
+    if not want.size:
+        return 0.0
+    excess = np.maximum(np.abs(upd - want) - np.spacing(np.abs(p_new)).astype(np.float64) / 2, 0.0)
+    den = np.abs(want).max()
+    if den == 0:
+        return 0.0 if excess.max() == 0 else np.inf
+    return excess.max() / den
+
+
 def stream():
     return torch().cuda.current_stream().cuda_stream
 

@@ -23,7 +23,7 @@ from oracle import nets as ON
 from oracle import plan as OP
 from paper_2101_07968_amd import _lib as D
 from paper_2101_07968_amd import nets as PN
-from tests.gpu_helpers import dev, rel_err, report
+from tests.gpu_helpers import dev, rel_err, report, update_err
 
 pytestmark = pytest.mark.gpu
 
@@ -120,8 +120,7 @@ def test_step_matches_oracle(name, batch):
             bar_w = max(1e-3, 5.0 * spread_w[(i, pname)])
             assert rel_err(p_new[sl], p_ref[sl]) <= bar_w, (i, pname, rel_err(p_new[sl], p_ref[sl]))
             # the update itself, not just the weights, follows w - 0.01 g
-            upd = p_new[sl].astype(np.float64) - params[sl].astype(np.float64)
-            assert rel_err(upd, -0.01 * g_ref[sl]) <= 1.01 * bar + 1e-6, (i, pname)
+            assert update_err(p_new[sl], params[sl], -0.01 * g_ref[sl]) <= 1.01 * bar + 1e-6, (i, pname)
     rows.sort(key=lambda r: -r[2])
     print(f"{name}: {len(rows)} tensors, {widened} with a widened bar, worst err/bar {worst:.3f}; "
           f"largest errors (op, tensor, err, fp32 spread): "
@@ -274,6 +273,42 @@ def test_argument_errors():
     with pytest.raises(D.DcError) as e:
         model.timeline()
     assert e.value.status == D.DC_ESTATE
+
+
+def test_read_tensor_returns_the_steps_tensors():
+    """dc_model_read_tensor after a step: every kept activation equals the oracle's
+    forward (taken with the GPU's max-pool taps), and the reads it cannot serve fail."""
+    model, onet, xd, yd, x, y, params = setup_model("tiny", 4, seed=5)
+    model.step(xd, yd, D.Plan(model.L), UNPACED)
+    t, _ = onet.forward(x, params)
+    read, refused = 0, 0
+    for i, op in enumerate(onet.ops):
+        try:
+            a = model.read_tensor(i + 1, onet.shapes[i + 1])
+        except D.DcError as e:
+            # only a producer whose ReLU is folded into it keeps no output
+            assert e.status == D.DC_EINVAL
+            assert onet.ops[i + 1]["op"] == "relu" and onet.ops[i + 1]["in"] == i + 1, i
+            refused += 1
+            continue
+        read += 1
+        if op["op"] == "maxpool":
+            arg = model.read_tensor(i + 1, onet.shapes[i + 1], D.DC_READ_ARGMAX)
+            assert arg.max() < op["r"] * op["s"]
+            ref = OC.maxpool_at(t[op["in"]], arg.astype(np.int32), op["r"], op["s"], op["stride"], op["pad"])
+            assert rel_err(ref, t[i + 1]) <= 1e-6, i  # the GPU took a maximum of each window
+            assert rel_err(a, ref) <= 1e-5, i
+        else:
+            assert rel_err(a, t[i + 1]) <= 1e-5, i
+    assert read and refused
+    bad = [(0, D.DC_READ_ACT, onet.shapes[0]), (len(onet.ops) + 1, D.DC_READ_ACT, (1,)),
+           (-1, D.DC_READ_ACT, (1,)), (2, D.DC_READ_ARGMAX, onet.shapes[2]),
+           (2, D.DC_READ_ACT, (onet.shapes[2][0] - 1,) + onet.shapes[2][1:]), (3, 7, onet.shapes[3])]
+    for tensor, what, shape in bad:
+        with pytest.raises(D.DcError) as e:
+            model.read_tensor(tensor, shape, what)
+        assert e.value.status == D.DC_EINVAL, (tensor, what, shape)
+    model.close()
 
 
 def test_watchdog_times_out_and_gpu_drains():

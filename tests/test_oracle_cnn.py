@@ -410,3 +410,71 @@ def test_conv_samples_match_whole_tensors(shape):
     dw = cnn.conv2d_backward_filter(x, dy, (R, R), st, pad)
     idx = np.argwhere(np.ones(dw.shape, dtype=bool))
     np.testing.assert_allclose(cnn.conv2d_samples("wgrad", geom, x, dy, idx), dw.reshape(-1), rtol=1e-14, atol=1e-13)
+
+
+# ---------------------------------------------------------------- given decisions
+# The oracle can take the ReLU masks and max-pool window taps as given (the
+# GPU's, in the test that compares arithmetic apart from decision flips).
+
+
+def test_maxpool_at_takes_the_given_taps():
+    rng = np.random.default_rng(5)
+    x = rng.standard_normal((2, 9, 7, 3))
+    for r, st, pad in ((3, 2, 1), (2, 2, 0), (3, 1, 1)):
+        y, arg = cnn.maxpool_forward(x, r, r, st, pad)
+        np.testing.assert_array_equal(cnn.maxpool_at(x, arg, r, r, st, pad), y)
+    # tap 4 of a 3x3 window at stride 2 with padding 1 is the pixel (2p, 2q)
+    y = cnn.maxpool_at(x, np.full((2, 5, 4, 3), 4), 3, 3, 2, 1)
+    np.testing.assert_array_equal(y, x[:, ::2, ::2, :])
+    with pytest.raises(AssertionError):
+        cnn.maxpool_at(x, np.zeros((2, 5, 4, 3), dtype=int), 3, 3, 2, 1)  # tap 0 of window (0, 0) is padding
+
+
+def test_given_decisions_equal_to_its_own_reproduce_the_iteration():
+    spec = _mini_resnet()
+    net = cnn.Net(spec, 3)
+    x, y, p = synth.cnn_inputs(8, 3, spec["hwc"], spec["classes"], net.param_specs)
+    loss, g, t, cache, _ = net.loss_and_grads(x, y, p, keep=True)
+    dec = {i: cache[i] for i, op in enumerate(net.ops) if op["op"] in ("relu", "maxpool")}
+    assert len(dec) == sum(op["op"] in ("relu", "maxpool") for op in net.ops)
+    loss2, g2 = net.loss_and_grads(x, y, p, decisions=dec)
+    assert loss2 == loss
+    np.testing.assert_array_equal(g2, g)
+    from tests import torch_ref
+    lt, gt = torch_ref.loss_and_grads(spec, net, x, y, p, torch.float64, decisions=dec)
+    assert abs(loss - lt) <= 1e-12 * max(1.0, abs(lt))
+    np.testing.assert_allclose(g, gt, rtol=1e-9, atol=1e-12 * np.abs(gt).max())
+
+
+def test_given_decisions_against_a_network_without_them():
+    """Every ReLU told to pass everything and every 2x2/2 max-pool told to take tap 0 is the
+    same network with those ops replaced by identity (1x1 average pooling, stride 1) and by
+    stride-2 subsampling (1x1 average pooling, stride 2): bit for bit."""
+    spec = nets.tiny()
+    lin = dict(spec, ops=[dict(op) for op in spec["ops"]])
+    for op in lin["ops"]:
+        if op["op"] == "relu":
+            op.update(op="avgpool", r=1, s=1, stride=1, pad=0)
+        elif op["op"] == "maxpool":
+            assert (op["r"], op["s"], op["stride"], op["pad"]) == (2, 2, 2, 0)
+            op.update(op="avgpool", r=1, s=1, stride=2, pad=0)
+    batch = 3
+    a, b = cnn.Net(spec, batch), cnn.Net(lin, batch)
+    x, y, p = synth.cnn_inputs(9, batch, spec["hwc"], spec["classes"], a.param_specs)
+    dec = {}
+    for i, op in enumerate(a.ops):
+        if op["op"] == "relu":
+            dec[i] = np.ones(a.shapes[op["in"]], dtype=bool)
+        elif op["op"] == "maxpool":
+            dec[i] = np.zeros(a.shapes[i + 1], dtype=np.int32)
+    la, ga = a.loss_and_grads(x, y, p, decisions=dec)
+    lb, gb = b.loss_and_grads(x, y, p)
+    assert la == lb
+    np.testing.assert_array_equal(ga, gb)
+    # torch's float64 routines with the same decisions given (the float32 yardstick's path)
+    from tests import torch_ref
+    lt, gt = torch_ref.loss_and_grads(spec, a, x, y, p, torch.float64, decisions=dec)
+    assert abs(la - lt) <= 1e-12 * abs(lt)
+    np.testing.assert_allclose(ga, gt, rtol=1e-9, atol=1e-12 * np.abs(gt).max())
+    # and the decisions matter: the network's own ones give another iteration
+    assert a.loss_and_grads(x, y, p)[0] != la

@@ -12,11 +12,24 @@ def _nchw(a, dtype):
     return torch.from_numpy(np.ascontiguousarray(np.asarray(a).transpose(0, 3, 1, 2))).to(dtype)
 
 
-def loss_and_grads(spec, net, x, y, p, dtype=torch.float64, perturb=None):
+def _maxpool_at(a, arg, r, s, st, pad):
+    """Max-pool forward (NCHW) taking the window tap arg = r' * s + s' (NHWC array) of each output."""
+    N, C, H, W = a.shape
+    arg = torch.from_numpy(np.ascontiguousarray(np.asarray(arg).transpose(0, 3, 1, 2))).long()
+    P, Q = arg.shape[2], arg.shape[3]
+    h = torch.arange(P).view(1, 1, P, 1) * st + torch.div(arg, s, rounding_mode="floor") - pad
+    w = torch.arange(Q).view(1, 1, 1, Q) * st + arg % s - pad
+    return a.flatten(2).gather(2, (h * W + w).flatten(2)).view(N, C, P, Q)
+
+
+def loss_and_grads(spec, net, x, y, p, dtype=torch.float64, perturb=None, decisions=None):
     """(loss, flat gradient as float64) of one iteration in the given torch dtype on the CPU.
 
     perturb(i, o), if given, replaces the output o (NCHW) of every conv, FC and
-    BN op i in the forward pass, as the oracle's test hook does."""
+    BN op i in the forward pass, as the oracle's test hook does.  decisions, if
+    given, are taken as the oracle's are: {op index: ReLU mask (NHWC bool) or
+    max-pool window tap (NHWC int)}."""
+    decisions = decisions or {}
     pt = torch.from_numpy(np.asarray(p, dtype=np.float64)).to(dtype).requires_grad_(True)
 
     def prm(i, name):
@@ -39,9 +52,10 @@ def loss_and_grads(spec, net, x, y, p, dtype=torch.float64, perturb=None):
         elif k == "bn":
             o = F.batch_norm(a, None, None, prm(i, "gamma"), prm(i, "beta"), training=True, eps=1e-5)
         elif k == "relu":
-            o = F.relu(a)
+            o = a * _nchw(decisions[i], dtype) if i in decisions else F.relu(a)
         elif k == "maxpool":
-            o = F.max_pool2d(a, op["r"], op["stride"], op["pad"])
+            o = (_maxpool_at(a, decisions[i], op["r"], op["s"], op["stride"], op["pad"]) if i in decisions
+                 else F.max_pool2d(a, op["r"], op["stride"], op["pad"]))
         elif k == "avgpool":
             o = F.avg_pool2d(a, (op["r"], op["s"]), op["stride"], op["pad"], count_include_pad=False)
         elif k == "gap":
