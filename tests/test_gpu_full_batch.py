@@ -31,10 +31,9 @@ import numpy as np
 import pytest
 
 from oracle import cnn as OC
-from paper_2101_07968_amd import _lib as D
 from tests import layerwise
 from tests.gpu_helpers import rel_err, report, update_err
-from tests.test_gpu_step import UNPACED, plans_for, setup_model
+from tests.test_gpu_step import UNPACED, gpu_decisions, plans_for, setup_model
 
 pytestmark = pytest.mark.gpu
 
@@ -77,13 +76,7 @@ def test_full_batch_matches_oracle(name, batch, seed):
     print(f"full batch {name} batch {batch} seed {seed}: dc_step", flush=True)
     st = model.step(xd, yd, plans_for(model.L, seed=seed)["random"], UNPACED)
     p_new, g = model.ps_read()
-    # the GPU's decisions in this iteration: tensor i + 1 is op i's output
-    dec = {}
-    for i, op in enumerate(onet.ops):
-        if op["op"] == "relu":
-            dec[i] = model.read_tensor(i + 1, onet.shapes[i + 1]) > 0
-        elif op["op"] == "maxpool":
-            dec[i] = model.read_tensor(i + 1, onet.shapes[i + 1], D.DC_READ_ARGMAX).astype(np.int32)
+    dec = gpu_decisions(model, onet, name)  # the GPU's ReLU masks and max-pool taps in this iteration
     model.close()
     del model, xd, yd
     torch.cuda.empty_cache()

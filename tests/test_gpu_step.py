@@ -56,7 +56,25 @@ PARITY = [("tiny", 4), ("alexnet", 2), ("resnet18", 8), ("resnet50", 2), ("vgg16
           ("vgg19", 1), ("resnet152", 2), ("inception_v4", 1), ("tiny", 1), ("resnet18", 1)]
 
 
-def fp32_spread(spec, onet, x, y, params, g_ref):
+def gpu_decisions(model, onet, name):
+    """The discrete decisions of the model's last step, keyed by oracle op, for the
+    oracle's forward: every ReLU's mask (its output > 0) and every max-pool's window
+    taps (dc_model_read_tensor; the product's op j + 1 output is its tensor j + 1, and
+    its op list nests concatenations of more than four parts, so ops are matched by
+    layerwise.op_map)."""
+    from tests import layerwise
+    omap = layerwise.op_map(PN.build(name)[0], onet)
+    prod = {i: j for j, i in omap.items() if i is not None}
+    dec = {}
+    for i, op in enumerate(onet.ops):
+        if op["op"] == "relu":
+            dec[i] = model.read_tensor(prod[i] + 1, onet.shapes[i + 1]) > 0
+        elif op["op"] == "maxpool":
+            dec[i] = model.read_tensor(prod[i] + 1, onet.shapes[i + 1], D.DC_READ_ARGMAX).astype(np.int32)
+    return dec
+
+
+def fp32_spread(spec, onet, x, y, params, g_ref, decisions=None):
     """Per tensor, how far float32-grade evaluations of this iteration land from the oracle.
 
     Members of the yardstick ensemble:
@@ -69,18 +87,19 @@ def fp32_spread(spec, onet, x, y, params, g_ref):
     discrete gradient changes (a decision near its threshold flips), so the
     float64 result is only determined to within this spread.  Returns the
     per-tensor largest distance from the oracle, for gradients and for the
-    post-step weights w - 0.01 g.
+    post-step weights w - 0.01 g.  With `decisions` every member holds those
+    ReLU masks and max-pool taps fixed.
     """
     import torch
     from tests import torch_ref
     rng = np.random.default_rng(1234)
-    runs_g = [torch_ref.loss_and_grads(spec, onet, x, y, params, torch.float32)[1]]
+    runs_g = [torch_ref.loss_and_grads(spec, onet, x, y, params, torch.float32, decisions=decisions)[1]]
     pp = params.astype(np.float64) * (1.0 + 2.0 ** -24 * rng.standard_normal(params.size))
-    runs_g.append(torch_ref.loss_and_grads(spec, onet, x, y, pp, torch.float32)[1])
+    runs_g.append(torch_ref.loss_and_grads(spec, onet, x, y, pp, torch.float32, decisions=decisions)[1])
     for eps in (2.0 ** -23, 2.0 ** -21):
         onet.perturb = lambda i, t, eps=eps: t * (1.0 + eps * rng.standard_normal(t.shape))
         try:
-            runs_g.append(onet.loss_and_grads(x, y, params)[1])
+            runs_g.append(onet.loss_and_grads(x, y, params, decisions=decisions)[1])
         finally:
             onet.perturb = None
     w_ref = params.astype(np.float64) - 0.01 * g_ref
@@ -98,7 +117,8 @@ def fp32_spread(spec, onet, x, y, params, g_ref):
 def test_step_matches_oracle(name, batch):
     """Loss within 1e-4; each gradient and post-step weight tensor within 1e-3 -
     or, for a tensor whose float32 evaluations scatter wider than that, within
-    5x the scatter of the float32 yardstick (see fp32_spread)."""
+    5x the scatter of the float32 yardstick (see fp32_spread).  Then the same
+    against the oracle given the GPU's own ReLU and max-pool decisions."""
     model, onet, xd, yd, x, y, params = setup_model(name, batch, seed=10 + batch)
     print(f"step {name} batch {batch}", flush=True)
     st = model.step(xd, yd, plans_for(model.L)["random"], UNPACED)
@@ -125,6 +145,28 @@ def test_step_matches_oracle(name, batch):
     print(f"{name}: {len(rows)} tensors, {widened} with a widened bar, worst err/bar {worst:.3f}; "
           f"largest errors (op, tensor, err, fp32 spread): "
           + ", ".join(f"({i},{p},{e:.1e},{s:.1e})" for i, p, e, s in rows[:4]), flush=True)
+    # The same iteration with the GPU's own ReLU masks and max-pool taps given to the
+    # oracle: no decision near its threshold can flip, so 1e-3 holds unless float32
+    # evaluations with those decisions held scatter wider than 2e-4 (then 5x that).
+    dec = gpu_decisions(model, onet, name)
+    loss_d, g_d = onet.loss_and_grads(x, y, params, decisions=dec)
+    assert abs(st["loss"] - loss_d) <= 1e-4 * abs(loss_d)
+    errs = {}
+    for i, slots in enumerate(onet.pslots):
+        for pname, (off, shape) in slots.items():
+            sl = slice(off, off + int(np.prod(shape)))
+            errs[(i, pname)] = max(rel_err(g[sl], g_d[sl]), rel_err(p_new[sl], params[sl] - 0.01 * g_d[sl]),
+                                   update_err(p_new[sl], params[sl], -0.01 * g_d[sl]) / 1.01)
+    spread_d = {}
+    if max(errs.values()) > 1e-3:
+        spread_d, _ = fp32_spread(ON.get(name), onet, x, y, params, g_d, decisions=dec)
+    bars = {k: 1e-3 if spread_d.get(k, 0.0) <= 2e-4 else max(1e-3, 5.0 * spread_d[k]) for k in errs}
+    worst_k = max(errs, key=lambda k: errs[k] / bars[k])
+    report(f"step {name} b{batch} with the GPU's decisions: {len(errs)} tensors, "
+           f"{sum(e > 1e-3 for e in errs.values())} above 1e-3, {sum(b > 1e-3 for b in bars.values())} on a "
+           f"widened bar, worst err/bar {errs[worst_k] / bars[worst_k]:.3f} at {worst_k} (err {errs[worst_k]:.1e})")
+    fails = [(k, errs[k], spread_d.get(k), bars[k]) for k in errs if errs[k] > bars[k]]
+    assert not fails, fails[:5]
 
 
 @pytest.mark.parametrize("name,batch", [("tiny", 4), ("resnet18", 16), ("resnet50", 2), ("googlenet", 2)])
