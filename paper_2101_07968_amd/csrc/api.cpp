@@ -3,6 +3,7 @@
 #include "dc_internal.h"
 
 #include <algorithm>
+#include <climits>
 #include <cstdarg>
 #include <cstdio>
 #include <mutex>
@@ -324,9 +325,11 @@ extern "C" int dc_relu_backward(const float *dy, const float *y, int accumulate,
 }
 
 static int pool_check(const dc_pool_shape *sh) {
-    if (!sh || sh->n < 0 || sh->h < 1 || sh->w < 1 || sh->c < 1 || sh->r < 1 || sh->s < 1 || sh->stride < 1 ||
-        sh->pad < 0 || sh->pad >= sh->r || sh->pad >= sh->s || sh->r * sh->s > 256 || sh->h + 2 * sh->pad < sh->r ||
-        sh->w + 2 * sh->pad < sh->s)
+    // r and s are bounded before their product; padded extents in 64 bits
+    if (!sh || sh->n < 0 || sh->h < 1 || sh->w < 1 || sh->c < 1 || sh->r < 1 || sh->s < 1 || sh->r > 256 ||
+        sh->s > 256 || sh->stride < 1 || sh->pad < 0 || sh->pad >= sh->r || sh->pad >= sh->s ||
+        sh->r * sh->s > 256 || (int64_t)sh->h + 2 * sh->pad < sh->r || (int64_t)sh->w + 2 * sh->pad < sh->s ||
+        (int64_t)sh->h + 2 * sh->pad >= INT_MAX || (int64_t)sh->w + 2 * sh->pad >= INT_MAX)
         return fail(DC_EINVAL, "invalid pooling shape");
     return DC_OK;
 }
@@ -414,7 +417,7 @@ extern "C" int dc_add_relu_backward(const float *dy, const float *y, int acc0, f
 extern "C" int dc_concat_forward(int64_t rows, int32_t c_in, int32_t c_out, int32_t off, const float *x, float *y,
                                  void *stream) {
     clear_error();
-    if (rows < 0 || c_in < 1 || off < 0 || off + c_in > c_out || (rows > 0 && (!x || !y)))
+    if (rows < 0 || c_in < 1 || off < 0 || (int64_t)off + c_in > c_out || (rows > 0 && (!x || !y)))
         return fail(DC_EINVAL, "bad concat arguments");
     return concat_forward(rows, c_in, c_out, off, x, y, static_cast<hipStream_t>(stream));
 }
@@ -422,7 +425,7 @@ extern "C" int dc_concat_forward(int64_t rows, int32_t c_in, int32_t c_out, int3
 extern "C" int dc_concat_backward(int64_t rows, int32_t c_in, int32_t c_out, int32_t off, const float *dy,
                                   int accumulate, float *dx, void *stream) {
     clear_error();
-    if (rows < 0 || c_in < 1 || off < 0 || off + c_in > c_out || (rows > 0 && (!dy || !dx)))
+    if (rows < 0 || c_in < 1 || off < 0 || (int64_t)off + c_in > c_out || (rows > 0 && (!dy || !dx)))
         return fail(DC_EINVAL, "bad concat arguments");
     return concat_backward(rows, c_in, c_out, off, dy, accumulate, dx, static_cast<hipStream_t>(stream));
 }
@@ -430,7 +433,7 @@ extern "C" int dc_concat_backward(int64_t rows, int32_t c_in, int32_t c_out, int
 extern "C" int dc_concat_backward_relu(int64_t rows, int32_t c_in, int32_t c_out, int32_t off, const float *dy,
                                        const float *relu_y, int accumulate, float *dx, void *stream) {
     clear_error();
-    if (rows < 0 || c_in < 1 || off < 0 || off + c_in > c_out || (rows > 0 && (!dy || !relu_y || !dx)))
+    if (rows < 0 || c_in < 1 || off < 0 || (int64_t)off + c_in > c_out || (rows > 0 && (!dy || !relu_y || !dx)))
         return fail(DC_EINVAL, "bad concat arguments");
     return concat_backward(rows, c_in, c_out, off, dy, accumulate, dx, static_cast<hipStream_t>(stream), relu_y);
 }

@@ -978,16 +978,21 @@ bool conv_geom_from_shape(const dc_conv_shape &sh, ConvGeom *g) {
     if (sh.n < 0 || sh.h < 1 || sh.w < 1 || sh.c < 1 || sh.k < 1 || sh.r < 1 || sh.s < 1 ||
         sh.stride < 1 || sh.pad < 0 || sh.pad >= sh.r || sh.pad_w < 0 || sh.pad_w >= sh.s)
         return false;
-    if (sh.h + 2 * sh.pad < sh.r || sh.w + 2 * sh.pad_w < sh.s)
+    // padded extents in 64 bits: pad is bounded only by the filter size
+    const int64_t hp = (int64_t)sh.h + 2 * (int64_t)sh.pad, wp = (int64_t)sh.w + 2 * (int64_t)sh.pad_w;
+    if (hp < sh.r || wp < sh.s)
+        return false;
+    const int64_t P = (hp - sh.r) / sh.stride + 1, Q = (wp - sh.s) / sh.stride + 1;
+    // every index the kernels form must stay below 2^31
+    const int64_t big = std::max<int64_t>({(int64_t)sh.n * sh.h * sh.w * sh.c, (int64_t)sh.n * P * Q * sh.k,
+                                           (int64_t)sh.k * sh.r * sh.s * sh.c, hp, wp});
+    if (big >= INT_MAX)
         return false;
     g->N = sh.n; g->H = sh.h; g->W = sh.w; g->C = sh.c; g->K = sh.k;
     g->R = sh.r; g->S = sh.s; g->st = sh.stride; g->pad = sh.pad; g->pad_w = sh.pad_w;
-    g->P = (sh.h + 2 * sh.pad - sh.r) / sh.stride + 1;
-    g->Q = (sh.w + 2 * sh.pad_w - sh.s) / sh.stride + 1;
-    // every index the kernels form must stay below 2^31
-    int64_t big = std::max<int64_t>({(int64_t)sh.n * sh.h * sh.w * sh.c, (int64_t)sh.n * g->P * g->Q * sh.k,
-                                     (int64_t)sh.k * sh.r * sh.s * sh.c});
-    return big < INT_MAX;
+    g->P = (int)P;
+    g->Q = (int)Q;
+    return true;
 }
 
 // force (mt, nt, splits), if given, restricts the choice to that plan; the

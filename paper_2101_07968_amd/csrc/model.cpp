@@ -11,6 +11,7 @@
 #include "runtime.h"
 
 #include <algorithm>
+#include <climits>
 #include <cstring>
 
 namespace dc {
@@ -24,6 +25,9 @@ int check_desc(const dc_op_desc *ops, int n_ops, int batch, int in_h, int in_w, 
         return fail(DC_EINVAL, "no operations");
     if (batch < 1 || in_h < 1 || in_w < 1 || in_c < 1 || classes < 1)
         return fail(DC_EINVAL, "batch and input sizes must be positive");
+    if ((int64_t)batch * in_h * in_w * in_c >= INT_MAX)
+        return fail(DC_EINVAL, "input batch of %lld elements (the limit is 2^31 - 1)",
+                    (long long)batch * in_h * in_w * in_c);
     int prev_layer = 0;
     for (int i = 0; i < n_ops; ++i) {
         const dc_op_desc &d = ops[i];
@@ -128,9 +132,9 @@ static int build_model(dc_model *m, const dc_op_desc *ops, int n_ops) {
             break;
         case DC_OP_MAXPOOL:
         case DC_OP_AVGPOOL: {
-            if (o.d.r < 1 || o.d.s < 1 || o.d.stride < 1 || o.d.pad < 0 || o.d.pad >= o.d.r || o.d.pad >= o.d.s ||
-                o.d.r * o.d.s > 256 || in.h + 2 * o.d.pad < o.d.r || in.w + 2 * o.d.pad < o.d.s ||
-                o.d.pad_w != o.d.pad)
+            if (o.d.r < 1 || o.d.s < 1 || o.d.r > 256 || o.d.s > 256 || o.d.stride < 1 || o.d.pad < 0 ||
+                o.d.pad >= o.d.r || o.d.pad >= o.d.s || o.d.r * o.d.s > 256 || in.h + 2 * o.d.pad < o.d.r ||
+                in.w + 2 * o.d.pad < o.d.s || o.d.pad_w != o.d.pad)
                 return fail(DC_EINVAL, "op %d: invalid pooling geometry (pad_w must equal pad)", i);
             o.pool = dc_pool_shape{in.n, in.h, in.w, in.c, o.d.r, o.d.s, o.d.stride, o.d.pad};
             out.h = (in.h + 2 * o.d.pad - o.d.r) / o.d.stride + 1;
@@ -147,18 +151,24 @@ static int build_model(dc_model *m, const dc_op_desc *ops, int n_ops) {
             break;
         }
         case DC_OP_CONCAT: {
-            int c = 0;
+            int64_t c = 0;
             for (int k = 0; k < o.n_in; ++k) {
                 const TensorInfo &b = m->tensors[o.in[k]];
                 if (b.n != in.n || b.h != in.h || b.w != in.w)
                     return fail(DC_EINVAL, "op %d: CONCAT inputs differ in n, h or w", i);
-                o.ch_off[k] = c;
+                o.ch_off[k] = (int)c;
                 c += b.c;
             }
-            out.c = c;
+            if (c >= INT_MAX)
+                return fail(DC_EINVAL, "op %d: CONCAT output has too many channels", i);
+            out.c = (int)c;
             break;
         }
         }
+        // every tensor is indexed with 32-bit element offsets somewhere
+        if (out.size() >= INT_MAX)
+            return fail(DC_EINVAL, "op %d: output tensor of %lld elements (the limit is 2^31 - 1)", i,
+                        (long long)out.size());
         m->layer_cnt[l] += poff - start;
         m->tensors[o.out] = out;
     }

@@ -163,6 +163,32 @@ def test_model_validation_rejects_bad_descriptions():
         assert b"pad_w" in D.lib().dc_last_error()
 
 
+def test_shape_checks_do_not_overflow():
+    """Sizes whose 32-bit products or sums would wrap are refused before any launch."""
+    lib = D.lib()
+    # padded extent past 2^31: h + 2 pad overflows int
+    sh = D.ConvShape(1, 2 ** 31 - 10, 1, 1, 1, 101, 1, 1, 100, 0)
+    assert lib.dc_conv2d_workspace_bytes(ctypes.byref(sh)) == 0
+    out = (ctypes.c_int32 * 8)()
+    assert lib.dc_conv2d_plan_info(ctypes.byref(sh), 0, out) == D.DC_EINVAL
+    # a pooling window of 65536 x 65536 taps: r * s wraps to 0 in 32 bits
+    ps = D.PoolShape(0, 65536, 65536, 1, 65536, 65536, 1, 0)
+    assert lib.dc_maxpool_forward(ctypes.byref(ps), None, None, None, None) == D.DC_EINVAL
+    assert lib.dc_avgpool_forward(ctypes.byref(ps), None, None, None) == D.DC_EINVAL
+    # channel offset + width past 2^31
+    for fn in ("dc_concat_forward", "dc_concat_backward"):
+        args = [0, 1, 10, 2 ** 31 - 1, None] + ([0] if fn == "dc_concat_backward" else []) + [None, None]
+        assert getattr(lib, fn)(*args) == D.DC_EINVAL, fn
+    # a concatenation of two 2^30-channel tensors: 2^31 channels
+    big = (D.DC_OP_CONV, 1, 0, -1, 2 ** 30, 1, 1, 1, 0, 0)
+    st, _ = _create([big, big, (D.DC_OP_CONCAT, 1, 1, 2, 0, 0, 0, 0, 0, 0, -1, -1, 0),
+                     (D.DC_OP_FC, 2, 3, -1, 10, 0, 0, 0, 0, 1)], batch=1, hwc=(1, 1, 1))
+    assert st == D.DC_EINVAL and b"channels" in lib.dc_last_error()
+    # an input batch of 2^31 elements
+    assert _create([(D.DC_OP_FC, 1, 0, -1, 10, 0, 0, 0, 0, 1)], batch=2, hwc=(32768, 32768, 1))[0] == D.DC_EINVAL
+    assert b"input batch" in lib.dc_last_error()
+
+
 @pytest.mark.parametrize("block", range(10))
 def test_ibatch_bit_exact(block):
     for i in range(100):
