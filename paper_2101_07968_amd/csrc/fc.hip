@@ -9,7 +9,7 @@
 // moves the O x I weights once and little else: 2 M flops per 4 weight
 // bytes, near the balance point of HBM and the fp32 matrix cores.  This
 // kernel streams W straight from HBM into registers, in rows of 512
-// contiguous bytes per half-wave, with no LDS staging and no barriers:
+// contiguous bytes per half-wave, with no LDS staging of the operands:
 //
 // * v_mfma_f32_32x32x2f32 takes, per lane l, one element of a 32 x 2 block
 //   of A (row l % 32, k = l / 32) and of a 2 x 32 block of B (k = l / 32,
@@ -24,8 +24,14 @@
 //   loads whose out-of-range offsets read as zero, which masks the ragged
 //   edges without a branch around a load.
 //
-// The reduction over o is split over waves: fixed-slot partial sums, then a
-// fixed-order reduction that applies a folded ReLU's mask and the
+// * The four waves of a workgroup share one 128-column strip and take
+//   interleaved groups of 8 rows, so a workgroup reads 32 consecutive rows of
+//   the strip per round (measured on 25088 -> 4096 at 32 rows: 97 us, against
+//   104 us with the waves on neighbouring strips); the waves' sums are then
+//   added in wave order through LDS.
+//
+// The reduction over o is split over workgroups: fixed-slot partial sums,
+// then a fixed-order reduction that applies a folded ReLU's mask and the
 // accumulate flag, so results are deterministic.
 //
 // The forward pass of such a layer has its own kernel here too:
@@ -50,7 +56,7 @@ namespace {
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 constexpr int WAVES = 4;              // waves per workgroup
-constexpr int TARGET_WAVES = 2048;    // 2 per SIMD on 256 CUs, each with two steps of loads in flight
+constexpr int TARGET_WGS = 1152;      // data gradient: about 4.5 workgroups of 4 waves per CU
 constexpr unsigned OOB = 0x80000000u; // a byte offset that reads as zero
 constexpr int64_t FWD_MIN = 16000000; // weights from which the forward kernel runs
 
@@ -70,17 +76,18 @@ __device__ __forceinline__ float el(const float4 &v, int e) {
     return e == 0 ? v.x : (e == 1 ? v.y : (e == 2 ? v.z : v.w));
 }
 
-// One wave: columns i0 .. i0+127 for rows 0 .. M-1 (M <= 32), over the o
-// range of split `sp` (ochunk rows, a multiple of 24); partial[sp][m][i].
+// One workgroup: columns i0 .. i0+127 for rows 0 .. M-1 (M <= 32), over the o
+// range of split `sp` (ochunk rows, a multiple of 96).  The o range is taken
+// in rounds of 32 rows, wave w reading rows 8w .. 8w+7 of each round, so the
+// four waves stream one 512-byte strip of 32 consecutive weight rows; their
+// sums are added in wave order through LDS.  partial[sp][m][i].
 __global__ __launch_bounds__(64 * WAVES) void fc_dgrad_kernel(const float *__restrict__ dY,
                                                               const float *__restrict__ W,
                                                               float *__restrict__ partial, int M, int I, int O,
-                                                              int tiles_i, int splits, int ochunk) {
-    const int wave = blockIdx.x * WAVES + (threadIdx.x >> 6);
-    if (wave >= tiles_i * splits)
-        return;
-    const int lane = threadIdx.x & 63, j = lane & 31, h = lane >> 5;
-    const int tile = wave % tiles_i, sp = wave / tiles_i;
+                                                              int tiles_i, int ochunk) {
+    __shared__ float red[64 * 64];
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, j = lane & 31, h = lane >> 5;
+    const int tile = blockIdx.x % tiles_i, sp = blockIdx.x / tiles_i;
     const int i = tile * 128 + 4 * j;
     const bool iok = i < I;
     const int ob = sp * ochunk, oe = min(O, ob + ochunk);
@@ -97,7 +104,7 @@ __global__ __launch_bounds__(64 * WAVES) void fc_dgrad_kernel(const float *__res
         float4 w[4], a;
     };
     auto load = [&](Buf &b, int o0) {
-        const int oa = o0 + 4 * h;
+        const int oa = o0 + 8 * wave + 4 * h;
 #pragma unroll
         for (int u = 0; u < 4; ++u)
             b.w[u] = ld4_sel(rw, (int64_t)(oa + u) * I + i, iok && oa + u < oe);
@@ -118,28 +125,43 @@ __global__ __launch_bounds__(64 * WAVES) void fc_dgrad_kernel(const float *__res
             for (int e = 0; e < 4; ++e)
                 acc[e] = __builtin_amdgcn_mfma_f32_32x32x2f32(el(b.a, u), el(b.w[u], e), acc[e], 0, 0, 0);
     };
-    // steps past oe load zeros and add nothing
+    // rounds past oe load zeros and add nothing
     Buf b0, b1, b2;
     load(b0, ob);
-    load(b1, ob + 8);
-    for (int o0 = ob; o0 < oe; o0 += 24) {
-        load(b2, o0 + 16);
+    load(b1, ob + 32);
+    for (int o0 = ob; o0 < oe; o0 += 96) {
+        load(b2, o0 + 64);
         step(b0);
-        load(b0, o0 + 24);
+        load(b0, o0 + 96);
         step(b1);
-        load(b1, o0 + 32);
+        load(b1, o0 + 128);
         step(b2);
+    }
+    // the waves in order: red = ((w0 + w1) + w2) + w3, element by element
+    for (int wv = 0; wv < WAVES; ++wv) {
+        if (wave == wv)
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) {
+                    float &r = red[(e * 16 + v) * 64 + lane];
+                    r = wv == 0 ? acc[e][v] : r + acc[e][v];
+                }
+        __syncthreads();
     }
     if (!iok)
         return;
-    // element v of lane l is row 8*(v/4) + 4*(l/32) + v%4 of a 32 x 32 block
+    // element v of lane l is row 8*(v/4) + 4*(l/32) + v%4 of a 32 x 32 block;
+    // wave w writes the rows of v = 4w .. 4w+3
     float *dst = partial + (size_t)sp * M * I;
 #pragma unroll
-    for (int v = 0; v < 16; ++v) {
+    for (int vv = 0; vv < 4; ++vv) {
+        const int v = 4 * wave + vv;
         const int m = 8 * (v >> 2) + 4 * h + (v & 3);
         if (m < M)
             *reinterpret_cast<float4 *>(dst + (size_t)m * I + i) =
-                make_float4(acc[0][v], acc[1][v], acc[2][v], acc[3][v]);
+                make_float4(red[(0 * 16 + v) * 64 + lane], red[(1 * 16 + v) * 64 + lane],
+                            red[(2 * 16 + v) * 64 + lane], red[(3 * 16 + v) * 64 + lane]);
     }
 }
 
@@ -271,7 +293,7 @@ bool fc_streaming(const ConvGeom &g, int pass) {
     const int64_t weights = (int64_t)g.K * g.C;
     // Measured on MI355X against the implicit GEMM's plans (VGG-16's and
     // AlexNet's FC layers at 32 rows): the streaming data gradient wins from
-    // about 4 M weights (25088 -> 4096: 106 against 133 us); the forward from
+    // about 4 M weights (25088 -> 4096: 97 against 133 us); the forward from
     // about 16 M (25088 -> 4096: 97 against 119 us, 9216 -> 4096: 39 against
     // 51, 4096 -> 4096: 25 against 28.5) and loses below (4096 -> 1000: 28
     // against 14).
@@ -282,9 +304,9 @@ bool fc_streaming(const ConvGeom &g, int pass) {
     return false;
 }
 
-// Data gradient: splits of the reduction over o, about TARGET_WAVES waves in
-// chunks of 24 rows (the ring's three steps), while the partial sums (splits
-// x M x I) stay within a quarter of the weight bytes.  Forward: about 768
+// Data gradient: splits of the reduction over o, about TARGET_WGS workgroups
+// in chunks of 96 rows (the ring's three rounds of 32), while the partial sums
+// (splits x M x I) stay within a quarter of the weight bytes.  Forward: about 768
 // workgroups (three per CU), splits of the reduction over i in whole LDS
 // stages.
 void fc_plan(const ConvGeom &g, int pass, int splits_out[1], int *chunk, size_t *ws_bytes) {
@@ -299,12 +321,12 @@ void fc_plan(const ConvGeom &g, int pass, int splits_out[1], int *chunk, size_t 
         return;
     }
     const int64_t tiles = (I + 127) / 128;
-    const int64_t steps = (O + 23) / 24;
-    int64_t s = std::max<int64_t>(1, (TARGET_WAVES + tiles - 1) / tiles);
+    const int64_t steps = (O + 95) / 96;
+    int64_t s = std::max<int64_t>(1, (TARGET_WGS + tiles - 1) / tiles);
     s = std::min<int64_t>(s, std::max<int64_t>(1, O / (4 * M)));
     s = std::min<int64_t>(s, steps);
     const int64_t per = (steps + s - 1) / s;
-    *chunk = (int)(per * 24);
+    *chunk = (int)(per * 96);
     splits_out[0] = (int)((steps + per - 1) / per);
     *ws_bytes = (size_t)splits_out[0] * M * I * sizeof(float);
 }
@@ -333,8 +355,7 @@ int fc_dgrad(const ConvGeom &g, int splits, int chunk, const float *dy, const fl
         return fail(DC_EINVAL, "FC dgrad needs a workspace");
     float *partial = static_cast<float *>(ws);
     const int tiles = (I + 127) / 128;
-    const int grid = (int)(((int64_t)tiles * splits + WAVES - 1) / WAVES);
-    hipLaunchKernelGGL(fc_dgrad_kernel, dim3(grid), dim3(64 * WAVES), 0, s, dy, w, partial, M, I, O, tiles, splits,
+    hipLaunchKernelGGL(fc_dgrad_kernel, dim3(tiles * splits), dim3(64 * WAVES), 0, s, dy, w, partial, M, I, O, tiles,
                        chunk);
     DC_HIP(hipGetLastError());
     const int64_t n4 = (int64_t)M * I / 4;
