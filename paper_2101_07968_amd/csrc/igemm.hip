@@ -136,7 +136,9 @@ __device__ __forceinline__ float4 bld4(__amdgpu_buffer_rsrc_t r, unsigned elem_o
 // Address of output row m of a pass in its destination tensor (row-major
 // [rows][Ng] for FWD / WGRAD, the NHWC pixel of the phase for DGRAD).
 __device__ __forceinline__ size_t out_row(const Args &a, int pass, const Phase &ph, int z, int m) {
-    if (pass != PASS_DGRAD)
+    // a stride-1 data gradient has one phase holding every pixel in NHWC order,
+    // so its rows are the pixels themselves (no division per row)
+    if (pass != PASS_DGRAD || a.st == 1)
         return (size_t)m * a.Ng;
     int hw = ph.Hh * ph.Wh;
     int n = m / hw;
