@@ -48,7 +48,7 @@ struct FDiv {
     }
 };
 
-FDiv make_fdiv(uint32_t d) {
+__host__ __device__ FDiv make_fdiv(uint32_t d) {
     FDiv f;
     f.d = d;
     if (d <= 1) {
@@ -86,6 +86,7 @@ struct Phase {
     int r0, s0;     // first tap
     int dh, dw;     // p = i + dh - tr, q = j + dw - ts
     int M, Kg;
+    FDiv fW, fHW;   // stride > 1: division by Wh and by Hh * Wh
 };
 
 __device__ __forceinline__ Phase make_phase(const Args &a, int z) {
@@ -101,6 +102,10 @@ __device__ __forceinline__ Phase make_phase(const Args &a, int z) {
     ph.dw = (rw + a.pad_w - ph.s0) / a.st;
     ph.M = a.N * ph.Hh * ph.Wh;
     ph.Kg = ph.Rt * ph.St * a.K;
+    if (a.st > 1) { // out_row decodes rows of this phase
+        ph.fW = make_fdiv((uint32_t)ph.Wh);
+        ph.fHW = make_fdiv((uint32_t)(ph.Hh * ph.Wh));
+    }
     return ph;
 }
 
@@ -140,11 +145,10 @@ __device__ __forceinline__ size_t out_row(const Args &a, int pass, const Phase &
     // so its rows are the pixels themselves (no division per row)
     if (pass != PASS_DGRAD || a.st == 1)
         return (size_t)m * a.Ng;
-    int hw = ph.Hh * ph.Wh;
-    int n = m / hw;
-    int rem = m - n * hw;
-    int i = rem / ph.Wh;
-    int j = rem - i * ph.Wh;
+    const int n = (int)ph.fHW.div((uint32_t)m);
+    const int rem = m - n * (ph.Hh * ph.Wh);
+    const int i = (int)ph.fW.div((uint32_t)rem);
+    const int j = rem - i * ph.Wh;
     int h = z / a.st + a.st * i;
     int w = z % a.st + a.st * j;
     return (((size_t)n * a.H + h) * a.W + w) * a.C;
