@@ -33,6 +33,31 @@ void clear_error();
 // ---------------------------------------------------------------- conv / GEMM
 enum Pass { PASS_FWD = 0, PASS_DGRAD = 1, PASS_WGRAD = 2 };
 
+// Division by a runtime constant d via multiply-high (valid for n < 2^31):
+// the round-up method for unsigned division by an invariant integer.
+struct FDiv {
+    uint32_t d, m, s;
+    __device__ __forceinline__ uint32_t div(uint32_t n) const {
+        uint32_t hi = __umulhi(n, m);
+        return (uint32_t)(((uint64_t)hi + n) >> s);
+    }
+};
+
+inline __host__ __device__ FDiv make_fdiv(uint32_t d) {
+    FDiv f;
+    f.d = d;
+    if (d <= 1) {
+        f.m = 0;
+        f.s = 0;
+        return f;
+    }
+    uint32_t l = 32 - __builtin_clz(d - 1);
+    uint64_t one = 1;
+    f.m = (uint32_t)(((one << 32) * ((one << l) - d)) / d + 1);
+    f.s = l;
+    return f;
+}
+
 struct ConvGeom {
     int N, H, W, C, K, R, S, st, pad, pad_w, P, Q; // pad: rows; pad_w: columns
 };

@@ -256,16 +256,18 @@ __global__ void maxpool_bwd_kernel(dc_pool_shape sh, int P, int Q, const float *
 // output (forward) or input (backward) pixel, so the index arithmetic is
 // paid once per four channels and in 32 bits (the host checks the sizes).
 // Per channel they make exactly the decisions and sums of the scalar kernels.
-__global__ void maxpool_fwd4_kernel(dc_pool_shape sh, int P, int Q, int c4, int total4,
+// Element e of the float4 output is decoded with multiply-high divisions by
+// the invariant c4, Q and P (fc4, fQ, fP), not integer divisions.
+__global__ void maxpool_fwd4_kernel(dc_pool_shape sh, int P, int Q, int c4, int total4, FDiv fc4, FDiv fQ, FDiv fP,
                                     const float4 *__restrict__ x, float4 *__restrict__ y,
                                     uchar4 *__restrict__ arg) {
     for (int e = blockIdx.x * blockDim.x + threadIdx.x; e < total4; e += gridDim.x * blockDim.x) {
-        const int q4 = e % c4;
-        const int pix = e / c4;
-        const int q = pix % Q;
-        const int t = pix / Q;
-        const int p = t % P;
-        const int n = t / P;
+        const int pix = (int)fc4.div((uint32_t)e);
+        const int q4 = e - pix * c4;
+        const int t = (int)fQ.div((uint32_t)pix);
+        const int q = pix - t * Q;
+        const int n = (int)fP.div((uint32_t)t);
+        const int p = t - n * P;
         float bv[4] = {0.f, 0.f, 0.f, 0.f};
         int best[4] = {-1, -1, -1, -1};
         for (int r = 0; r < sh.r; ++r) {
@@ -294,21 +296,24 @@ __global__ void maxpool_fwd4_kernel(dc_pool_shape sh, int P, int Q, int c4, int 
 }
 
 template <bool MASK>
-__global__ void maxpool_bwd4_kernel(dc_pool_shape sh, int P, int Q, int c4, int total4,
-                                    const float4 *__restrict__ dy, const uchar4 *__restrict__ arg, int acc,
+// Element e of the float4 input gradient is decoded, and its window range
+// found, with multiply-high divisions by the invariant c4, W, H and stride.
+__global__ void maxpool_bwd4_kernel(dc_pool_shape sh, int P, int Q, int c4, int total4, FDiv fc4, FDiv fW, FDiv fH,
+                                    FDiv fst, const float4 *__restrict__ dy, const uchar4 *__restrict__ arg, int acc,
                                     float4 *__restrict__ dx, const float4 *__restrict__ y) {
     for (int e = blockIdx.x * blockDim.x + threadIdx.x; e < total4; e += gridDim.x * blockDim.x) {
-        const int q4 = e % c4;
-        const int pix = e / c4;
-        const int w = pix % sh.w;
-        const int t = pix / sh.w;
-        const int h = t % sh.h;
-        const int n = t / sh.h;
+        const int pix = (int)fc4.div((uint32_t)e);
+        const int q4 = e - pix * c4;
+        const int t = (int)fW.div((uint32_t)pix);
+        const int w = pix - t * sh.w;
+        const int n = (int)fH.div((uint32_t)t);
+        const int h = t - n * sh.h;
         const int hp = h + sh.pad, wp = w + sh.pad;
-        const int p_lo = hp - sh.r + 1 > 0 ? (hp - sh.r + 1 + sh.stride - 1) / sh.stride : 0;
-        const int p_hi = min(P - 1, hp / sh.stride);
-        const int q_lo = wp - sh.s + 1 > 0 ? (wp - sh.s + 1 + sh.stride - 1) / sh.stride : 0;
-        const int q_hi = min(Q - 1, wp / sh.stride);
+        // windows p with p * stride <= hp < p * stride + r (all operands >= 0)
+        const int p_lo = hp - sh.r + 1 > 0 ? (int)fst.div((uint32_t)(hp - sh.r + sh.stride)) : 0;
+        const int p_hi = min(P - 1, (int)fst.div((uint32_t)hp));
+        const int q_lo = wp - sh.s + 1 > 0 ? (int)fst.div((uint32_t)(wp - sh.s + sh.stride)) : 0;
+        const int q_hi = min(Q - 1, (int)fst.div((uint32_t)wp));
         float4 g = make_float4(0.f, 0.f, 0.f, 0.f);
         for (int p = p_lo; p <= p_hi; ++p)
             for (int q = q_lo; q <= q_hi; ++q) {
@@ -959,8 +964,8 @@ int maxpool_forward(const dc_pool_shape &sh, const float *x, float *y, uint8_t *
     if (pool4_ok(sh, P, Q, x, y, arg)) {
         const int total4 = (int)(total / 4);
         hipLaunchKernelGGL(maxpool_fwd4_kernel, dim3(ew_blocks(total4)), dim3(EW_THREADS), 0, s, sh, P, Q, sh.c / 4,
-                           total4, reinterpret_cast<const float4 *>(x), reinterpret_cast<float4 *>(y),
-                           reinterpret_cast<uchar4 *>(arg));
+                           total4, make_fdiv(sh.c / 4), make_fdiv(Q), make_fdiv(P), reinterpret_cast<const float4 *>(x),
+                           reinterpret_cast<float4 *>(y), reinterpret_cast<uchar4 *>(arg));
     } else {
         hipLaunchKernelGGL(maxpool_fwd_kernel, dim3(ew_blocks(total)), dim3(EW_THREADS), 0, s, sh, P, Q, x, y, arg);
     }
@@ -981,12 +986,13 @@ int maxpool_backward(const dc_pool_shape &sh, const float *dy, const uint8_t *ar
         const auto *arg4 = reinterpret_cast<const uchar4 *>(arg);
         const auto *y4 = reinterpret_cast<const float4 *>(relu_y);
         auto *dx4 = reinterpret_cast<float4 *>(dx);
+        const FDiv fc4 = make_fdiv(sh.c / 4), fW = make_fdiv(sh.w), fH = make_fdiv(sh.h), fst = make_fdiv(sh.stride);
         if (relu_y)
             hipLaunchKernelGGL(maxpool_bwd4_kernel<true>, dim3(ew_blocks(total4)), dim3(EW_THREADS), 0, s, sh, P, Q,
-                               sh.c / 4, total4, dy4, arg4, accumulate, dx4, y4);
+                               sh.c / 4, total4, fc4, fW, fH, fst, dy4, arg4, accumulate, dx4, y4);
         else
             hipLaunchKernelGGL(maxpool_bwd4_kernel<false>, dim3(ew_blocks(total4)), dim3(EW_THREADS), 0, s, sh, P, Q,
-                               sh.c / 4, total4, dy4, arg4, accumulate, dx4, y4);
+                               sh.c / 4, total4, fc4, fW, fH, fst, dy4, arg4, accumulate, dx4, y4);
     } else if (relu_y) {
         hipLaunchKernelGGL(maxpool_bwd_kernel<true>, dim3(ew_blocks(total)), dim3(EW_THREADS), 0, s, sh, P, Q, dy, arg,
                            accumulate, dx, relu_y);

@@ -39,30 +39,6 @@ constexpr int NTHR = 256;
 constexpr int PADK = 4;  // padding of k-contiguous LDS rows (floats)
 constexpr int PADR = 4;  // padding of row-contiguous LDS rows (floats)
 
-// Division by a runtime constant d via multiply-high (valid for n < 2^31).
-struct FDiv {
-    uint32_t d, m, s;
-    __device__ __forceinline__ uint32_t div(uint32_t n) const {
-        uint32_t hi = __umulhi(n, m);
-        return (uint32_t)(((uint64_t)hi + n) >> s);
-    }
-};
-
-__host__ __device__ FDiv make_fdiv(uint32_t d) {
-    FDiv f;
-    f.d = d;
-    if (d <= 1) {
-        f.m = 0;
-        f.s = 0;
-        return f;
-    }
-    uint32_t l = 32 - __builtin_clz(d - 1);
-    uint64_t one = 1;
-    f.m = (uint32_t)(((one << 32) * ((one << l) - d)) / d + 1);
-    f.s = l;
-    return f;
-}
-
 struct Args {
     int N, H, W, C, K, R, S, st, pad, pad_w, P, Q;
     int M, Ng, Kg;          // FWD / WGRAD sizes; DGRAD: maxima over phases
