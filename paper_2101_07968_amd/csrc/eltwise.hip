@@ -138,13 +138,15 @@ __global__ void copy_grad_kernel(const float *__restrict__ dy, int acc, float *_
 
 // Channel slice copies: a thread per float4 (or float) of the slice, rows
 // outermost, so consecutive threads touch consecutive channels of one row.
-template <int V>
-__global__ void concat_kernel(int64_t rows, int c_in, int c_out, int off, const float *__restrict__ x,
+// With I32 (fewer than 2^31 slice elements) the row is found by a multiply-high
+// division by cv (fcv); else by a 64-bit division.
+template <int V, bool I32>
+__global__ void concat_kernel(int64_t rows, int c_in, int c_out, int off, FDiv fcv, const float *__restrict__ x,
                               float *__restrict__ y) {
     const int cv = c_in / V;
     const int64_t total = rows * cv;
     for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total; e += (int64_t)gridDim.x * blockDim.x) {
-        int64_t m = e / cv;
+        const int64_t m = I32 ? (int64_t)fcv.div((uint32_t)e) : e / cv;
         int c = (int)(e - m * cv) * V;
         if (V == 4)
             *reinterpret_cast<float4 *>(y + m * c_out + off + c) = *reinterpret_cast<const float4 *>(x + m * c_in + c);
@@ -156,13 +158,13 @@ __global__ void concat_kernel(int64_t rows, int c_in, int c_out, int off, const 
 // relu_y (may be null, laid out like dx): dx is the gradient of the input of
 // a ReLU whose output was this concatenation's input; dy is kept where
 // relu_y > 0.
-template <int V>
-__global__ void concat_bwd_kernel(int64_t rows, int c_in, int c_out, int off, const float *__restrict__ dy, int acc,
-                                  float *__restrict__ dx, const float *__restrict__ relu_y) {
+template <int V, bool I32>
+__global__ void concat_bwd_kernel(int64_t rows, int c_in, int c_out, int off, FDiv fcv, const float *__restrict__ dy,
+                                  int acc, float *__restrict__ dx, const float *__restrict__ relu_y) {
     const int cv = c_in / V;
     const int64_t total = rows * cv;
     for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total; e += (int64_t)gridDim.x * blockDim.x) {
-        int64_t m = e / cv;
+        const int64_t m = I32 ? (int64_t)fcv.div((uint32_t)e) : e / cv;
         int c = (int)(e - m * cv) * V;
         if (V == 4) {
             float4 g = *reinterpret_cast<const float4 *>(dy + m * c_out + off + c);
@@ -351,15 +353,15 @@ __device__ __forceinline__ int pool_count(const dc_pool_shape &sh, int p, int q)
 }
 
 template <int V>
-__global__ void avgpool_fwd_kernel(dc_pool_shape sh, int P, int Q, int cv, int total, const float *__restrict__ x,
-                                   float *__restrict__ y) {
+__global__ void avgpool_fwd_kernel(dc_pool_shape sh, int P, int Q, int cv, int total, FDiv fcv, FDiv fQ, FDiv fP,
+                                   const float *__restrict__ x, float *__restrict__ y) {
     using T = typename std::conditional<V == 4, float4, float>::type;
     const T *xv = reinterpret_cast<const T *>(x);
     T *yv = reinterpret_cast<T *>(y);
     for (int e = blockIdx.x * blockDim.x + threadIdx.x; e < total; e += gridDim.x * blockDim.x) {
-        const int qc = e % cv, pix = e / cv;
-        const int q = pix % Q, t = pix / Q;
-        const int p = t % P, n = t / P;
+        const int pix = (int)fcv.div((uint32_t)e), qc = e - pix * cv;
+        const int t = (int)fQ.div((uint32_t)pix), q = pix - t * Q;
+        const int n = (int)fP.div((uint32_t)t), p = t - n * P;
         float acc[4] = {0.f, 0.f, 0.f, 0.f};
         for (int r = 0; r < sh.r; ++r) {
             const int h = p * sh.stride + r - sh.pad;
@@ -386,20 +388,20 @@ __global__ void avgpool_fwd_kernel(dc_pool_shape sh, int P, int Q, int cv, int t
 }
 
 template <int V>
-__global__ void avgpool_bwd_kernel(dc_pool_shape sh, int P, int Q, int cv, int total, const float *__restrict__ dy,
-                                   int acc_in, float *__restrict__ dx) {
+__global__ void avgpool_bwd_kernel(dc_pool_shape sh, int P, int Q, int cv, int total, FDiv fcv, FDiv fW, FDiv fH,
+                                   FDiv fst, const float *__restrict__ dy, int acc_in, float *__restrict__ dx) {
     using T = typename std::conditional<V == 4, float4, float>::type;
     const T *dv = reinterpret_cast<const T *>(dy);
     T *xv = reinterpret_cast<T *>(dx);
     for (int e = blockIdx.x * blockDim.x + threadIdx.x; e < total; e += gridDim.x * blockDim.x) {
-        const int qc = e % cv, pix = e / cv;
-        const int w = pix % sh.w, t = pix / sh.w;
-        const int h = t % sh.h, n = t / sh.h;
+        const int pix = (int)fcv.div((uint32_t)e), qc = e - pix * cv;
+        const int t = (int)fW.div((uint32_t)pix), w = pix - t * sh.w;
+        const int n = (int)fH.div((uint32_t)t), h = t - n * sh.h;
         const int hp = h + sh.pad, wp = w + sh.pad;
-        const int p_lo = hp - sh.r + 1 > 0 ? (hp - sh.r + 1 + sh.stride - 1) / sh.stride : 0;
-        const int p_hi = min(P - 1, hp / sh.stride);
-        const int q_lo = wp - sh.s + 1 > 0 ? (wp - sh.s + 1 + sh.stride - 1) / sh.stride : 0;
-        const int q_hi = min(Q - 1, wp / sh.stride);
+        const int p_lo = hp - sh.r + 1 > 0 ? (int)fst.div((uint32_t)(hp - sh.r + sh.stride)) : 0;
+        const int p_hi = min(P - 1, (int)fst.div((uint32_t)hp));
+        const int q_lo = wp - sh.s + 1 > 0 ? (int)fst.div((uint32_t)(wp - sh.s + sh.stride)) : 0;
+        const int q_hi = min(Q - 1, (int)fst.div((uint32_t)wp));
         float g[4] = {0.f, 0.f, 0.f, 0.f};
         for (int p = p_lo; p <= p_hi; ++p)
             for (int q = q_lo; q <= q_hi; ++q) {
@@ -924,12 +926,24 @@ static bool concat_vec(int c_in, int c_out, int off, const void *a, const void *
 int concat_forward(int64_t rows, int c_in, int c_out, int off, const float *x, float *y, hipStream_t s) {
     if (rows <= 0 || c_in <= 0)
         return DC_OK;
-    if (concat_vec(c_in, c_out, off, x, y))
-        hipLaunchKernelGGL(concat_kernel<4>, dim3(ew_blocks(rows * c_in, 4)), dim3(EW_THREADS), 0, s, rows, c_in,
-                           c_out, off, x, y);
-    else
-        hipLaunchKernelGGL(concat_kernel<1>, dim3(ew_blocks(rows * c_in)), dim3(EW_THREADS), 0, s, rows, c_in, c_out,
-                           off, x, y);
+    const bool i32 = rows * c_in < INT_MAX;
+    if (concat_vec(c_in, c_out, off, x, y)) {
+        const FDiv f = make_fdiv(c_in / 4);
+        if (i32)
+            hipLaunchKernelGGL((concat_kernel<4, true>), dim3(ew_blocks(rows * c_in, 4)), dim3(EW_THREADS), 0, s, rows,
+                               c_in, c_out, off, f, x, y);
+        else
+            hipLaunchKernelGGL((concat_kernel<4, false>), dim3(ew_blocks(rows * c_in, 4)), dim3(EW_THREADS), 0, s, rows,
+                               c_in, c_out, off, f, x, y);
+    } else {
+        const FDiv f = make_fdiv(c_in);
+        if (i32)
+            hipLaunchKernelGGL((concat_kernel<1, true>), dim3(ew_blocks(rows * c_in)), dim3(EW_THREADS), 0, s, rows,
+                               c_in, c_out, off, f, x, y);
+        else
+            hipLaunchKernelGGL((concat_kernel<1, false>), dim3(ew_blocks(rows * c_in)), dim3(EW_THREADS), 0, s, rows,
+                               c_in, c_out, off, f, x, y);
+    }
     DC_HIP(hipGetLastError());
     return DC_OK;
 }
@@ -938,12 +952,24 @@ int concat_backward(int64_t rows, int c_in, int c_out, int off, const float *dy,
                     hipStream_t s, const float *relu_y) {
     if (rows <= 0 || c_in <= 0)
         return DC_OK;
-    if (concat_vec(c_in, c_out, off, dy, dx) && al16(relu_y))
-        hipLaunchKernelGGL(concat_bwd_kernel<4>, dim3(ew_blocks(rows * c_in, 4)), dim3(EW_THREADS), 0, s, rows, c_in,
-                           c_out, off, dy, accumulate, dx, relu_y);
-    else
-        hipLaunchKernelGGL(concat_bwd_kernel<1>, dim3(ew_blocks(rows * c_in)), dim3(EW_THREADS), 0, s, rows, c_in,
-                           c_out, off, dy, accumulate, dx, relu_y);
+    const bool i32 = rows * c_in < INT_MAX;
+    if (concat_vec(c_in, c_out, off, dy, dx) && al16(relu_y)) {
+        const FDiv f = make_fdiv(c_in / 4);
+        if (i32)
+            hipLaunchKernelGGL((concat_bwd_kernel<4, true>), dim3(ew_blocks(rows * c_in, 4)), dim3(EW_THREADS), 0, s,
+                               rows, c_in, c_out, off, f, dy, accumulate, dx, relu_y);
+        else
+            hipLaunchKernelGGL((concat_bwd_kernel<4, false>), dim3(ew_blocks(rows * c_in, 4)), dim3(EW_THREADS), 0, s,
+                               rows, c_in, c_out, off, f, dy, accumulate, dx, relu_y);
+    } else {
+        const FDiv f = make_fdiv(c_in);
+        if (i32)
+            hipLaunchKernelGGL((concat_bwd_kernel<1, true>), dim3(ew_blocks(rows * c_in)), dim3(EW_THREADS), 0, s,
+                               rows, c_in, c_out, off, f, dy, accumulate, dx, relu_y);
+        else
+            hipLaunchKernelGGL((concat_bwd_kernel<1, false>), dim3(ew_blocks(rows * c_in)), dim3(EW_THREADS), 0, s,
+                               rows, c_in, c_out, off, f, dy, accumulate, dx, relu_y);
+    }
     DC_HIP(hipGetLastError());
     return DC_OK;
 }
@@ -1014,10 +1040,10 @@ int avgpool_forward(const dc_pool_shape &sh, const float *x, float *y, hipStream
         return fail(DC_EINVAL, "average pooling of %lld elements exceeds the 2^31 limit", (long long)total);
     if (sh.c % 4 == 0 && ((uintptr_t)x & 15) == 0 && ((uintptr_t)y & 15) == 0)
         hipLaunchKernelGGL(avgpool_fwd_kernel<4>, dim3(ew_blocks(total / 4)), dim3(EW_THREADS), 0, s, sh, P, Q,
-                           sh.c / 4, (int)(total / 4), x, y);
+                           sh.c / 4, (int)(total / 4), make_fdiv(sh.c / 4), make_fdiv(Q), make_fdiv(P), x, y);
     else
         hipLaunchKernelGGL(avgpool_fwd_kernel<1>, dim3(ew_blocks(total)), dim3(EW_THREADS), 0, s, sh, P, Q, sh.c,
-                           (int)total, x, y);
+                           (int)total, make_fdiv(sh.c), make_fdiv(Q), make_fdiv(P), x, y);
     DC_HIP(hipGetLastError());
     return DC_OK;
 }
@@ -1032,10 +1058,12 @@ int avgpool_backward(const dc_pool_shape &sh, const float *dy, int accumulate, f
         return fail(DC_EINVAL, "average pooling of %lld elements exceeds the 2^31 limit", (long long)total);
     if (sh.c % 4 == 0 && ((uintptr_t)dy & 15) == 0 && ((uintptr_t)dx & 15) == 0)
         hipLaunchKernelGGL(avgpool_bwd_kernel<4>, dim3(ew_blocks(total / 4)), dim3(EW_THREADS), 0, s, sh, P, Q,
-                           sh.c / 4, (int)(total / 4), dy, accumulate, dx);
+                           sh.c / 4, (int)(total / 4), make_fdiv(sh.c / 4), make_fdiv(sh.w), make_fdiv(sh.h),
+                           make_fdiv(sh.stride), dy, accumulate, dx);
     else
         hipLaunchKernelGGL(avgpool_bwd_kernel<1>, dim3(ew_blocks(total)), dim3(EW_THREADS), 0, s, sh, P, Q, sh.c,
-                           (int)total, dy, accumulate, dx);
+                           (int)total, make_fdiv(sh.c), make_fdiv(sh.w), make_fdiv(sh.h), make_fdiv(sh.stride), dy,
+                           accumulate, dx);
     DC_HIP(hipGetLastError());
     return DC_OK;
 }
