@@ -37,8 +37,8 @@ enum Pass { PASS_FWD = 0, PASS_DGRAD = 1, PASS_WGRAD = 2 };
 // the round-up method for unsigned division by an invariant integer.
 struct FDiv {
     uint32_t d, m, s;
-    __device__ __forceinline__ uint32_t div(uint32_t n) const {
-        uint32_t hi = __umulhi(n, m);
+    __host__ __device__ __forceinline__ uint32_t div(uint32_t n) const {
+        const uint32_t hi = (uint32_t)(((uint64_t)n * m) >> 32); // the high word of n * m
         return (uint32_t)(((uint64_t)hi + n) >> s);
     }
 };
