@@ -7,6 +7,7 @@
   plain, under ThreadSanitizer, and under AddressSanitizer + UBSan.
 * The planner (both DPs, iBatch, f_m) on random profiles up to L = 300 and
   near-overflow magnitudes under AddressSanitizer + UBSan.
+* The multiply-high division the kernels index with, against plain division.
 """
 import os
 import subprocess
@@ -48,5 +49,20 @@ def test_planner_under_sanitizers(tmp_path):
         pytest.fail(r.stderr)
     out = subprocess.run([exe, "3000"], capture_output=True, text=True, timeout=300,
                          env=dict(os.environ, ASAN_OPTIONS="halt_on_error=1"))
+    assert out.returncode == 0, (out.returncode, out.stdout, out.stderr[-3000:])
+    assert out.stdout.startswith("ok"), out.stdout
+
+
+def test_multiply_high_division(tmp_path):
+    """dc::FDiv, the division by an invariant integer behind the kernels' index
+    arithmetic, equals n / d for n < 2^31 (under UBSan)."""
+    exe = str(tmp_path / "fdiv_check")
+    r = subprocess.run(["g++", "-O1", "-g", "-std=c++17", "-D__HIP_PLATFORM_AMD__", "-I", "/opt/rocm/include",
+                        "-I", os.path.join(ROOT, "include"), "-I", CSRC,
+                        "-fsanitize=undefined", "-fno-sanitize-recover=undefined",
+                        os.path.join(ROOT, "tests", "fdiv_check.cpp"), "-o", exe], capture_output=True, text=True)
+    if r.returncode != 0:
+        pytest.fail(r.stderr)
+    out = subprocess.run([exe], capture_output=True, text=True, timeout=300)
     assert out.returncode == 0, (out.returncode, out.stdout, out.stderr[-3000:])
     assert out.stdout.startswith("ok"), out.stdout
