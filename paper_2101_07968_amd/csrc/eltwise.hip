@@ -439,12 +439,24 @@ __global__ void gap_fwd_kernel(int n, int hw, int c, const float *__restrict__ x
     }
 }
 
-__global__ void gap_bwd_kernel(int n, int hw, int c, const float *__restrict__ dy, int acc, float *__restrict__ dx) {
+// With I32 (fewer than 2^31 elements) the channel and image of element e come
+// from multiply-high divisions by c and hw (fc, fhw); else 64-bit divisions.
+template <bool I32>
+__global__ void gap_bwd_kernel(int n, int hw, int c, FDiv fc, FDiv fhw, const float *__restrict__ dy, int acc,
+                               float *__restrict__ dx) {
     int64_t total = (int64_t)n * hw * c;
     float inv = 1.0f / (float)hw;
     for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total; e += (int64_t)gridDim.x * blockDim.x) {
-        int ch = (int)(e % c);
-        int64_t b = e / ((int64_t)hw * c);
+        int ch;
+        int64_t b;
+        if (I32) {
+            const uint32_t q = fc.div((uint32_t)e); // pixel index b * hw + i
+            ch = (int)((uint32_t)e - q * (uint32_t)c);
+            b = fhw.div(q);
+        } else {
+            ch = (int)(e % c);
+            b = e / ((int64_t)hw * c);
+        }
         float g = dy[b * c + ch] * inv;
         dx[e] = acc ? dx[e] + g : g;
     }
@@ -1081,7 +1093,12 @@ int gap_backward(int n, int hw, int c, const float *dy, int accumulate, float *d
     int64_t total = (int64_t)n * hw * c;
     if (total <= 0)
         return DC_OK;
-    hipLaunchKernelGGL(gap_bwd_kernel, dim3(ew_blocks(total)), dim3(EW_THREADS), 0, s, n, hw, c, dy, accumulate, dx);
+    if (total < INT_MAX)
+        hipLaunchKernelGGL(gap_bwd_kernel<true>, dim3(ew_blocks(total)), dim3(EW_THREADS), 0, s, n, hw, c, make_fdiv(c),
+                           make_fdiv(hw), dy, accumulate, dx);
+    else
+        hipLaunchKernelGGL(gap_bwd_kernel<false>, dim3(ew_blocks(total)), dim3(EW_THREADS), 0, s, n, hw, c,
+                           make_fdiv(c), make_fdiv(hw), dy, accumulate, dx);
     DC_HIP(hipGetLastError());
     return DC_OK;
 }
