@@ -257,6 +257,8 @@ __global__ void maxpool_bwd_kernel(dc_pool_shape sh, int P, int Q, const float *
 // Float4 variants for c % 4 == 0: a thread owns one channel quad of one
 // output (forward) or input (backward) pixel, so the index arithmetic is
 // paid once per four channels and in 32 bits (the host checks the sizes).
+// The grid-stride step stays in 32 bits too: total4 < 2^29 and the grid has at
+// most 2^28 threads, so e + stride never passes INT_MAX.
 // Per channel they make exactly the decisions and sums of the scalar kernels.
 // Element e of the float4 output is decoded with multiply-high divisions by
 // the invariant c4, Q and P (fc4, fQ, fP), not integer divisions.
@@ -344,7 +346,9 @@ __global__ void maxpool_bwd4_kernel(dc_pool_shape sh, int P, int Q, int c4, int 
 // Average pooling over the window positions that lie inside the input (the
 // padded ones are not counted).  V channels per thread (4 when c % 4 == 0 and
 // the tensors are 16-byte aligned); the host keeps every element count below
-// 2^31.  Backward gathers, for each input element, dy / count of every
+// 2^31, so an element and its offsets fit in 32 bits, but the grid-stride step
+// is taken in 64 bits: near 2^31 elements e + stride would pass INT_MAX.
+// Backward gathers, for each input element, dy / count of every
 // window that contains it, in window order: deterministic, no atomics.
 __device__ __forceinline__ int pool_count(const dc_pool_shape &sh, int p, int q) {
     const int h0 = p * sh.stride - sh.pad, w0 = q * sh.stride - sh.pad;
@@ -358,7 +362,9 @@ __global__ void avgpool_fwd_kernel(dc_pool_shape sh, int P, int Q, int cv, int t
     using T = typename std::conditional<V == 4, float4, float>::type;
     const T *xv = reinterpret_cast<const T *>(x);
     T *yv = reinterpret_cast<T *>(y);
-    for (int e = blockIdx.x * blockDim.x + threadIdx.x; e < total; e += gridDim.x * blockDim.x) {
+    for (int64_t e64 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e64 < total;
+         e64 += (int64_t)gridDim.x * blockDim.x) {
+        const int e = (int)e64;
         const int pix = (int)fcv.div((uint32_t)e), qc = e - pix * cv;
         const int t = (int)fQ.div((uint32_t)pix), q = pix - t * Q;
         const int n = (int)fP.div((uint32_t)t), p = t - n * P;
@@ -393,7 +399,9 @@ __global__ void avgpool_bwd_kernel(dc_pool_shape sh, int P, int Q, int cv, int t
     using T = typename std::conditional<V == 4, float4, float>::type;
     const T *dv = reinterpret_cast<const T *>(dy);
     T *xv = reinterpret_cast<T *>(dx);
-    for (int e = blockIdx.x * blockDim.x + threadIdx.x; e < total; e += gridDim.x * blockDim.x) {
+    for (int64_t e64 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e64 < total;
+         e64 += (int64_t)gridDim.x * blockDim.x) {
+        const int e = (int)e64;
         const int pix = (int)fcv.div((uint32_t)e), qc = e - pix * cv;
         const int t = (int)fW.div((uint32_t)pix), w = pix - t * sh.w;
         const int n = (int)fH.div((uint32_t)t), h = t - n * sh.h;

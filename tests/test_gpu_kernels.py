@@ -450,6 +450,39 @@ def test_avgpool_rejects_bad_shapes():
     assert D.lib().dc_avgpool_forward(ctypes.byref(sh), None, None, stream()) == D.DC_OK
 
 
+def test_pooling_near_2g_elements():
+    """Largest pooling sizes: 1,996,920,000 elements (below the 2^31 limit, past
+    2^31 - 2^28, where a 32-bit grid-stride step would wrap), c = 3 so the
+    per-channel kernels run.  With 1 x 1 windows at stride 1 each output is its
+    one input tap divided by a count of 1, so average and max pooling are the
+    identity both ways, bit for bit: y = x, dx = dy, every argmax 0."""
+    t = __import__("torch")
+    n, h, w, c = 1, 25800, 25800, 3
+    total = n * h * w * c
+    assert 2 ** 31 - 2 ** 28 < total < 2 ** 31 - 1
+    print(f"pooling near 2^31: {total} elements", flush=True)
+    g = t.Generator(device="cuda").manual_seed(95)
+    x = t.rand(total, device="cuda", generator=g)
+    y = t.full((total,), float("nan"), device="cuda")
+    sh = D.PoolShape(n, h, w, c, 1, 1, 1, 0)
+    D.call("dc_avgpool_forward", ctypes.byref(sh), x.data_ptr(), y.data_ptr(), stream())
+    t.cuda.synchronize()
+    assert t.equal(x, y)
+    y.fill_(float("nan"))
+    D.call("dc_avgpool_backward", ctypes.byref(sh), x.data_ptr(), 0, y.data_ptr(), stream())
+    t.cuda.synchronize()
+    assert t.equal(x, y)
+    y.fill_(float("nan"))
+    arg = t.full((total,), 7, dtype=t.uint8, device="cuda")
+    D.call("dc_maxpool_forward", ctypes.byref(sh), x.data_ptr(), y.data_ptr(), arg.data_ptr(), stream())
+    t.cuda.synchronize()
+    assert t.equal(x, y) and int(arg.max()) == 0
+    y.fill_(float("nan"))
+    D.call("dc_maxpool_backward", ctypes.byref(sh), x.data_ptr(), arg.data_ptr(), 0, y.data_ptr(), stream())
+    t.cuda.synchronize()
+    assert t.equal(x, y)
+
+
 @pytest.mark.parametrize("cfg", [(3, 4, 4, 10), (128, 4, 4, 512), (64, 7, 7, 2048)])
 def test_gap(cfg):
     n, h, w, c = cfg
