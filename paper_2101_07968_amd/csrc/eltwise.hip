@@ -343,6 +343,50 @@ __global__ void maxpool_bwd4_kernel(dc_pool_shape sh, int P, int Q, int c4, int 
     }
 }
 
+// Backward of windows that tile the input exactly (stride = r = s, no padding,
+// P r = H, Q s = W): every input element lies in one window, so a thread owns
+// one output channel quad and writes its window's r x s input quads, dy where
+// the tap is the argmax (and, with MASK, the maximum is positive), zero
+// elsewhere.  The index arithmetic is paid once per output quad; each element
+// gets exactly the gather kernel's value (0 + dy, or the accumulated sum).
+template <bool MASK>
+__global__ void maxpool_bwd4_tiled_kernel(dc_pool_shape sh, int P, int Q, int c4, int total4, FDiv fc4, FDiv fQ,
+                                          FDiv fP, const float4 *__restrict__ dy, const uchar4 *__restrict__ arg,
+                                          int acc, float4 *__restrict__ dx, const float4 *__restrict__ y) {
+    for (int e = blockIdx.x * blockDim.x + threadIdx.x; e < total4; e += gridDim.x * blockDim.x) {
+        const int pix = (int)fc4.div((uint32_t)e);
+        const int q4 = e - pix * c4;
+        const int t = (int)fQ.div((uint32_t)pix);
+        const int q = pix - t * Q;
+        const int n = (int)fP.div((uint32_t)t);
+        const int p = t - n * P;
+        const uchar4 ar = arg[e];
+        const float4 d = dy[e];
+        const float4 ym = MASK ? y[e] : make_float4(1.f, 1.f, 1.f, 1.f);
+        for (int i = 0; i < sh.r; ++i) {
+            const int row = (n * sh.h + p * sh.r + i) * sh.w + q * sh.s;
+            for (int j = 0; j < sh.s; ++j) {
+                const int a = i * sh.s + j;
+                float4 g = make_float4(0.f, 0.f, 0.f, 0.f);
+                if (ar.x == a && ym.x > 0.f)
+                    g.x += d.x;
+                if (ar.y == a && ym.y > 0.f)
+                    g.y += d.y;
+                if (ar.z == a && ym.z > 0.f)
+                    g.z += d.z;
+                if (ar.w == a && ym.w > 0.f)
+                    g.w += d.w;
+                const int o = (row + j) * c4 + q4;
+                if (acc) {
+                    const float4 v = dx[o];
+                    g.x = v.x + g.x; g.y = v.y + g.y; g.z = v.z + g.z; g.w = v.w + g.w;
+                }
+                dx[o] = g;
+            }
+        }
+    }
+}
+
 // Average pooling over the window positions that lie inside the input (the
 // padded ones are not counted).  V channels per thread (4 when c % 4 == 0 and
 // the tensors are 16-byte aligned); the host keeps every element count below
@@ -1032,6 +1076,19 @@ int maxpool_backward(const dc_pool_shape &sh, const float *dy, const uint8_t *ar
         const auto *arg4 = reinterpret_cast<const uchar4 *>(arg);
         const auto *y4 = reinterpret_cast<const float4 *>(relu_y);
         auto *dx4 = reinterpret_cast<float4 *>(dx);
+        if (sh.pad == 0 && sh.stride == sh.r && sh.stride == sh.s && P * sh.r == sh.h && Q * sh.s == sh.w) {
+            // windows tile the input: one thread per output quad writes its window
+            const int out4 = (int)((int64_t)sh.n * P * Q * sh.c / 4);
+            const FDiv fc4 = make_fdiv(sh.c / 4), fQ = make_fdiv(Q), fP = make_fdiv(P);
+            if (relu_y)
+                hipLaunchKernelGGL(maxpool_bwd4_tiled_kernel<true>, dim3(ew_blocks(out4)), dim3(EW_THREADS), 0, s, sh,
+                                   P, Q, sh.c / 4, out4, fc4, fQ, fP, dy4, arg4, accumulate, dx4, y4);
+            else
+                hipLaunchKernelGGL(maxpool_bwd4_tiled_kernel<false>, dim3(ew_blocks(out4)), dim3(EW_THREADS), 0, s,
+                                   sh, P, Q, sh.c / 4, out4, fc4, fQ, fP, dy4, arg4, accumulate, dx4, y4);
+            DC_HIP(hipGetLastError());
+            return DC_OK;
+        }
         const FDiv fc4 = make_fdiv(sh.c / 4), fW = make_fdiv(sh.w), fH = make_fdiv(sh.h), fst = make_fdiv(sh.stride);
         if (relu_y)
             hipLaunchKernelGGL(maxpool_bwd4_kernel<true>, dim3(ew_blocks(total4)), dim3(EW_THREADS), 0, s, sh, P, Q,

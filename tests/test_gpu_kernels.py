@@ -388,7 +388,10 @@ def test_relu_add_copy(n, offset):
 
 
 POOLS = [(2, 8, 8, 5, 2, 2, 0), (3, 13, 13, 16, 3, 2, 0), (2, 12, 12, 7, 3, 2, 1), (32, 55, 55, 64, 3, 2, 0),
-         (64, 112, 112, 64, 3, 2, 1), (32, 224, 224, 64, 2, 2, 0), (2, 9, 9, 12, 3, 1, 1), (3, 14, 14, 4, 3, 2, 1)]
+         (64, 112, 112, 64, 3, 2, 1), (32, 224, 224, 64, 2, 2, 0), (2, 9, 9, 12, 3, 1, 1), (3, 14, 14, 4, 3, 2, 1),
+         # windows that tile the input (r = stride, no padding): the per-window backward kernel, also with
+         # c / 4 = 1 and 3 x 3 windows; an odd extent leaves a row uncovered and takes the gather kernel
+         (2, 12, 12, 8, 3, 3, 0), (4, 16, 16, 4, 2, 2, 0), (2, 9, 10, 8, 2, 2, 0)]
 
 
 @pytest.mark.parametrize("cfg", POOLS, ids=[str(p) for p in POOLS])
