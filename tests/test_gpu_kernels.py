@@ -419,6 +419,40 @@ def test_maxpool(cfg):
     assert rel_err(host(dxa), dx_ref + acc0) <= 1e-6
 
 
+POOLS_RELU = [p for p in POOLS if p[0] * p[1] * p[2] * p[3] < 100000]
+
+
+@pytest.mark.parametrize("cfg", POOLS_RELU, ids=[str(p) for p in POOLS_RELU])
+def test_maxpool_backward_relu(cfg):
+    """Max-pool backward with the ReLU before it folded in (dc_maxpool_backward_relu):
+    a window adds its dy only where its maximum, the pool's output, is positive.
+    Against the oracle's backward of dy masked by y > 0, plain and accumulating, on the
+    scalar, gather and per-window kernels; inputs shifted by -1 so that about a third
+    of the windows have a negative maximum."""
+    n, h, w, c, r, st, pad = cfg
+    x = (synth.random_tensor(21, (n, h, w, c)) - 1.0).astype(np.float32)
+    P, Q = out_hw(h, r, st, pad), out_hw(w, r, st, pad)
+    dy = synth.random_tensor(22, (n, P, Q, c))
+    sh = D.PoolShape(n, h, w, c, r, r, st, pad)
+    xd, dyd = dev(x), dev(dy)
+    y = zeros((n, P, Q, c))
+    arg = zeros((n, P, Q, c), "uint8")
+    D.call("dc_maxpool_forward", ctypes.byref(sh), xd.data_ptr(), y.data_ptr(), arg.data_ptr(), stream())
+    y_ref, arg_ref = OC.maxpool_forward(x, r, r, st, pad)
+    neg = float((y_ref <= 0).mean())
+    assert 0.05 < neg < 0.95, neg
+    dx_ref = OC.maxpool_backward(np.where(y_ref > 0, dy, 0.0), arg_ref, x.shape, r, r, st, pad)
+    dx = zeros((n, h, w, c))
+    D.call("dc_maxpool_backward_relu", ctypes.byref(sh), dyd.data_ptr(), arg.data_ptr(), y.data_ptr(), 0,
+           dx.data_ptr(), stream())
+    assert rel_err(host(dx), dx_ref) <= 1e-7
+    acc0 = synth.random_tensor(23, (n, h, w, c))
+    dxa = dev(acc0)
+    D.call("dc_maxpool_backward_relu", ctypes.byref(sh), dyd.data_ptr(), arg.data_ptr(), y.data_ptr(), 1,
+           dxa.data_ptr(), stream())
+    assert rel_err(host(dxa), dx_ref + acc0) <= 1e-6
+
+
 AVGPOOLS = [(2, 8, 8, 5, 3, 1, 1), (2, 9, 7, 12, 3, 1, 1), (3, 13, 13, 16, 3, 2, 1), (2, 12, 12, 7, 2, 2, 0),
             (32, 35, 35, 384, 3, 1, 1), (32, 17, 17, 1024, 3, 1, 1), (32, 8, 8, 1536, 3, 1, 1),
             (2, 11, 10, 6, 5, 3, 2), (1, 1, 1, 4, 3, 1, 1)]
