@@ -630,3 +630,51 @@ def test_concat(cfg):
         np.testing.assert_array_equal(host(dx), (acc0 + dy[:, off:off + c]).astype(np.float32))
         off += c
     assert D.lib().dc_concat_forward(rows, parts[0], cout, cout, None, None, None) == D.DC_EINVAL
+
+
+@pytest.mark.parametrize("cfg", [(10, (4, 8, 12, 4)), (7, (3, 5, 2)), (32 * 28 * 28, (64, 128, 32, 32))])
+def test_concat_backward_relu(cfg):
+    """The concatenation's backward with the ReLU that produced a part folded in:
+    dx (+)= dy's slice where the ReLU's output is positive, bit for bit, written and
+    accumulated, on the float4 and per-channel kernels."""
+    rows, parts = cfg
+    cout = sum(parts)
+    dy = synth.random_tensor(60, (rows, cout))
+    dyd = dev(dy)
+    off = 0
+    for i, c in enumerate(parts):
+        relu_y = np.maximum(synth.random_tensor(61 + i, (rows, c)), 0.0).astype(np.float32)
+        g = np.where(relu_y > 0, dy[:, off:off + c], np.float32(0.0)).astype(np.float32)
+        yd = dev(relu_y)
+        dx = zeros((rows, c))
+        D.call("dc_concat_backward_relu", rows, c, cout, off, dyd.data_ptr(), yd.data_ptr(), 0, dx.data_ptr(),
+               stream())
+        np.testing.assert_array_equal(host(dx), g)
+        acc0 = synth.random_tensor(70 + i, (rows, c))
+        dxa = dev(acc0)
+        D.call("dc_concat_backward_relu", rows, c, cout, off, dyd.data_ptr(), yd.data_ptr(), 1, dxa.data_ptr(),
+               stream())
+        np.testing.assert_array_equal(host(dxa), (acc0 + g).astype(np.float32))
+        off += c
+
+
+@pytest.mark.parametrize("n", [1, 7, 4096 + 3, 32 * 56 * 56 * 64])
+def test_add_relu_backward(n):
+    """Backward of relu(a + b): m = dy where y > 0, written to one input's gradient
+    and accumulated into the other's (and the reverse), or to one of them alone,
+    bit for bit, on the float4 body and the scalar tail."""
+    dy = synth.random_tensor(80, (n,))
+    y = np.maximum(synth.random_tensor(81, (n,)), 0.0).astype(np.float32)
+    m = np.where(y > 0, dy, np.float32(0.0)).astype(np.float32)
+    acc = synth.random_tensor(82, (n,))
+    dyd, yd = dev(dy), dev(y)
+    for acc0, acc1 in ((0, 1), (1, 0)):
+        d0 = dev(acc) if acc0 else zeros((n,))
+        d1 = dev(acc) if acc1 else zeros((n,))
+        D.call("dc_add_relu_backward", dyd.data_ptr(), yd.data_ptr(), acc0, d0.data_ptr(), acc1, d1.data_ptr(), n,
+               stream())
+        np.testing.assert_array_equal(host(d0), (acc + m).astype(np.float32) if acc0 else m)
+        np.testing.assert_array_equal(host(d1), (acc + m).astype(np.float32) if acc1 else m)
+    d0 = dev(acc)
+    D.call("dc_add_relu_backward", dyd.data_ptr(), yd.data_ptr(), 1, d0.data_ptr(), 0, None, n, stream())
+    np.testing.assert_array_equal(host(d0), (acc + m).astype(np.float32))
